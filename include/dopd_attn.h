@@ -1,0 +1,173 @@
+/*
+ * dopd_attn.h -- C ABI of the MI355X (gfx950) attention hot path inside the
+ * prefill (P) and decode (D) instances of a prefill/decode-disaggregated LLM
+ * server.
+ *
+ * The operation is attention as defined by Eq. 1 of the paper,
+ *     out = softmax(scale * Q K^T) V,
+ * with the softmax scale as an argument (Eq. 1 prints no scale; callers
+ * normally pass 1/sqrt(head_dim)).  A P-instance runs a variable-length causal
+ * prefill over a batch of prompts (the per-request input lengths of the
+ * length-aware batching of Sec. III-C, Alg. 1) and writes K/V into a paged
+ * cache (the KV-cache blocks of Sec. I and Sec. IV-C); a D-instance runs
+ * single-query attention over each request's cached context (decode is
+ * memory bound, Sec. III-B, Eq. 12); a prefill-completed request is handed to
+ * a D-instance together with its KV cache (Sec. III-B, Sec. IV-C), for which
+ * the packer gathers the request's pages into one contiguous buffer.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * - Pointers are DEVICE pointers unless the parameter name ends in "_host".
+ *   The caller owns every buffer; the library never allocates or frees
+ *   device memory and keeps no state between calls (re-entrant).
+ * - `stream` is a hipStream_t passed as void* (NULL = default stream).  Every
+ *   call only enqueues work on that stream; nothing synchronises.
+ * - Element types: DOPD_BF16 (bf16 storage, fp32 accumulation, outputs
+ *   rounded to nearest even) or DOPD_FP32 (fp32 throughout).
+ * - Fresh tokens are token-major: Q/out [T][Hq][d], K/V [T][Hkv][d].
+ * - GQA: query head h uses KV head h / (Hq / Hkv); Hq % Hkv must be 0.
+ * - Paged cache (one pool per layer, page_size = 16 tokens):
+ *       k_pool[num_pages][Hkv][16][d]   (token-major inside a page)
+ *       v_pool[num_pages][Hkv][d][16]   (dim-major inside a page)
+ *   page_table[r * page_table_stride + i] is the physical page of logical
+ *   page i (tokens 16i .. 16i+15) of request r.  Device-resident page ids are
+ *   trusted on the hot path: entries a call reads must lie in
+ *   [0, num_pages).  dopd_validate_page_table_host() checks a host copy.
+ * - Errors are returned as dopd_status codes; nothing is thrown across the
+ *   ABI.  Host-side argument checks run before any HIP call, so an invalid
+ *   call touches no device.  DOPD_ERR_HIP means a HIP launch failed; its code
+ *   is available from dopd_last_hip_error() on the calling thread.
+ */
+#ifndef DOPD_ATTN_H
+#define DOPD_ATTN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t dopd_status;
+enum {
+  DOPD_OK = 0,
+  DOPD_ERR_NULL_POINTER = 1,       /* a required pointer is NULL                 */
+  DOPD_ERR_INVALID_SHAPE = 2,      /* counts, lengths or head ratio out of range */
+  DOPD_ERR_UNSUPPORTED = 3,        /* dtype / head_dim / page_size not built     */
+  DOPD_ERR_WORKSPACE_TOO_SMALL = 4,
+  DOPD_ERR_HIP = 5
+};
+
+enum { DOPD_BF16 = 0, DOPD_FP32 = 1 };
+
+typedef struct {
+  int32_t num_q_heads;   /* Hq                                   */
+  int32_t num_kv_heads;  /* Hkv, divides Hq                      */
+  int32_t head_dim;      /* d: 64 or 128                         */
+  int32_t page_size;     /* tokens per cache page: 16            */
+  int32_t dtype;         /* DOPD_BF16 or DOPD_FP32               */
+  float softmax_scale;   /* multiplies Q.K before the softmax    */
+} dopd_attn_shape;
+
+/*
+ * Variable-length causal prefill attention (Eq. 1 over each prompt, causal,
+ * no prefix: token i of a request attends to tokens 0..i of the same request).
+ *   q[T][Hq][d], k/v[T][Hkv][d], out[T][Hq][d]; T = cu_seqlens_host[num_reqs].
+ *   cu_seqlens[num_reqs+1]: request r owns rows [cu[r], cu[r+1]); cu[0] = 0,
+ *     non-decreasing (an empty request is allowed and produces nothing).
+ *   cu_seqlens_host: identical host copy, used to size and order the launch
+ *     (longest work first); it must equal the device copy.
+ *   lse (nullable): fp32 [T][Hq], natural-log log-sum-exp of each row's
+ *     scaled scores.
+ * bf16: Q.K and P.V run on bf16 MFMA with fp32 accumulation, P is rounded to
+ * bf16 before the P.V product.  fp32: plain fp32 arithmetic.
+ */
+dopd_status dopd_prefill_attn(const dopd_attn_shape* shape, const void* q, const void* k,
+                              const void* v, void* out, float* lse, const int32_t* cu_seqlens,
+                              const int32_t* cu_seqlens_host, int32_t num_reqs, void* stream);
+
+/*
+ * Paged KV write: request r appends n_r = cu_new_tokens[r+1] - cu_new_tokens[r]
+ * tokens at logical positions start_pos[r] .. start_pos[r] + n_r - 1, taken
+ * from rows cu_new_tokens[r] .. of k_new/v_new[total_new_tokens][Hkv][d].
+ * Position p goes to page page_table[r*stride + p/16], slot p % 16.  Pure bit
+ * copy; every other slot of the pools is left untouched.  Prefill writes use
+ * start_pos = 0; a decode step appends at start_pos = context_len - 1.
+ *   cu_new_tokens[num_reqs+1], start_pos[num_reqs] are device arrays;
+ *   total_new_tokens = cu_new_tokens[num_reqs] (host value, sizes the launch).
+ */
+dopd_status dopd_kv_write(const dopd_attn_shape* shape, const void* k_new, const void* v_new,
+                          void* k_pool, void* v_pool, int32_t num_pages,
+                          const int32_t* page_table, int32_t page_table_stride,
+                          const int32_t* cu_new_tokens, const int32_t* start_pos,
+                          int32_t num_reqs, int32_t total_new_tokens, void* stream);
+
+/*
+ * Paged single-query decode attention: for request r with context_lens[r]
+ * cached tokens (counting the current one, whose K/V must already be in the
+ * cache) and every query head h,
+ *   out[r][h] = softmax_j(scale * q[r][h] . K_j) V_j,  j < context_lens[r].
+ *   q/out [num_reqs][Hq][d]; lse (nullable) fp32 [num_reqs][Hq].
+ *   context_lens_host: identical host copy (>= 1 each), used to size the
+ *     launch and the key-range split.
+ *   split_tokens: keys per split-K work item, 0 = automatic, else a positive
+ *     multiple of 32.  The result does not depend on it beyond rounding.
+ *   workspace: device memory of at least dopd_decode_workspace_size() bytes
+ *     for the same arguments.  Its first 256-byte-aligned counter region must
+ *     be zero when the workspace is first used (allocate it zeroed); every
+ *     completed call leaves it zero again.  Calls that overlap in time must
+ *     not share a workspace.
+ * bf16 path: one kernel; each work item (request, KV head, key split) reads
+ * its pages once for all Hq/Hkv query heads of the group (at most 16), and
+ * the last item of a request to finish merges the split partials exactly
+ * (log-sum-exp rescaling).
+ */
+dopd_status dopd_decode_attn(const dopd_attn_shape* shape, const void* q, const void* k_pool,
+                             const void* v_pool, int32_t num_pages, const int32_t* page_table,
+                             int32_t page_table_stride, const int32_t* context_lens,
+                             const int32_t* context_lens_host, int32_t num_reqs,
+                             int32_t split_tokens, void* out, float* lse, void* workspace,
+                             size_t workspace_bytes, void* stream);
+
+/* Workspace bytes dopd_decode_attn needs for these arguments (0 on bad input). */
+size_t dopd_decode_workspace_size(const dopd_attn_shape* shape,
+                                  const int32_t* context_lens_host, int32_t num_reqs,
+                                  int32_t split_tokens);
+
+/*
+ * Handoff pack of prefill-completed requests (the KV blocks that the
+ * Connector moves from a P-instance to a D-instance, Sec. IV-C): handoff n
+ * (request req_ids[n], seq_lens[n] cached tokens) is written to
+ *   out[out_offsets[n] + (((layer*2 + c)*Hkv + h)*len + t)*d + e]
+ * with c = 0 for K and 1 for V, i.e. (layer, K/V, head, token, dim) order.
+ *   k_pool/v_pool carry a leading layer dimension: [num_layers][num_pages]...
+ *   req_ids, seq_lens [num_handoff], out_offsets [num_handoff+1] (int64
+ *   element offsets) are device arrays; seq_lens_host is a host copy that
+ *   sizes the launch.  Tail slots of a request's last page are not copied.
+ */
+dopd_status dopd_kv_pack_for_handoff(const dopd_attn_shape* shape, int32_t num_layers,
+                                     const void* k_pool, const void* v_pool, int32_t num_pages,
+                                     const int32_t* page_table, int32_t page_table_stride,
+                                     const int32_t* req_ids, const int32_t* seq_lens,
+                                     const int32_t* seq_lens_host, const int64_t* out_offsets,
+                                     int32_t num_handoff, void* out, void* stream);
+
+/*
+ * Host check of a page table copy: for each request r, the entries
+ * page_table_host[r*stride + i], i < ceil(lens_host[r]/16), must lie in
+ * [0, num_pages).  Returns DOPD_OK or DOPD_ERR_INVALID_SHAPE.
+ */
+dopd_status dopd_validate_page_table_host(const int32_t* page_table_host,
+                                          int32_t page_table_stride, int32_t num_reqs,
+                                          const int32_t* lens_host, int32_t num_pages);
+
+/* Static description of a status code. */
+const char* dopd_status_string(dopd_status status);
+
+/* hipError_t of the last DOPD_ERR_HIP on the calling thread (0 if none). */
+int32_t dopd_last_hip_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* DOPD_ATTN_H */

@@ -1,0 +1,319 @@
+// C ABI of the gfx950 attention hot path (declarations and contracts in
+// include/dopd_attn.h).  Host side: argument validation before any HIP call,
+// launch planning from the host copies of the lengths, launches on the
+// caller's stream.  No allocation, no synchronisation, no state.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdint>
+#include <cstring>
+
+#include "dopd_attn.h"
+#include "kernels/attn_f32.hpp"
+#include "kernels/common.hpp"
+#include "kernels/decode_bf16.hpp"
+#include "kernels/kv_pack.hpp"
+#include "kernels/kv_write.hpp"
+#include "kernels/prefill_bf16.hpp"
+
+namespace {
+
+thread_local int32_t g_last_hip_error = 0;
+
+dopd_status hip_status(hipError_t e) {
+  if (e == hipSuccess) return DOPD_OK;
+  g_last_hip_error = (int32_t)e;
+  return DOPD_ERR_HIP;
+}
+
+dopd_status launch_status() { return hip_status(hipGetLastError()); }
+
+hipStream_t as_stream(void* s) { return reinterpret_cast<hipStream_t>(s); }
+
+// Checks the parts of the shape every entry point relies on.
+dopd_status check_shape(const dopd_attn_shape* s) {
+  if (!s) return DOPD_ERR_NULL_POINTER;
+  if (s->num_q_heads <= 0 || s->num_kv_heads <= 0 || s->num_q_heads % s->num_kv_heads != 0)
+    return DOPD_ERR_INVALID_SHAPE;
+  if (s->head_dim != 64 && s->head_dim != 128) return DOPD_ERR_UNSUPPORTED;
+  if (s->page_size != dopd::kPage) return DOPD_ERR_UNSUPPORTED;
+  if (s->dtype != DOPD_BF16 && s->dtype != DOPD_FP32) return DOPD_ERR_UNSUPPORTED;
+  return DOPD_OK;
+}
+
+
+// ---- decode planning --------------------------------------------------------
+constexpr int kMaxGroupBf16 = 16;   // query heads per KV head handled by one decode wave
+constexpr int kAutoSplitMax = 512;
+constexpr int kAutoSplitMin = 64;
+constexpr int64_t kTargetItems = 8192;  // ~4 waves per SIMD slot of the 256 CUs
+
+int64_t decode_items(const int32_t* ctx, int32_t n, int split, int hkv) {
+  int64_t items = 0;
+  for (int32_t r = 0; r < n; ++r) items += (int64_t)((ctx[r] + split - 1) / split) * hkv;
+  return items;
+}
+
+int choose_split(const int32_t* ctx, int32_t n, int hkv, int32_t requested) {
+  if (requested > 0) return requested;
+  int split = kAutoSplitMax;
+  while (split > kAutoSplitMin && decode_items(ctx, n, split, hkv) < kTargetItems) split /= 2;
+  return split;
+}
+
+struct DecodeLayout {
+  size_t counters_off, counters_bytes, part_o_off, part_ml_off, total;
+};
+
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+DecodeLayout decode_layout(const dopd_attn_shape* s, const int32_t* ctx, int32_t n, int split) {
+  DecodeLayout L{};
+  const int g = s->num_q_heads / s->num_kv_heads;
+  const int64_t items = decode_items(ctx, n, split, s->num_kv_heads);
+  L.counters_off = 0;
+  L.counters_bytes = align256((size_t)n * s->num_kv_heads * sizeof(int));
+  L.part_o_off = L.counters_bytes;
+  L.part_ml_off = L.part_o_off + align256((size_t)items * g * s->head_dim * sizeof(float));
+  L.total = L.part_ml_off + align256((size_t)items * g * 2 * sizeof(float));
+  return L;
+}
+
+dopd_status check_decode_host(const dopd_attn_shape* s, const int32_t* ctx_host, int32_t n,
+                              int32_t split) {
+  dopd_status st = check_shape(s);
+  if (st != DOPD_OK) return st;
+  if (n < 0) return DOPD_ERR_INVALID_SHAPE;
+  if (n > 0 && !ctx_host) return DOPD_ERR_NULL_POINTER;
+  for (int32_t r = 0; r < n; ++r)
+    if (ctx_host[r] < 1) return DOPD_ERR_INVALID_SHAPE;
+  if (split < 0 || (split > 0 && split % 32 != 0)) return DOPD_ERR_INVALID_SHAPE;
+  if (s->dtype == DOPD_BF16 && s->num_q_heads / s->num_kv_heads > kMaxGroupBf16)
+    return DOPD_ERR_UNSUPPORTED;
+  return DOPD_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* dopd_status_string(dopd_status status) {
+  switch (status) {
+    case DOPD_OK: return "ok";
+    case DOPD_ERR_NULL_POINTER: return "null pointer argument";
+    case DOPD_ERR_INVALID_SHAPE: return "invalid shape, count or length";
+    case DOPD_ERR_UNSUPPORTED: return "unsupported dtype, head_dim, page_size or head ratio";
+    case DOPD_ERR_WORKSPACE_TOO_SMALL: return "workspace too small";
+    case DOPD_ERR_HIP: return "HIP launch error";
+    default: return "unknown status";
+  }
+}
+
+int32_t dopd_last_hip_error(void) { return g_last_hip_error; }
+
+dopd_status dopd_validate_page_table_host(const int32_t* pt, int32_t stride, int32_t n,
+                                          const int32_t* lens, int32_t num_pages) {
+  if (n < 0 || num_pages < 0) return DOPD_ERR_INVALID_SHAPE;
+  if (n == 0) return DOPD_OK;
+  if (!pt || !lens) return DOPD_ERR_NULL_POINTER;
+  for (int32_t r = 0; r < n; ++r) {
+    if (lens[r] < 0) return DOPD_ERR_INVALID_SHAPE;
+    const int64_t need = ((int64_t)lens[r] + dopd::kPage - 1) / dopd::kPage;
+    if (need > stride) return DOPD_ERR_INVALID_SHAPE;
+    for (int64_t i = 0; i < need; ++i) {
+      const int32_t p = pt[(int64_t)r * stride + i];
+      if (p < 0 || p >= num_pages) return DOPD_ERR_INVALID_SHAPE;
+    }
+  }
+  return DOPD_OK;
+}
+
+// ---------------------------------------------------------------- prefill
+dopd_status dopd_prefill_attn(const dopd_attn_shape* s, const void* q, const void* k,
+                              const void* v, void* out, float* lse, const int32_t* cu,
+                              const int32_t* cu_host, int32_t nreq, void* stream) {
+  dopd_status st = check_shape(s);
+  if (st != DOPD_OK) return st;
+  if (nreq < 0) return DOPD_ERR_INVALID_SHAPE;
+  if (nreq == 0) return DOPD_OK;
+  if (!q || !k || !v || !out || !cu || !cu_host) return DOPD_ERR_NULL_POINTER;
+  if (cu_host[0] != 0) return DOPD_ERR_INVALID_SHAPE;
+  int max_len = 0;
+  int64_t bf16_items = 0;
+  for (int32_t r = 0; r < nreq; ++r) {
+    const int len = cu_host[r + 1] - cu_host[r];
+    if (len < 0) return DOPD_ERR_INVALID_SHAPE;
+    max_len = std::max(max_len, len);
+    bf16_items += (len + dopd::kPfBM - 1) / dopd::kPfBM;
+  }
+  const int64_t T = cu_host[nreq];
+  if (T == 0) return DOPD_OK;
+  const int hq = s->num_q_heads, hkv = s->num_kv_heads, d = s->head_dim;
+  hipStream_t strm = as_stream(stream);
+  if (s->dtype == DOPD_FP32) {
+    dim3 grid((unsigned)T, (unsigned)hq);
+    if (d == 64)
+      hipLaunchKernelGGL(dopd::prefill_f32_kernel<64>, grid, dim3(64), 0, strm, (const float*)q,
+                         (const float*)k, (const float*)v, (float*)out, lse, cu, nreq, hq, hkv,
+                         s->softmax_scale);
+    else
+      hipLaunchKernelGGL(dopd::prefill_f32_kernel<128>, grid, dim3(64), 0, strm, (const float*)q,
+                         (const float*)k, (const float*)v, (float*)out, lse, cu, nreq, hq, hkv,
+                         s->softmax_scale);
+    return launch_status();
+  }
+  dopd::PrefillArgs a;
+  a.q = (const uint16_t*)q;
+  a.k = (const uint16_t*)k;
+  a.v = (const uint16_t*)v;
+  a.out = (uint16_t*)out;
+  a.lse = lse;
+  a.cu = cu;
+  a.nreq = nreq;
+  a.hq = hq;
+  a.hkv = hkv;
+  a.max_tiles = (max_len + dopd::kPfBM - 1) / dopd::kPfBM;
+  a.scale_log2 = s->softmax_scale * dopd::kLog2e;
+  const int64_t blocks = bf16_items * hq;
+  if (blocks > INT32_MAX) return DOPD_ERR_INVALID_SHAPE;
+  if (d == 64)
+    hipLaunchKernelGGL(dopd::prefill_bf16_kernel<64>, dim3((unsigned)blocks), dim3(256), 0, strm, a);
+  else
+    hipLaunchKernelGGL(dopd::prefill_bf16_kernel<128>, dim3((unsigned)blocks), dim3(256), 0, strm, a);
+  return launch_status();
+}
+
+// ---------------------------------------------------------------- kv write
+dopd_status dopd_kv_write(const dopd_attn_shape* s, const void* k_new, const void* v_new,
+                          void* k_pool, void* v_pool, int32_t num_pages, const int32_t* pt,
+                          int32_t pt_stride, const int32_t* cu_new, const int32_t* start_pos,
+                          int32_t nreq, int32_t total_new, void* stream) {
+  dopd_status st = check_shape(s);
+  if (st != DOPD_OK) return st;
+  if (nreq < 0 || total_new < 0 || num_pages < 0 || pt_stride < 0) return DOPD_ERR_INVALID_SHAPE;
+  if (nreq == 0 || total_new == 0) return DOPD_OK;
+  if (!k_new || !v_new || !k_pool || !v_pool || !pt || !cu_new || !start_pos)
+    return DOPD_ERR_NULL_POINTER;
+  // Touched pages per request <= n/16 + 2, so this bounds the item count.
+  const int64_t blocks = (int64_t)total_new / dopd::kPage + 2 * (int64_t)nreq + 1;
+  if (blocks > INT32_MAX) return DOPD_ERR_INVALID_SHAPE;
+  hipStream_t strm = as_stream(stream);
+  const int hkv = s->num_kv_heads, d = s->head_dim;
+  if (s->dtype == DOPD_BF16)
+    hipLaunchKernelGGL(dopd::kv_write_kernel<uint16_t>, dim3((unsigned)blocks), dim3(256), 0, strm,
+                       (const uint16_t*)k_new, (const uint16_t*)v_new, (uint16_t*)k_pool,
+                       (uint16_t*)v_pool, pt, pt_stride, cu_new, start_pos, nreq, hkv, d);
+  else
+    hipLaunchKernelGGL(dopd::kv_write_kernel<uint32_t>, dim3((unsigned)blocks), dim3(256), 0, strm,
+                       (const uint32_t*)k_new, (const uint32_t*)v_new, (uint32_t*)k_pool,
+                       (uint32_t*)v_pool, pt, pt_stride, cu_new, start_pos, nreq, hkv, d);
+  return launch_status();
+}
+
+// ---------------------------------------------------------------- decode
+size_t dopd_decode_workspace_size(const dopd_attn_shape* s, const int32_t* ctx_host, int32_t n,
+                                  int32_t split_tokens) {
+  if (check_decode_host(s, ctx_host, n, split_tokens) != DOPD_OK) return 0;
+  if (n == 0 || s->dtype != DOPD_BF16) return 256;
+  const int split = choose_split(ctx_host, n, s->num_kv_heads, split_tokens);
+  return decode_layout(s, ctx_host, n, split).total;
+}
+
+dopd_status dopd_decode_attn(const dopd_attn_shape* s, const void* q, const void* k_pool,
+                             const void* v_pool, int32_t num_pages, const int32_t* pt,
+                             int32_t pt_stride, const int32_t* ctx, const int32_t* ctx_host,
+                             int32_t nreq, int32_t split_tokens, void* out, float* lse,
+                             void* workspace, size_t workspace_bytes, void* stream) {
+  dopd_status st = check_decode_host(s, ctx_host, nreq, split_tokens);
+  if (st != DOPD_OK) return st;
+  if (num_pages < 0 || pt_stride < 0) return DOPD_ERR_INVALID_SHAPE;
+  if (nreq == 0) return DOPD_OK;
+  if (!q || !k_pool || !v_pool || !pt || !ctx || !out) return DOPD_ERR_NULL_POINTER;
+  for (int32_t r = 0; r < nreq; ++r)
+    if ((int64_t)(ctx_host[r] + dopd::kPage - 1) / dopd::kPage > pt_stride)
+      return DOPD_ERR_INVALID_SHAPE;
+  const int hq = s->num_q_heads, hkv = s->num_kv_heads, d = s->head_dim;
+  hipStream_t strm = as_stream(stream);
+  if (s->dtype == DOPD_FP32) {
+    dim3 grid((unsigned)nreq, (unsigned)hq);
+    if (d == 64)
+      hipLaunchKernelGGL(dopd::decode_f32_kernel<64>, grid, dim3(64), 0, strm, (const float*)q,
+                         (const float*)k_pool, (const float*)v_pool, pt, pt_stride, ctx, hq, hkv,
+                         s->softmax_scale, (float*)out, lse);
+    else
+      hipLaunchKernelGGL(dopd::decode_f32_kernel<128>, grid, dim3(64), 0, strm, (const float*)q,
+                         (const float*)k_pool, (const float*)v_pool, pt, pt_stride, ctx, hq, hkv,
+                         s->softmax_scale, (float*)out, lse);
+    return launch_status();
+  }
+  const int split = choose_split(ctx_host, nreq, hkv, split_tokens);
+  const DecodeLayout L = decode_layout(s, ctx_host, nreq, split);
+  if (!workspace) return DOPD_ERR_NULL_POINTER;
+  if (workspace_bytes < L.total) return DOPD_ERR_WORKSPACE_TOO_SMALL;
+  if ((reinterpret_cast<uintptr_t>(workspace) & 255) != 0) return DOPD_ERR_INVALID_SHAPE;
+  const int64_t items = decode_items(ctx_host, nreq, split, hkv);
+  if (items > INT32_MAX) return DOPD_ERR_INVALID_SHAPE;
+  char* ws = static_cast<char*>(workspace);
+  dopd::DecodeArgs a;
+  a.q = (const uint16_t*)q;
+  a.k_pool = (const uint16_t*)k_pool;
+  a.v_pool = (const uint16_t*)v_pool;
+  a.page_table = pt;
+  a.ctx_lens = ctx;
+  a.out = (uint16_t*)out;
+  a.lse = lse;
+  a.counters = reinterpret_cast<int*>(ws + L.counters_off);
+  a.part_o = reinterpret_cast<float*>(ws + L.part_o_off);
+  a.part_ml = reinterpret_cast<float*>(ws + L.part_ml_off);
+  a.pt_stride = pt_stride;
+  a.nreq = nreq;
+  a.hq = hq;
+  a.hkv = hkv;
+  a.split = split;
+  a.scale_log2 = s->softmax_scale * dopd::kLog2e;
+  if (d == 64)
+    hipLaunchKernelGGL(dopd::decode_bf16_kernel<64>, dim3((unsigned)items), dim3(64), 0, strm, a);
+  else
+    hipLaunchKernelGGL(dopd::decode_bf16_kernel<128>, dim3((unsigned)items), dim3(64), 0, strm, a);
+  return launch_status();
+}
+
+// ---------------------------------------------------------------- handoff pack
+dopd_status dopd_kv_pack_for_handoff(const dopd_attn_shape* s, int32_t num_layers,
+                                     const void* k_pool, const void* v_pool, int32_t num_pages,
+                                     const int32_t* pt, int32_t pt_stride, const int32_t* req_ids,
+                                     const int32_t* seq_lens, const int32_t* seq_lens_host,
+                                     const int64_t* out_offsets, int32_t num_handoff, void* out,
+                                     void* stream) {
+  dopd_status st = check_shape(s);
+  if (st != DOPD_OK) return st;
+  if (num_layers < 1 || num_pages < 0 || pt_stride < 0 || num_handoff < 0)
+    return DOPD_ERR_INVALID_SHAPE;
+  if (num_handoff == 0) return DOPD_OK;
+  if (!k_pool || !v_pool || !pt || !req_ids || !seq_lens || !seq_lens_host || !out_offsets || !out)
+    return DOPD_ERR_NULL_POINTER;
+  int max_len = 0;
+  for (int32_t n = 0; n < num_handoff; ++n) {
+    if (seq_lens_host[n] < 0) return DOPD_ERR_INVALID_SHAPE;
+    if ((int64_t)(seq_lens_host[n] + dopd::kPage - 1) / dopd::kPage > pt_stride)
+      return DOPD_ERR_INVALID_SHAPE;
+    max_len = std::max(max_len, seq_lens_host[n]);
+  }
+  if (max_len == 0) return DOPD_OK;
+  const int64_t zdim = (int64_t)num_layers * 2 * s->num_kv_heads;
+  if (zdim > 65535 || num_handoff > 65535) return DOPD_ERR_INVALID_SHAPE;
+  dim3 grid((unsigned)((max_len + dopd::kPage - 1) / dopd::kPage), (unsigned)num_handoff,
+            (unsigned)zdim);
+  hipStream_t strm = as_stream(stream);
+  if (s->dtype == DOPD_BF16)
+    hipLaunchKernelGGL(dopd::kv_pack_kernel<uint16_t>, grid, dim3(256), 0, strm,
+                       (const uint16_t*)k_pool, (const uint16_t*)v_pool, num_pages, pt, pt_stride,
+                       req_ids, seq_lens, out_offsets, s->num_kv_heads, s->head_dim, (uint16_t*)out);
+  else
+    hipLaunchKernelGGL(dopd::kv_pack_kernel<uint32_t>, grid, dim3(256), 0, strm,
+                       (const uint32_t*)k_pool, (const uint32_t*)v_pool, num_pages, pt, pt_stride,
+                       req_ids, seq_lens, out_offsets, s->num_kv_heads, s->head_dim, (uint32_t*)out);
+  return launch_status();
+}
+
+}  // extern "C"

@@ -1,0 +1,72 @@
+// Shared device helpers for the gfx950 attention kernels.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace dopd {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+constexpr int kPage = 16;        // tokens per cache page
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.6931471805599453f;
+
+__device__ __forceinline__ float bf16_bits_to_f32(uint32_t b) { return __uint_as_float(b << 16); }
+
+// fp32 -> bf16 bits, round to nearest even; NaN stays a quiet NaN.
+__device__ __forceinline__ uint32_t f32_to_bf16_bits(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return 0x7fc0u;
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return u >> 16;
+}
+
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  return f32_to_bf16_bits(lo) | (f32_to_bf16_bits(hi) << 16);
+}
+
+__device__ __forceinline__ int lane_id() { return __lane_id(); }
+
+// Wave-wide inclusive prefix sum (wave64).
+__device__ __forceinline__ int wave_inclusive_scan(int x) {
+  const int l = lane_id();
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    int y = __shfl_up(x, o, 64);
+    if (l >= o) x += y;
+  }
+  return x;
+}
+
+// Locates the owner of global item `idx` when request r owns count(r) items,
+// laid out request after request.  Every lane of the wave gets the same answer.
+// Returns false when idx is past the last item.
+template <class CountFn>
+__device__ __forceinline__ bool find_owner(int idx, int nreq, CountFn count, int& owner,
+                                           int& local) {
+  const int l = lane_id();
+  int base = 0;
+  for (int r0 = 0; r0 < nreq; r0 += 64) {
+    const int r = r0 + l;
+    const int c = (r < nreq) ? count(r) : 0;
+    const int incl = wave_inclusive_scan(c);
+    const int total = __shfl(incl, 63, 64);
+    if (idx < base + total) {
+      const unsigned long long hit = __ballot(idx - base < incl);
+      const int ol = __ffsll((long long)hit) - 1;
+      const int excl = __shfl(incl - c, ol, 64);
+      owner = r0 + ol;
+      local = idx - base - excl;
+      return true;
+    }
+    base += total;
+  }
+  return false;
+}
+
+}  // namespace dopd

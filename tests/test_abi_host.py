@@ -1,0 +1,129 @@
+"""C ABI checks that need no GPU: the library loads, exports every symbol the
+header declares, and rejects invalid arguments on the host before any HIP
+call (pointers passed here are never dereferenced)."""
+import ctypes as C
+import os
+import re
+
+import numpy as np
+import pytest
+
+from paper_2511_20982_amd import attn as A
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "dopd_attn.h")
+FAKE = 0x1000  # a non-null device address; host validation fails before it is used
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(A.LIB_PATH):
+        from paper_2511_20982_amd import build
+        build.build()
+    return A.lib()
+
+
+def declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(dopd_[a-z_0-9]+)\s*\(", src)))
+
+
+def test_every_declared_symbol_is_exported(lib):
+    names = declared_functions()
+    assert set(names) == set(A.EXPORTS)
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_status_strings(lib):
+    for s in range(6):
+        assert A.status_string(s)
+    assert A.status_string(99) == "unknown status"
+    assert lib.dopd_last_hip_error() == 0
+
+
+def _shape(hq=8, hkv=2, d=128, dtype="bf16", page=16):
+    return A.make_shape(hq, hkv, d, dtype, page_size=page)
+
+
+def _prefill(lib, shape, cu_host, ptrs=FAKE, nreq=None):
+    cu = np.asarray(cu_host, np.int32)
+    n = len(cu) - 1 if nreq is None else nreq
+    p = C.c_void_p(ptrs) if ptrs else None
+    return lib.dopd_prefill_attn(C.byref(shape), p, p, p, p, None, p, A._hptr(cu), n, None)
+
+
+def test_prefill_host_validation(lib):
+    assert _prefill(lib, _shape(hq=6, hkv=4), [0, 4]) == A.DOPD_ERR_INVALID_SHAPE
+    assert _prefill(lib, _shape(d=96), [0, 4]) == A.DOPD_ERR_UNSUPPORTED
+    assert _prefill(lib, _shape(page=32), [0, 4]) == A.DOPD_ERR_UNSUPPORTED
+    assert _prefill(lib, _shape(), [0, 4], ptrs=0) == A.DOPD_ERR_NULL_POINTER
+    assert _prefill(lib, _shape(), [0, 4, 2]) == A.DOPD_ERR_INVALID_SHAPE     # negative length
+    assert _prefill(lib, _shape(), [1, 4]) == A.DOPD_ERR_INVALID_SHAPE        # cu[0] != 0
+    assert _prefill(lib, _shape(), [0], nreq=-1) == A.DOPD_ERR_INVALID_SHAPE
+    assert _prefill(lib, _shape(), [0], nreq=0) == A.DOPD_OK                  # empty batch
+    assert _prefill(lib, _shape(), [0, 0, 0]) == A.DOPD_OK                    # all-empty requests
+    assert lib.dopd_prefill_attn(None, None, None, None, None, None, None, None, 1, None) == \
+        A.DOPD_ERR_NULL_POINTER
+
+
+def _decode(lib, shape, ctx, split=0, ws_bytes=1 << 30, pt_stride=1024, ws=FAKE, nreq=None):
+    ctx = np.asarray(ctx, np.int32)
+    p = C.c_void_p(FAKE)
+    n = len(ctx) if nreq is None else nreq
+    return lib.dopd_decode_attn(C.byref(shape), p, p, p, 10, p, pt_stride, p, A._hptr(ctx), n,
+                                split, p, None, C.c_void_p(ws) if ws else None, ws_bytes, None)
+
+
+def test_decode_host_validation(lib):
+    s = _shape()
+    assert _decode(lib, s, [5, 0]) == A.DOPD_ERR_INVALID_SHAPE               # context < 1
+    assert _decode(lib, s, [5], split=48) == A.DOPD_ERR_INVALID_SHAPE        # not a multiple of 32
+    assert _decode(lib, s, [5], split=-32) == A.DOPD_ERR_INVALID_SHAPE
+    assert _decode(lib, s, [5000], pt_stride=4) == A.DOPD_ERR_INVALID_SHAPE  # table too narrow
+    assert _decode(lib, _shape(hq=34, hkv=2), [5]) == A.DOPD_ERR_UNSUPPORTED  # group > 16
+    need = A.dopd_decode_workspace_size(s, [3000, 17], 2)
+    assert need > 0
+    assert _decode(lib, s, [3000, 17], ws_bytes=need - 1) == A.DOPD_ERR_WORKSPACE_TOO_SMALL
+    assert _decode(lib, s, [3000, 17], ws=0) == A.DOPD_ERR_NULL_POINTER
+    assert _decode(lib, s, [3000, 17], ws=FAKE + 16) == A.DOPD_ERR_INVALID_SHAPE   # misaligned
+    assert _decode(lib, s, [], nreq=0) == A.DOPD_OK
+    assert A.dopd_decode_workspace_size(s, [0], 1) == 0
+
+
+def test_decode_workspace_grows_with_smaller_splits(lib):
+    s = _shape()
+    ctx = [16384, 100, 4096]
+    big = A.dopd_decode_workspace_size(s, ctx, 3, 64)
+    small = A.dopd_decode_workspace_size(s, ctx, 3, 4096)
+    assert big > small > 0
+    assert big % 256 == 0
+
+
+def test_kv_write_and_pack_host_validation(lib):
+    s = _shape()
+    p = C.c_void_p(FAKE)
+    w = lib.dopd_kv_write
+    assert w(C.byref(s), p, p, p, p, 10, p, 4, p, p, -1, 5, None) == A.DOPD_ERR_INVALID_SHAPE
+    assert w(C.byref(s), None, p, p, p, 10, p, 4, p, p, 1, 5, None) == A.DOPD_ERR_NULL_POINTER
+    assert w(C.byref(s), p, p, p, p, 10, p, 4, p, p, 1, 0, None) == A.DOPD_OK    # nothing to do
+    lens = np.array([40, 600], np.int32)
+    pk = lib.dopd_kv_pack_for_handoff
+    assert pk(C.byref(s), 0, p, p, 10, p, 64, p, p, A._hptr(lens), p, 2, p, None) == \
+        A.DOPD_ERR_INVALID_SHAPE                                               # no layers
+    assert pk(C.byref(s), 1, p, p, 10, p, 8, p, p, A._hptr(lens), p, 2, p, None) == \
+        A.DOPD_ERR_INVALID_SHAPE                                               # 600 tokens > 8 pages
+    assert pk(C.byref(s), 1, p, p, 10, p, 64, p, p, None, p, 2, p, None) == \
+        A.DOPD_ERR_NULL_POINTER
+    assert pk(C.byref(_shape(dtype="fp32", d=80)), 1, p, p, 10, p, 64, p, p, A._hptr(lens), p,
+              2, p, None) == A.DOPD_ERR_UNSUPPORTED
+
+
+def test_validate_page_table_host(lib):
+    pt = np.array([[3, 1, -1], [0, -1, -1]], np.int32)
+    assert A.dopd_validate_page_table_host(pt, 3, 2, [20, 16], 4) == A.DOPD_OK
+    assert A.dopd_validate_page_table_host(pt, 3, 2, [40, 16], 4) == A.DOPD_ERR_INVALID_SHAPE
+    assert A.dopd_validate_page_table_host(pt, 3, 2, [20, 17], 4) == A.DOPD_ERR_INVALID_SHAPE
+    assert A.dopd_validate_page_table_host(pt, 3, 2, [20, 16], 3) == A.DOPD_ERR_INVALID_SHAPE
+    assert A.dopd_validate_page_table_host(pt, 3, 0, [], 4) == A.DOPD_OK
