@@ -1,0 +1,349 @@
+#!/usr/bin/env python3
+"""Benchmark of the attention hot path on one MI355X.
+
+Default workload: one mixed prefill/decode step with handoff (28 query heads,
+4 KV heads, d 128, bf16):
+
+  stream A: varlen causal prefill over 8 x 512 fresh tokens -> paged KV write
+            of those 4096 tokens -> handoff pack of the 8 requests (1 layer)
+  stream B: split-K paged decode of 192 requests, context lognormal(2048, 0.7)
+            clipped to [64, 16384], concurrently with stream A
+
+A "step" is one such launch set; K timed steps run back to back after W
+warm-up steps.  Every kernel is bracketed by HIP events on the stream it runs
+on.  The headline value is decode attention HBM throughput (algorithmic bytes /
+decode kernel time); prefill TFLOP/s and the write/pack bandwidths are
+reported beside it.  ``--workload`` selects the single-kernel workloads
+(decode MHA 7B-shaped, varlen prefill + write, GQA decode 70B-shaped) for the
+per-workload tables.
+
+Prints ONE JSON line.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0       # MI355X HBM3E
+BF16_PEAK_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+
+WORKLOADS = {
+    "mixed": ("mixed P/D step + handoff: prefill 8x512, decode 192 req ctx lognormal(2048,0.7) "
+              "[64,16384], 28/4 heads, d128, bf16, pack 8 req x 1 layer", 5),
+    "decode_mha": ("decode, MHA 7B-shaped: B64, 32 heads, d128, bf16, ctx lognormal(1024,0.8) "
+                   "[16,4096]", 2),
+    "prefill": ("varlen causal prefill + paged write: 16 prompts lognormal(1500,1.0) [32,8192], "
+                "32/32 heads, d128, bf16", 3),
+    "decode_gqa": ("decode, GQA 70B-shaped: B256, 64/8 heads, d128, bf16, ctx 80% U[100,500] + "
+                   "20% U[4096,16384]", 4),
+}
+
+
+# ------------------------------------------------------------------ algorithmic work
+def decode_bytes(ctx, hq, hkv, d, s=2):
+    ctx = np.asarray(ctx, np.int64)
+    b = len(ctx)
+    return int((2 * hkv * d * ctx * s).sum() + b * hq * d * 2 * s + (4 * ((ctx + 15) // 16)).sum() + 4 * b)
+
+
+def prefill_flops(lens, hq, d):
+    lens = np.asarray(lens, np.int64)
+    return int((4 * d * hq * lens * (lens + 1) // 2).sum())
+
+
+def write_bytes(lens, hkv, d, s=2):
+    lens = np.asarray(lens, np.int64)
+    t = int(lens.sum())
+    return int(2 * (2 * t * hkv * d * s) + 4 * ((lens + 15) // 16).sum() + 8 * len(lens))
+
+
+def pack_bytes(lens, layers, hkv, d, s=2):
+    lens = np.asarray(lens, np.int64)
+    return int(2 * (layers * 2 * hkv * lens * d * s).sum())
+
+
+# ------------------------------------------------------------------ helpers
+def cpu_info():
+    model = "unknown"
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    return model
+
+
+class Timer:
+    """HIP events around a call on a given stream, accumulated over steps."""
+
+    def __init__(self, torch, stream):
+        self.torch, self.stream, self.pairs = torch, stream, []
+
+    def __enter__(self):
+        e = self.torch.cuda.Event(enable_timing=True)
+        e.record(self.stream)
+        self.pairs.append([e, None])
+        return self
+
+    def __exit__(self, *exc):
+        e = self.torch.cuda.Event(enable_timing=True)
+        e.record(self.stream)
+        self.pairs[-1][1] = e
+
+    def avg_us(self, skip=0):
+        ts = [a.elapsed_time(b) * 1e3 for a, b in self.pairs[skip:]]
+        return float(np.mean(ts)) if ts else float("nan")
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", choices=sorted(WORKLOADS), default="mixed")
+    ap.add_argument("--pack-layers", type=int, default=1,
+                    help="layers packed per handoff in the mixed step (1 = the configured step)")
+    ap.add_argument("--split", type=int, default=0, help="decode split tokens (0 = automatic)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py runs on one GPU only: the hot path is measured on a single MI355X; "
+              "--gpus must be 1", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2511_20982_amd import attn as A
+    from paper_2511_20982_amd import inputs as I
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(2)
+    A.lib()  # fail loudly if the HIP library is not built
+
+    desc, cfg = WORKLOADS[args.workload]
+    t0 = time.time()
+    w = {5: lambda: I.config5(num_layers=args.pack_layers), 2: I.config2, 3: I.config3,
+         4: I.config4}[cfg]()
+    gen_s = time.time() - t0
+    dev = "cuda"
+    shape = A.make_shape(w.hq, w.hkv, w.d, w.dtype, w.scale)
+    sA = torch.cuda.current_stream()
+    sB = torch.cuda.Stream()  # default priority
+
+    kern = {}
+    if args.workload in ("mixed",):
+        L = args.pack_layers
+        # paged pools: layer 0 is the attention layer; extra layers only widen the pack
+        kp_np, vp_np = w.k_pool, w.v_pool
+        kp = torch.empty((L,) + kp_np.shape, dtype=torch.bfloat16, device=dev)
+        vp = torch.empty((L,) + vp_np.shape, dtype=torch.bfloat16, device=dev)
+        kp[0].copy_(A.to_device(kp_np))
+        vp[0].copy_(A.to_device(vp_np))
+        for layer in range(1, L):
+            kp[layer].copy_(kp[0])
+            vp[layer].copy_(vp[0])
+        pt = A.to_device(w.page_table)
+        stride = w.page_table.shape[1]
+        pre_pt = pt[w.prefill_rows[0]:]  # rows of the prefill requests
+        q, k, v = A.to_device(w.q), A.to_device(w.k), A.to_device(w.v)
+        cu = A.to_device(w.cu_seqlens)
+        out_p = torch.empty_like(q)
+        n_pre = len(w.prefill_lens)
+        start = torch.zeros(n_pre, dtype=torch.int32, device=dev)
+        n_dec = len(w.context_lens)
+        q_dec = A.to_device(w.q_dec)
+        ctx = A.to_device(w.context_lens)
+        out_d = torch.empty_like(q_dec)
+        ws = A.decode_workspace(shape, w.context_lens, n_dec, args.split)
+        offs_np = I.handoff_offsets(w.handoff_lens, L, w.hkv, w.d)
+        offs = A.to_device(offs_np)
+        hreq, hlen = A.to_device(w.handoff_reqs), A.to_device(w.handoff_lens)
+        out_h = torch.empty(int(offs_np[-1]), dtype=torch.bfloat16, device=dev)
+        T = int(w.cu_seqlens[-1])
+        tm = {n: Timer(torch, s) for n, s in
+              (("prefill", sA), ("kv_write", sA), ("pack", sA), ("decode", sB))}
+        ev_join = torch.cuda.Event()
+
+        def step():
+            # The prefill is enqueued first: its large workgroups are dispatched
+            # before the decode work items fill the machine.
+            sB.wait_stream(sA)
+            with tm["prefill"]:
+                A.dopd_prefill_attn(shape, q, k, v, out_p, None, cu, w.cu_seqlens, n_pre, sA)
+            with tm["decode"]:
+                A.dopd_decode_attn(shape, q_dec, kp[0], vp[0], w.num_pages, pt, stride, ctx,
+                                   w.context_lens, n_dec, args.split, out_d, None, ws, stream=sB)
+            with tm["kv_write"]:
+                A.dopd_kv_write(shape, k, v, kp[0], vp[0], w.num_pages, pre_pt, stride, cu, start,
+                                n_pre, T, sA)
+            with tm["pack"]:
+                A.dopd_kv_pack_for_handoff(shape, L, kp, vp, w.num_pages, pt, stride, hreq, hlen,
+                                           w.handoff_lens, offs, n_pre, out_h, sA)
+            ev_join.record(sB)
+            sA.wait_event(ev_join)
+
+        work = {
+            "decode": ("GB/s", decode_bytes(w.context_lens, w.hq, w.hkv, w.d)),
+            "prefill": ("TFLOP/s", prefill_flops(w.prefill_lens, w.hq, w.d)),
+            "kv_write": ("GB/s", write_bytes(w.prefill_lens, w.hkv, w.d)),
+            "pack": ("GB/s", pack_bytes(w.handoff_lens, L, w.hkv, w.d)),
+        }
+        dominant = "decode"
+    elif args.workload in ("decode_mha", "decode_gqa"):
+        kp, vp = A.to_device(w.k_pool), A.to_device(w.v_pool)
+        pt = A.to_device(w.page_table)
+        q_dec = A.to_device(w.q_dec)
+        ctx = A.to_device(w.context_lens)
+        out_d = torch.empty_like(q_dec)
+        n_dec = len(w.context_lens)
+        ws = A.decode_workspace(shape, w.context_lens, n_dec, args.split)
+        tm = {"decode": Timer(torch, sA)}
+
+        def step():
+            with tm["decode"]:
+                A.dopd_decode_attn(shape, q_dec, kp, vp, w.num_pages, pt, w.page_table.shape[1],
+                                   ctx, w.context_lens, n_dec, args.split, out_d, None, ws, stream=sA)
+
+        work = {"decode": ("GB/s", decode_bytes(w.context_lens, w.hq, w.hkv, w.d))}
+        dominant = "decode"
+    else:  # prefill + write
+        q, k, v = A.to_device(w.q), A.to_device(w.k), A.to_device(w.v)
+        cu = A.to_device(w.cu_seqlens)
+        out_p = torch.empty_like(q)
+        kp, vp = A.to_device(w.k_pool), A.to_device(w.v_pool)
+        pt = A.to_device(w.page_table)
+        n_pre = len(w.prefill_lens)
+        start = torch.zeros(n_pre, dtype=torch.int32, device=dev)
+        T = int(w.cu_seqlens[-1])
+        tm = {"prefill": Timer(torch, sA), "kv_write": Timer(torch, sA)}
+
+        def step():
+            with tm["prefill"]:
+                A.dopd_prefill_attn(shape, q, k, v, out_p, None, cu, w.cu_seqlens, n_pre, sA)
+            with tm["kv_write"]:
+                A.dopd_kv_write(shape, k, v, kp, vp, w.num_pages, pt, w.page_table.shape[1], cu,
+                                start, n_pre, T, sA)
+
+        work = {"prefill": ("TFLOP/s", prefill_flops(w.prefill_lens, w.hq, w.d)),
+                "kv_write": ("GB/s", write_bytes(w.prefill_lens, w.hkv, w.d))}
+        dominant = "prefill"
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    for t in tm.values():
+        t.pairs.clear()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    ev0.record(sA)
+    for _ in range(args.steps):
+        step()
+    ev1.record(sA)
+    torch.cuda.synchronize()
+    ms_step = ev0.elapsed_time(ev1) / args.steps
+
+    for name, t in tm.items():
+        unit, amount = work[name]
+        us = t.avg_us()
+        rate = amount / (us * 1e-6) / (1e12 if unit == "TFLOP/s" else 1e9)
+        peak = BF16_PEAK_TFLOPS if unit == "TFLOP/s" else HBM_PEAK_GBS
+        kern[name] = {"avg_us": round(us, 2), "rate": round(rate, 2), "unit": unit,
+                      "frac": round(rate / peak, 4),
+                      ("flops" if unit == "TFLOP/s" else "bytes"): amount}
+
+    dk = kern[dominant]
+    roofline = {"kernel": dominant, "bound": "mfma" if dk["unit"] == "TFLOP/s" else "hbm",
+                "achieved": dk["rate"], "peak": BF16_PEAK_TFLOPS if dk["unit"] == "TFLOP/s" else HBM_PEAK_GBS,
+                "unit": dk["unit"], "frac": dk["frac"], "traffic": None}
+
+    # ---- CPU baseline: the fp64 oracle on host cores, plus a parity spot check
+    cpu = None
+    parity = None
+    if not args.no_cpu_baseline:
+        import oracle
+        threads = int(os.environ.get("OMP_NUM_THREADS", "0")) or len(os.sched_getaffinity(0))
+        os.environ.setdefault("OMP_NUM_THREADS", str(threads))
+        if dominant == "decode":
+            # The whole decode batch of the step (about a second of host work).
+            t1 = time.time()
+            ref, _ = oracle.decode(w.q_dec, w.k_pool, w.v_pool, w.page_table, w.context_lens,
+                                   w.scale)
+            dt = time.time() - t1
+            amount = decode_bytes(w.context_lens, w.hq, w.hkv, w.d)
+            cpu = {"value": round(amount / dt / 1e9, 4), "unit": "GB/s", "cores": threads,
+                   "kind": "oracle", "cpu": cpu_info(), "seconds": round(dt, 2),
+                   "sample": f"fp64 oracle decode of the whole batch ({len(w.context_lens)} "
+                             f"requests, {amount / 1e9:.3f} GB algorithmic)"}
+            gotf = I.bf16_bits_to_f32(A.to_host(out_d)).astype(np.float64)
+            parity = {"decode_max_abs_err": float(np.max(np.abs(gotf - ref))),
+                      "decode_rows": int(ref.shape[0] * ref.shape[1])}
+            if "prefill" in kern:
+                t1 = time.time()
+                ref_p, _ = oracle.prefill(w.q, w.k, w.v, w.cu_seqlens, w.scale)
+                dtp = time.time() - t1
+                cpu["prefill_tflops"] = round(work["prefill"][1] / dtp / 1e12, 6)
+                cpu["prefill_seconds"] = round(dtp, 2)
+                cpu["sample"] += f"; fp64 oracle prefill of the whole prefill batch ({dtp:.1f} s)"
+                gotp = I.bf16_bits_to_f32(A.to_host(out_p)).astype(np.float64)
+                parity["prefill_max_abs_err"] = float(np.max(np.abs(gotp - ref_p)))
+        else:
+            # Bounded sample: the last 4 rows of every prompt (the longest rows), per head.
+            rows_tok = np.concatenate([w.cu_seqlens[1:] - 1 - i for i in range(4)])
+            rows_tok = np.repeat(rows_tok, 4)
+            heads = (np.arange(len(rows_tok)) * 7) % w.hq
+            t1 = time.time()
+            ref, _ = oracle.prefill_rows(w.q, w.k, w.v, w.cu_seqlens, w.scale, rows_tok, heads)
+            dt = time.time() - t1
+            req_of = np.searchsorted(w.cu_seqlens, rows_tok, side="right") - 1
+            pos = rows_tok - w.cu_seqlens[req_of]
+            flops = int((4 * w.d * (pos + 1)).sum())
+            cpu = {"value": round(flops / dt / 1e12, 6), "unit": "TFLOP/s", "cores": threads,
+                   "kind": "oracle", "cpu": cpu_info(), "seconds": round(dt, 2),
+                   "sample": f"fp64 oracle prefill of {len(rows_tok)} sampled rows (the last 4 "
+                             f"rows of every prompt, 4 heads each; {flops / 1e9:.2f} GFLOP)"}
+            gotf = I.bf16_bits_to_f32(A.to_host(out_p)[rows_tok, heads]).astype(np.float64)
+            parity = {"prefill_max_abs_err": float(np.max(np.abs(gotf - ref))),
+                      "prefill_rows": int(len(rows_tok))}
+
+    value = kern[dominant]["rate"]
+    line = {
+        "metric": "decode attn HBM GB/s (% peak) + prefill attn TFLOP/s (% MFMA peak)",
+        "value": value,
+        "unit": kern[dominant]["unit"],
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": desc, "seed": int(w.seed), "split_tokens": args.split,
+                   "pack_layers": args.pack_layers if args.workload == "mixed" else None},
+        "roofline": roofline,
+        "kernels": kern,
+        "cpu_baseline": cpu,
+        "parity": parity,
+        "input_gen_s": round(gen_s, 1),
+    }
+    if "prefill" in kern and dominant != "prefill":
+        line["prefill_tflops"] = kern["prefill"]["rate"]
+        line["prefill_mfma_frac"] = kern["prefill"]["frac"]
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

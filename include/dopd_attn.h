@@ -111,16 +111,15 @@ dopd_status dopd_kv_write(const dopd_attn_shape* shape, const void* k_new, const
  *   context_lens_host: identical host copy (>= 1 each), used to size the
  *     launch and the key-range split.
  *   split_tokens: keys per split-K work item, 0 = automatic, else a positive
- *     multiple of 32.  The result does not depend on it beyond rounding.
+ *     multiple of 32, at most 4096.  The result does not depend on it beyond
+ *     rounding.
  *   workspace: device memory of at least dopd_decode_workspace_size() bytes
- *     for the same arguments.  Its first 256-byte-aligned counter region must
- *     be zero when the workspace is first used (allocate it zeroed); every
- *     completed call leaves it zero again.  Calls that overlap in time must
- *     not share a workspace.
- * bf16 path: one kernel; each work item (request, KV head, key split) reads
- * its pages once for all Hq/Hkv query heads of the group (at most 16), and
- * the last item of a request to finish merges the split partials exactly
- * (log-sum-exp rescaling).
+ *     for the same arguments, 256-byte aligned, any contents; it holds the
+ *     split-K partials.  Calls that overlap in time must not share it.
+ * bf16 path: work items (request, KV head, key split) read each page once for
+ * all Hq/Hkv query heads of the group (at most 16); requests whose context
+ * exceeds one split are finished by a second kernel that merges the split
+ * partials exactly (log-sum-exp rescaling), on the same stream.
  */
 dopd_status dopd_decode_attn(const dopd_attn_shape* shape, const void* q, const void* k_pool,
                              const void* v_pool, int32_t num_pages, const int32_t* page_table,

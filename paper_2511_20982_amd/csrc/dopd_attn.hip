@@ -44,9 +44,11 @@ dopd_status check_shape(const dopd_attn_shape* s) {
 
 // ---- decode planning --------------------------------------------------------
 constexpr int kMaxGroupBf16 = 16;   // query heads per KV head handled by one decode wave
-constexpr int kAutoSplitMax = 512;
-constexpr int kAutoSplitMin = 64;
-constexpr int64_t kTargetItems = 8192;  // ~4 waves per SIMD slot of the 256 CUs
+constexpr int kAutoSplitMax = 2048;
+constexpr int kAutoSplitMin = 128;
+// Four-wave work items, two resident per CU: 512 slots on 256 CUs; aim for
+// about four rounds so that the ragged items dispatched last fill the tail.
+constexpr int64_t kTargetItems = 2048;
 
 int64_t decode_items(const int32_t* ctx, int32_t n, int split, int hkv) {
   int64_t items = 0;
@@ -62,7 +64,7 @@ int choose_split(const int32_t* ctx, int32_t n, int hkv, int32_t requested) {
 }
 
 struct DecodeLayout {
-  size_t counters_off, counters_bytes, part_o_off, part_ml_off, total;
+  size_t part_o_off, part_ml_off, total;
 };
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
@@ -70,12 +72,10 @@ size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 DecodeLayout decode_layout(const dopd_attn_shape* s, const int32_t* ctx, int32_t n, int split) {
   DecodeLayout L{};
   const int g = s->num_q_heads / s->num_kv_heads;
-  const int64_t items = decode_items(ctx, n, split, s->num_kv_heads);
-  L.counters_off = 0;
-  L.counters_bytes = align256((size_t)n * s->num_kv_heads * sizeof(int));
-  L.part_o_off = L.counters_bytes;
-  L.part_ml_off = L.part_o_off + align256((size_t)items * g * s->head_dim * sizeof(float));
-  L.total = L.part_ml_off + align256((size_t)items * g * 2 * sizeof(float));
+  const int64_t slots = decode_items(ctx, n, split, s->num_kv_heads);
+  L.part_o_off = 0;
+  L.part_ml_off = align256((size_t)slots * g * s->head_dim * sizeof(float));
+  L.total = L.part_ml_off + align256((size_t)slots * g * 2 * sizeof(float));
   return L;
 }
 
@@ -87,7 +87,8 @@ dopd_status check_decode_host(const dopd_attn_shape* s, const int32_t* ctx_host,
   if (n > 0 && !ctx_host) return DOPD_ERR_NULL_POINTER;
   for (int32_t r = 0; r < n; ++r)
     if (ctx_host[r] < 1) return DOPD_ERR_INVALID_SHAPE;
-  if (split < 0 || (split > 0 && split % 32 != 0)) return DOPD_ERR_INVALID_SHAPE;
+  if (split < 0 || (split > 0 && split % 32 != 0) || split > dopd::kDecMaxSplit)
+    return DOPD_ERR_INVALID_SHAPE;
   if (s->dtype == DOPD_BF16 && s->num_q_heads / s->num_kv_heads > kMaxGroupBf16)
     return DOPD_ERR_UNSUPPORTED;
   return DOPD_OK;
@@ -253,7 +254,11 @@ dopd_status dopd_decode_attn(const dopd_attn_shape* s, const void* q, const void
   if ((reinterpret_cast<uintptr_t>(workspace) & 255) != 0) return DOPD_ERR_INVALID_SHAPE;
   const int64_t items = decode_items(ctx_host, nreq, split, hkv);
   if (items > INT32_MAX) return DOPD_ERR_INVALID_SHAPE;
+  int64_t full_items = 0;
+  for (int32_t r = 0; r < nreq; ++r) full_items += (int64_t)(ctx_host[r] / split) * hkv;
   char* ws = static_cast<char*>(workspace);
+  int64_t merge_items = 0;
+  for (int32_t r = 0; r < nreq; ++r) merge_items += ctx_host[r] > split ? hkv : 0;
   dopd::DecodeArgs a;
   a.q = (const uint16_t*)q;
   a.k_pool = (const uint16_t*)k_pool;
@@ -262,7 +267,6 @@ dopd_status dopd_decode_attn(const dopd_attn_shape* s, const void* q, const void
   a.ctx_lens = ctx;
   a.out = (uint16_t*)out;
   a.lse = lse;
-  a.counters = reinterpret_cast<int*>(ws + L.counters_off);
   a.part_o = reinterpret_cast<float*>(ws + L.part_o_off);
   a.part_ml = reinterpret_cast<float*>(ws + L.part_ml_off);
   a.pt_stride = pt_stride;
@@ -270,11 +274,18 @@ dopd_status dopd_decode_attn(const dopd_attn_shape* s, const void* q, const void
   a.hq = hq;
   a.hkv = hkv;
   a.split = split;
+  a.full_items = (int)full_items;
   a.scale_log2 = s->softmax_scale * dopd::kLog2e;
   if (d == 64)
-    hipLaunchKernelGGL(dopd::decode_bf16_kernel<64>, dim3((unsigned)items), dim3(64), 0, strm, a);
+    hipLaunchKernelGGL(dopd::decode_split_kernel<64>, dim3((unsigned)items), dim3(256), 0, strm, a);
   else
-    hipLaunchKernelGGL(dopd::decode_bf16_kernel<128>, dim3((unsigned)items), dim3(64), 0, strm, a);
+    hipLaunchKernelGGL(dopd::decode_split_kernel<128>, dim3((unsigned)items), dim3(256), 0, strm, a);
+  st = launch_status();
+  if (st != DOPD_OK || merge_items == 0) return st;
+  if (d == 64)
+    hipLaunchKernelGGL(dopd::decode_merge_kernel<64>, dim3((unsigned)merge_items), dim3(256), 0, strm, a);
+  else
+    hipLaunchKernelGGL(dopd::decode_merge_kernel<128>, dim3((unsigned)merge_items), dim3(256), 0, strm, a);
   return launch_status();
 }
 

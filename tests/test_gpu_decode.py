@@ -34,12 +34,9 @@ def test_decode_bf16_matches_oracle(hq, hkv, d):
 def test_decode_split_size_independent(split):
     w = I.decode_workload("t", 51, [1, 40, 300, 5000, 16384], 16, 2, 128, "bf16")
     ref, _ = oracle.decode(w.q_dec, w.k_pool, w.v_pool, w.page_table, w.context_lens, w.scale)
-    out, _, ws = G.gpu_decode(G.shape_of(w), w.q_dec, w.k_pool, w.v_pool, w.page_table,
-                              w.context_lens, split=split, return_ws=True)
+    out, _ = G.gpu_decode(G.shape_of(w), w.q_dec, w.k_pool, w.v_pool, w.page_table,
+                          w.context_lens, split=split)
     G.assert_attention_close(out, ref, "bf16", f"split={split}")
-    n_counters = len(w.context_lens) * w.hkv
-    assert int(ws[: 4 * n_counters].view(torch.int32).abs().sum()) == 0, \
-        "split-K counters not left at zero"
 
 
 def test_decode_deterministic_and_page_permutation_bit_identical():
