@@ -35,6 +35,18 @@ if ROOT not in sys.path:
 
 HBM_PEAK_GBS = 8000.0       # MI355X HBM3E
 BF16_PEAK_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PROFILES = os.path.join(ROOT, "profiles")
+KERNEL_SOURCES = ("paper_2511_20982_amd/csrc/dopd_attn.hip",
+                  "paper_2511_20982_amd/csrc/kernels/common.hpp",
+                  "paper_2511_20982_amd/csrc/kernels/decode_bf16.hpp",
+                  "paper_2511_20982_amd/csrc/kernels/prefill_bf16.hpp",
+                  "paper_2511_20982_amd/csrc/kernels/kv_write.hpp",
+                  "paper_2511_20982_amd/csrc/kernels/kv_pack.hpp")
+# Kernels behind each timed call (the decode call is a split kernel plus, when
+# some context exceeds one split, a merge kernel).
+CALL_KERNELS = {"decode": ("decode_split_kernel", "decode_merge_kernel"),
+                "prefill": ("prefill_bf16_kernel",), "kv_write": ("kv_write_kernel",),
+                "pack": ("kv_pack_kernel",)}
 
 WORKLOADS = {
     "mixed": ("mixed P/D step + handoff: prefill 8x512, decode 192 req ctx lognormal(2048,0.7) "
@@ -72,6 +84,99 @@ def pack_bytes(lens, layers, hkv, d, s=2):
 
 
 # ------------------------------------------------------------------ helpers
+def source_hash() -> str:
+    import hashlib
+    h = hashlib.sha256()
+    for rel in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def load_traffic(workload, call):
+    """HBM bytes per call from committed counter summaries, if the kernels are unchanged."""
+    path = os.path.join(PROFILES, f"traffic_{workload}.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        t = json.load(f)
+    if t.get("source_hash") != source_hash() or call not in t.get("calls", {}):
+        return None
+    return t["calls"][call]["hbm_bytes_per_call"]
+
+
+def summarize(args):
+    """Turns rocprofv3 CSV output into the markdown/JSON summaries kept in profiles/."""
+    import csv
+    import glob
+    from collections import defaultdict
+    out = []
+    stats = sorted(glob.glob(os.path.join(args.summarize, "**", "*kernel_stats.csv"), recursive=True))
+    if stats:
+        out.append(f"# rocprofv3 kernel statistics: {args.label}\n")
+        out.append(f"Command: `{args.command}`\n")
+        out.append("| kernel | calls | avg us | min us | max us | share |")
+        out.append("|---|---|---|---|---|---|")
+        for row in csv.DictReader(open(stats[0])):
+            name = row["Name"][:90].replace("|", "/")
+            out.append(f"| {name} | {row['Calls']} | {float(row['AverageNs']) / 1e3:.2f} | "
+                       f"{float(row['MinNs']) / 1e3:.2f} | {float(row['MaxNs']) / 1e3:.2f} | "
+                       f"{float(row['Percentage']):.1f}% |")
+    pmc = sorted(glob.glob(os.path.join(args.summarize, "**", "*counter_collection.csv"),
+                           recursive=True))
+    if pmc:
+        # per kernel name: list of per-dispatch counter sums
+        per = defaultdict(lambda: defaultdict(list))
+        for f in pmc:
+            acc = defaultdict(float)
+            names = {}
+            for r in csv.DictReader(open(f)):
+                key = (r["Dispatch_Id"], r["Counter_Name"])
+                acc[key] += float(r["Counter_Value"])
+                names[r["Dispatch_Id"]] = r["Kernel_Name"]
+            for (disp, ctr), v in acc.items():
+                per[names[disp]][ctr].append(v)
+        copy_mib = args.copy_calib_mib
+        factors = {}
+        for kname, ctrs in per.items():
+            if "neg_kernel" in kname:
+                for ctr in ("FETCH_SIZE", "WRITE_SIZE"):
+                    if ctr in ctrs:
+                        measured = float(np.median(ctrs[ctr]))  # KiB per dispatch
+                        factors[ctr] = copy_mib * 1024.0 / measured if measured > 0 else None
+        out.append(f"\n# rocprofv3 HBM counters (KiB per dispatch, median): {args.label}\n")
+        out.append(f"`--pmc FETCH_SIZE` and `--pmc WRITE_SIZE` in separate runs.  Calibration: one "
+                   f"elementwise kernel reading and writing {copy_mib} MiB in the same run; scale = "
+                   f"known bytes / counter = {json.dumps(factors)}.\n")
+        out.append("| kernel | dispatches | FETCH_SIZE KiB | WRITE_SIZE KiB |")
+        out.append("|---|---|---|---|")
+        calls = {}
+        for kname, ctrs in sorted(per.items()):
+            f_k = float(np.median(ctrs["FETCH_SIZE"])) if "FETCH_SIZE" in ctrs else float("nan")
+            w_k = float(np.median(ctrs["WRITE_SIZE"])) if "WRITE_SIZE" in ctrs else float("nan")
+            n = max(len(ctrs.get("FETCH_SIZE", [])), len(ctrs.get("WRITE_SIZE", [])))
+            out.append(f"| {kname[:90]} | {n} | {f_k:.0f} | {w_k:.0f} |")
+            for call, kernels in CALL_KERNELS.items():
+                if any(k in kname for k in kernels):
+                    c = calls.setdefault(call, {"fetch_kib": 0.0, "write_kib": 0.0, "kernels": []})
+                    c["fetch_kib"] += f_k
+                    c["write_kib"] += w_k
+                    c["kernels"].append(kname)
+        for call, c in calls.items():
+            ff, fw = factors.get("FETCH_SIZE") or 1.0, factors.get("WRITE_SIZE") or 1.0
+            c["hbm_bytes_per_call"] = int(1024 * (c["fetch_kib"] * ff + c["write_kib"] * fw))
+        tr = {"workload": args.label, "source_hash": source_hash(), "copy_factors": factors,
+              "calls": calls, "command": args.command}
+        with open(os.path.join(PROFILES, f"traffic_{args.label}.json"), "w") as f:
+            json.dump(tr, f, indent=1)
+        out.append("\nHBM bytes per call (scaled): " +
+                   ", ".join(f"{k}: {v['hbm_bytes_per_call'] / 1e6:.1f} MB" for k, v in calls.items()))
+    text = "\n".join(out) + "\n"
+    with open(args.summary_out, "w") as f:
+        f.write(text)
+    print(text)
+
+
 def cpu_info():
     model = "unknown"
     try:
@@ -115,8 +220,21 @@ def main():
     ap.add_argument("--pack-layers", type=int, default=1,
                     help="layers packed per handoff in the mixed step (1 = the configured step)")
     ap.add_argument("--split", type=int, default=0, help="decode split tokens (0 = automatic)")
+    ap.add_argument("--streams", type=int, default=1, choices=(1, 2),
+                    help="mixed step: 2 = decode on its own stream beside prefill/write/pack, "
+                         "1 = everything in order on one stream")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calib-mib", type=int, default=0,
+                    help="after timing, run one device copy of this size (counter calibration)")
+    ap.add_argument("--summarize", default=None,
+                    help="summarise a rocprofv3 output directory instead of benchmarking")
+    ap.add_argument("--label", default="mixed")
+    ap.add_argument("--command", default="")
+    ap.add_argument("--summary-out", default=None)
     args = ap.parse_args()
+    if args.summarize:
+        summarize(args)
+        return
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py runs on one GPU only: the hot path is measured on a single MI355X; "
@@ -176,23 +294,36 @@ def main():
               (("prefill", sA), ("kv_write", sA), ("pack", sA), ("decode", sB))}
         ev_join = torch.cuda.Event()
 
+        sD = sB if args.streams == 2 else sA
+        if args.streams == 1:
+            tm["decode"] = Timer(torch, sA)
+
         def step():
-            # The prefill is enqueued first: its large workgroups are dispatched
-            # before the decode work items fill the machine.
-            sB.wait_stream(sA)
+            # Two streams: the prefill is enqueued first, so its large workgroups
+            # are dispatched before the decode work items fill the machine.
+            if args.streams == 2:
+                sB.wait_stream(sA)
             with tm["prefill"]:
                 A.dopd_prefill_attn(shape, q, k, v, out_p, None, cu, w.cu_seqlens, n_pre, sA)
-            with tm["decode"]:
-                A.dopd_decode_attn(shape, q_dec, kp[0], vp[0], w.num_pages, pt, stride, ctx,
-                                   w.context_lens, n_dec, args.split, out_d, None, ws, stream=sB)
+            if args.streams == 2:
+                with tm["decode"]:
+                    A.dopd_decode_attn(shape, q_dec, kp[0], vp[0], w.num_pages, pt, stride, ctx,
+                                       w.context_lens, n_dec, args.split, out_d, None, ws,
+                                       stream=sD)
             with tm["kv_write"]:
                 A.dopd_kv_write(shape, k, v, kp[0], vp[0], w.num_pages, pre_pt, stride, cu, start,
                                 n_pre, T, sA)
+            if args.streams == 1:
+                with tm["decode"]:
+                    A.dopd_decode_attn(shape, q_dec, kp[0], vp[0], w.num_pages, pt, stride, ctx,
+                                       w.context_lens, n_dec, args.split, out_d, None, ws,
+                                       stream=sD)
             with tm["pack"]:
                 A.dopd_kv_pack_for_handoff(shape, L, kp, vp, w.num_pages, pt, stride, hreq, hlen,
                                            w.handoff_lens, offs, n_pre, out_h, sA)
-            ev_join.record(sB)
-            sA.wait_event(ev_join)
+            if args.streams == 2:
+                ev_join.record(sB)
+                sA.wait_event(ev_join)
 
         work = {
             "decode": ("GB/s", decode_bytes(w.context_lens, w.hq, w.hkv, w.d)),
@@ -263,10 +394,21 @@ def main():
                       "frac": round(rate / peak, 4),
                       ("flops" if unit == "TFLOP/s" else "bytes"): amount}
 
+    if args.copy_calib_mib:
+        # A shader kernel of known traffic (reads and writes N MiB once), used to
+        # scale the HBM counters; a plain device copy would go to a DMA engine.
+        src = torch.ones(args.copy_calib_mib << 18, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        torch.neg(src, out=dst)
+        torch.cuda.synchronize()
+        del src, dst
+
     dk = kern[dominant]
-    roofline = {"kernel": dominant, "bound": "mfma" if dk["unit"] == "TFLOP/s" else "hbm",
+    roofline = {"kernel": dominant, "kernels": list(CALL_KERNELS[dominant]),
+                "bound": "mfma" if dk["unit"] == "TFLOP/s" else "hbm",
                 "achieved": dk["rate"], "peak": BF16_PEAK_TFLOPS if dk["unit"] == "TFLOP/s" else HBM_PEAK_GBS,
-                "unit": dk["unit"], "frac": dk["frac"], "traffic": None}
+                "unit": dk["unit"], "frac": dk["frac"],
+                "traffic": load_traffic(args.workload, dominant)}
 
     # ---- CPU baseline: the fp64 oracle on host cores, plus a parity spot check
     cpu = None
@@ -332,6 +474,7 @@ def main():
         "dtype": "bf16",
         "data": "synthetic",
         "config": {"workload": desc, "seed": int(w.seed), "split_tokens": args.split,
+                   "streams": args.streams if args.workload == "mixed" else 1,
                    "pack_layers": args.pack_layers if args.workload == "mixed" else None},
         "roofline": roofline,
         "kernels": kern,

@@ -178,9 +178,9 @@ dopd_status dopd_prefill_attn(const dopd_attn_shape* s, const void* q, const voi
   const int64_t blocks = bf16_items * hq;
   if (blocks > INT32_MAX) return DOPD_ERR_INVALID_SHAPE;
   if (d == 64)
-    hipLaunchKernelGGL(dopd::prefill_bf16_kernel<64>, dim3((unsigned)blocks), dim3(256), 0, strm, a);
+    hipLaunchKernelGGL(dopd::prefill_bf16_kernel<64>, dim3((unsigned)blocks), dim3(dopd::kPfThreads), 0, strm, a);
   else
-    hipLaunchKernelGGL(dopd::prefill_bf16_kernel<128>, dim3((unsigned)blocks), dim3(256), 0, strm, a);
+    hipLaunchKernelGGL(dopd::prefill_bf16_kernel<128>, dim3((unsigned)blocks), dim3(dopd::kPfThreads), 0, strm, a);
   return launch_status();
 }
 

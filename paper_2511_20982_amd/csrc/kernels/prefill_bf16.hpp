@@ -1,9 +1,9 @@
 // Variable-length causal prefill attention, bf16 in / fp32 accumulate, gfx950.
 //
-// Workgroup = 4 waves = one (q tile of 128 rows, request, query head); each
+// Workgroup = 8 waves = one (q tile of 256 rows, request, query head); each
 // wave owns 32 query rows.  K/V tiles of 64 tokens are staged in LDS (K
-// token-major, V transposed to dim-major on the way in) and shared by the four
-// waves.  Per tile and wave:
+// token-major, V transposed to dim-major on the way in), double-buffered, and
+// shared by the eight waves.  Per tile and wave:
 //
 //   S^T[64 tok][32 q] = K[64][d] . Q^T[d][32]       2 x (d/16) v_mfma_f32_32x32x16_bf16
 //   O^T[d][32 q]     += V^T[d][64] . P^T[64][32]    (d/32) x 4  v_mfma_f32_32x32x16_bf16
@@ -32,7 +32,8 @@ struct PrefillArgs {
   float scale_log2;
 };
 
-constexpr int kPfBM = 128;  // query rows per workgroup
+constexpr int kPfBM = 256;  // query rows per workgroup (32 per wave)
+constexpr int kPfThreads = kPfBM / 32 * 64;
 constexpr int kPfBN = 64;   // keys per LDS tile
 
 // Number of BM-row q tiles of request rr.
@@ -70,17 +71,18 @@ __device__ __forceinline__ bool pf_find_item(const PrefillArgs& a, int b, int& t
 }
 
 template <int D>
-__global__ __launch_bounds__(256, 2) void prefill_bf16_kernel(PrefillArgs a) {
+__global__ __launch_bounds__(kPfThreads, 2) void prefill_bf16_kernel(PrefillArgs a) {
   constexpr int BM = kPfBM, BN = kPfBN;
   constexpr int KP = D + 8;      // padded K row (elements)
   constexpr int VP = BN + 8;     // padded V^T row (elements)
   constexpr int KS = D / 16;     // k-steps of the QK MFMA
   constexpr int ET = D / 32;     // O^T tiles of 32 dims
   constexpr int CPR = D / 8;     // 16-byte chunks per K/V row
-  constexpr int KCH = BN * CPR / 256;   // K chunks staged per thread
+  constexpr int NTH = kPfThreads;
+  constexpr int KCH = BN * CPR / NTH;   // K chunks staged per thread
   constexpr int VTH = (BN / 4) * CPR;   // threads staging V (4 tokens x 8 dims each)
-  __shared__ __attribute__((aligned(16))) uint16_t sK[BN * KP];
-  __shared__ __attribute__((aligned(16))) uint16_t sV[D * VP];
+  __shared__ __attribute__((aligned(16))) uint16_t sK[2][BN * KP];
+  __shared__ __attribute__((aligned(16))) uint16_t sV[2][D * VP];
 
   const int tid = threadIdx.x, l = lane_id(), w = tid >> 6;
   int tile, r, h;
@@ -118,118 +120,202 @@ __global__ __launch_bounds__(256, 2) void prefill_bf16_kernel(PrefillArgs a) {
   const uint16_t* kg = a.k + (int64_t)seq0 * kv_row + (int64_t)kvh * D;
   const uint16_t* vg = a.v + (int64_t)seq0 * kv_row + (int64_t)kvh * D;
 
-  u32x4 kreg[KCH], vreg[4];
   const int v_tg = tid % 16, v_col = tid / 16;  // V staging: tokens 4*v_tg.., dims 8*v_col..
-  auto gload = [&](int kv0) {
+  u32x4 rk[KCH], rv[4];                          // global -> LDS staging registers
+  // Rows past the end of the request are read from its last token instead
+  // (always in bounds and finite); their scores are masked and their P is 0.
+  auto gload_k = [&](int kv0) {
 #pragma unroll
     for (int u = 0; u < KCH; ++u) {
-      const int ch = tid + 256 * u, t = ch / CPR, col = ch % CPR, tok = kv0 + t;
-      kreg[u] = tok < kv_end ? *reinterpret_cast<const u32x4*>(kg + (int64_t)tok * kv_row + 8 * col)
-                             : u32x4{0, 0, 0, 0};
+      const int ch = tid + NTH * u, t = ch / CPR, col = ch % CPR;
+      const int tok = min(kv0 + t, kv_end - 1);
+      rk[u] = *reinterpret_cast<const u32x4*>(kg + (int64_t)tok * kv_row + 8 * col);
     }
+  };
+  auto gload_v = [&](int kv0) {
     if (tid < VTH) {
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
-        const int tok = kv0 + 4 * v_tg + u;
-        vreg[u] = tok < kv_end
-                      ? *reinterpret_cast<const u32x4*>(vg + (int64_t)tok * kv_row + 8 * v_col)
-                      : u32x4{0, 0, 0, 0};
+        const int tok = min(kv0 + 4 * v_tg + u, kv_end - 1);
+        rv[u] = *reinterpret_cast<const u32x4*>(vg + (int64_t)tok * kv_row + 8 * v_col);
       }
     }
   };
-  auto lstore = [&]() {
+  auto lstore_k = [&](int buf) {
 #pragma unroll
     for (int u = 0; u < KCH; ++u) {
-      const int ch = tid + 256 * u, t = ch / CPR, col = ch % CPR;
-      *reinterpret_cast<u32x4*>(&sK[t * KP + 8 * col]) = kreg[u];
+      const int ch = tid + NTH * u, t = ch / CPR, col = ch % CPR;
+      *reinterpret_cast<u32x4*>(&sK[buf][t * KP + 8 * col]) = rk[u];
     }
+  };
+  auto lstore_v = [&](int buf) {
     if (tid < VTH) {
+      // 4 tokens x 8 dims -> 8 dim rows of 4 tokens: byte permutes pick the
+      // low (even dim) or high (odd dim) bf16 of two token words.
 #pragma unroll
-      for (int i = 0; i < 8; ++i) {  // dim 8*v_col + i, tokens 4*v_tg .. +3
-        const int wd = i >> 1, sh = (i & 1) * 16;
-        const uint32_t t0 = (vreg[0][wd] >> sh) & 0xffffu, t1 = (vreg[1][wd] >> sh) & 0xffffu;
-        const uint32_t t2 = (vreg[2][wd] >> sh) & 0xffffu, t3 = (vreg[3][wd] >> sh) & 0xffffu;
+      for (int i = 0; i < 8; ++i) {
+        const int wd = i >> 1;
+        const uint32_t sel = (i & 1) ? 0x07060302u : 0x05040100u;
         u32x2 x;
-        x[0] = t0 | (t1 << 16);
-        x[1] = t2 | (t3 << 16);
-        *reinterpret_cast<u32x2*>(&sV[(8 * v_col + i) * VP + 4 * v_tg]) = x;
+        x[0] = __builtin_amdgcn_perm(rv[1][wd], rv[0][wd], sel);
+        x[1] = __builtin_amdgcn_perm(rv[3][wd], rv[2][wd], sel);
+        *reinterpret_cast<u32x2*>(&sV[buf][(8 * v_col + i) * VP + 4 * v_tg]) = x;
       }
     }
   };
 
-  gload(0);
-  lstore();
-  __syncthreads();
+  // Scores stay raw until the exponent: p = 2^(s*c - m) as one fma, with the
+  // running max m kept in the scaled domain.  For c <= 0 the scores are scaled
+  // first and c is taken as 1, so the max is always taken on the exponent.
+  const float c_in = a.scale_log2;
+  const bool pos_scale = c_in > 0.f;
+  const float c_eff = pos_scale ? c_in : 1.f;
+  // Lazy rescaling: the running max only moves when a new tile raises it by
+  // more than kLazy (log2 units), so P <= 2^kLazy and the O/l rescale is
+  // skipped for most tiles.  The result is the same softmax (the final O/l
+  // uses the same m throughout).
+  constexpr float kLazy = 8.f;
 
-  for (int j = 0; j < ntiles; ++j) {
-    const int kv0 = j * BN;
-    if (j + 1 < ntiles) gload(kv0 + BN);
-    const bool skip = !wave_active || kv0 > row_w + 31;  // whole tile above this wave's rows
-    if (!skip) {
-      f32x16 st[2];
+  f32x16 st[2];   // S^T of the tile being scored
+  bf16x8 pb[4];   // P^T of the tile waiting for its P.V product
+  auto skip_tile = [&](int j) { return !wave_active || j * BN > row_w + 31; };
+
+  // Operands are read from LDS a whole k-chain (or e-row) at a time before the
+  // MFMAs that use them, so LDS latency overlaps the matrix work instead of
+  // stalling every MFMA.
+  // Operands are read from LDS ahead of the MFMAs that use them (scheduling
+  // groups pin the order), so LDS latency overlaps the matrix work instead of
+  // stalling every MFMA.
+  constexpr int kDsRead = 0x100, kMfma = 0x008;
+  auto qk = [&](int j) {  // st = S^T of tile j, K from sK[j & 1]
+    bf16x8 ka[2][KS];
 #pragma unroll
-      for (int tt = 0; tt < 2; ++tt) {
+    for (int tt = 0; tt < 2; ++tt) {
+      const uint16_t* kr = &sK[j & 1][(32 * tt + (l & 31)) * KP + 8 * hi];
 #pragma unroll
-        for (int x = 0; x < 16; ++x) st[tt][x] = 0.f;
-        const uint16_t* kr = &sK[(32 * tt + (l & 31)) * KP + 8 * hi];
+      for (int ks = 0; ks < KS; ++ks) ka[tt][ks] = *reinterpret_cast<const bf16x8*>(kr + 16 * ks);
+    }
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
-          const bf16x8 ka = *reinterpret_cast<const bf16x8*>(kr + 16 * ks);
-          st[tt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka, qop[ks], st[tt], 0, 0, 0);
-        }
+    for (int tt = 0; tt < 2; ++tt)
+#pragma unroll
+      for (int x = 0; x < 16; ++x) st[tt][x] = 0.f;
+    // the two accumulator chains alternate so consecutive MFMAs are independent
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+      for (int tt = 0; tt < 2; ++tt)
+        st[tt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[tt][ks], qop[ks], st[tt], 0, 0, 0);
+    // reads run two k-steps ahead of the MFMAs that consume them
+    __builtin_amdgcn_sched_group_barrier(kDsRead, 4, 0);
+#pragma unroll
+    for (int ks = 0; ks < KS - 2; ++ks) {
+      __builtin_amdgcn_sched_group_barrier(kMfma, 2, 0);
+      __builtin_amdgcn_sched_group_barrier(kDsRead, 2, 0);
+    }
+    __builtin_amdgcn_sched_group_barrier(kMfma, 4, 0);
+  };
+  auto pv = [&](int j) {  // O^T += V^T P^T of tile j, V from sV[j & 1]
+    // k-step (tt, hh): k-slot 8hi + jj <-> token 32tt + 16hh + 8(jj/4) + 4hi + jj%4
+    u32x4 va[4][ET];
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) {
+      const int tcol = 32 * (kk >> 1) + 16 * (kk & 1) + 4 * hi;
+#pragma unroll
+      for (int et = 0; et < ET; ++et) {
+        const uint16_t* vr = &sV[j & 1][(32 * et + (l & 31)) * VP + tcol];
+        const u32x2 lo = *reinterpret_cast<const u32x2*>(vr);
+        const u32x2 hi2 = *reinterpret_cast<const u32x2*>(vr + 8);
+        va[kk][et] = u32x4{lo[0], lo[1], hi2[0], hi2[1]};
       }
-      // lane holds S^T[t = kv0 + 32tt + 8(x/4) + 4hi + x%4][q = myq]
-      const bool need_mask = (kv0 + BN - 1 > row_w) || (kv0 + BN > kv_end);
-      float mx = -INFINITY;
+    }
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk)
+#pragma unroll
+      for (int et = 0; et < ET; ++et)
+        oacc[et] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, va[kk][et]),
+                                                           pb[kk], oacc[et], 0, 0, 0);
+    // one k-step of reads ahead of its MFMAs
+    __builtin_amdgcn_sched_group_barrier(kDsRead, ET, 0);
+#pragma unroll
+    for (int kk = 0; kk < 3; ++kk)
+#pragma unroll
+      for (int et = 0; et < ET; ++et) {
+        __builtin_amdgcn_sched_group_barrier(kMfma, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(kDsRead, 1, 0);
+      }
+    __builtin_amdgcn_sched_group_barrier(kMfma, ET, 0);
+  };
+  auto softmax = [&](int j) {  // st (tile j) -> pb, updating m_run, l_run (and O lazily)
+    const int kv0 = j * BN;
+    // lane holds S^T[t = kv0 + 32tt + 8(x/4) + 4hi + x%4][q = myq]
+    if (!pos_scale) {
+#pragma unroll
+      for (int tt = 0; tt < 2; ++tt) st[tt] *= c_in;
+    }
+    if ((kv0 + BN - 1 > row_w) || (kv0 + BN > kv_end)) {  // diagonal or ragged tile
 #pragma unroll
       for (int tt = 0; tt < 2; ++tt)
 #pragma unroll
         for (int x = 0; x < 16; ++x) {
-          float y = st[tt][x] * a.scale_log2;
-          if (need_mask) {
-            const int t = kv0 + 32 * tt + 8 * (x >> 2) + 4 * hi + (x & 3);
-            if (t > myq || t >= kv_end) y = -INFINITY;
-          }
-          st[tt][x] = y;
-          mx = fmaxf(mx, y);
+          const int t = kv0 + 32 * tt + 8 * (x >> 2) + 4 * hi + (x & 3);
+          if (t > myq || t >= kv_end) st[tt][x] = -INFINITY;
         }
-      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-      const float m_new = fmaxf(m_run, mx);  // finite: key 0 is seen in the first tile
+    }
+    float mx = fmaxf(st[0][0], st[1][0]);
+#pragma unroll
+    for (int x = 1; x < 16; ++x) mx = fmaxf(mx, fmaxf(st[0][x], st[1][x]));
+    {
+      const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx),
+                                                       false, false);
+      mx = fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1]));  // max with lane ^ 32
+    }
+    const float m_tile = mx * c_eff;  // finite: key 0 is seen in the first tile
+    if (__ballot(m_tile > m_run + kLazy)) {  // wave-uniform
+      const float m_new = fmaxf(m_run, m_tile);
       const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
-      float psum = 0.f;
-      bf16x8 pb[4];  // B operands of the four P.V k-steps
-#pragma unroll
-      for (int tt = 0; tt < 2; ++tt)
-#pragma unroll
-        for (int x = 0; x < 16; ++x) {
-          const float p = __builtin_amdgcn_exp2f(st[tt][x] - m_new);
-          psum += p;
-          pb[2 * tt + (x >> 3)][x & 7] = (__bf16)p;
-        }
-      l_run = l_run * alpha + psum;
       m_run = m_new;
+      l_run *= alpha;
 #pragma unroll
       for (int et = 0; et < ET; ++et) oacc[et] *= alpha;
-      // k-step (tt, hh): k-slot 8hi + jj <-> token 32tt + 16hh + 8(jj/4) + 4hi + jj%4
+    }
+    float psum = 0.f;
 #pragma unroll
-      for (int kk = 0; kk < 4; ++kk) {
-        const int tcol = 32 * (kk >> 1) + 16 * (kk & 1) + 4 * hi;
+    for (int tt = 0; tt < 2; ++tt)
 #pragma unroll
-        for (int et = 0; et < ET; ++et) {
-          const uint16_t* vr = &sV[(32 * et + (l & 31)) * VP + tcol];
-          const u32x2 lo = *reinterpret_cast<const u32x2*>(vr);
-          const u32x2 hi2 = *reinterpret_cast<const u32x2*>(vr + 8);
-          const u32x4 va = {lo[0], lo[1], hi2[0], hi2[1]};
-          oacc[et] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, va),
-                                                             pb[kk], oacc[et], 0, 0, 0);
-        }
+      for (int x = 0; x < 16; ++x) {
+        const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(st[tt][x], c_eff, -m_run));
+        psum += p;
+        pb[2 * tt + (x >> 3)][x & 7] = (__bf16)p;
       }
-    }
+    l_run += psum;
+  };
+
+  // Pipeline: K runs one tile ahead of V in LDS (buffers alternate by tile
+  // parity).  Iteration j issues the Q.K MFMAs of tile j+1 and the P.V MFMAs of
+  // tile j back to back, then computes the softmax of tile j+1 on the VALU
+  // while those MFMAs drain, so matrix and vector work of one wave overlap.
+  gload_k(0);
+  gload_v(0);
+  lstore_k(0);
+  lstore_v(0);
+  gload_k(BN);
+  lstore_k(1);
+  __syncthreads();
+  if (!skip_tile(0)) {
+    qk(0);
+    softmax(0);
+  }
+  __syncthreads();  // everyone has read K tile 0 before its buffer is refilled
+  for (int j = 0; j < ntiles; ++j) {
+    gload_k((j + 2) * BN);  // unconditional: past the end it re-reads the last row
+    gload_v((j + 1) * BN);
+    const bool more = j + 1 < ntiles;
+    if (more && !skip_tile(j + 1)) qk(j + 1);
+    if (!skip_tile(j)) pv(j);
+    if (more && !skip_tile(j + 1)) softmax(j + 1);
+    if (j + 2 < ntiles) lstore_k(j & 1);        // K tile j+2 replaces K tile j
+    if (more) lstore_v((j + 1) & 1);             // V tile j+1 replaces V tile j-1
     __syncthreads();
-    if (j + 1 < ntiles) {
-      lstore();
-      __syncthreads();
-    }
   }
 
   if (!wave_active || myq >= L) return;
