@@ -8,11 +8,11 @@
  * with the softmax scale as an argument (Eq. 1 prints no scale; callers
  * normally pass 1/sqrt(head_dim)).  A P-instance runs a variable-length causal
  * prefill over a batch of prompts (the per-request input lengths of the
- * length-aware batching of Sec. III-C, Alg. 1) and writes K/V into a paged
- * cache (the KV-cache blocks of Sec. I and Sec. IV-C); a D-instance runs
+ * length-aware batching of Sec. IV-C, Alg. 1) and writes K/V into a paged
+ * cache (the KV-cache blocks of Sec. I and Sec. V-C); a D-instance runs
  * single-query attention over each request's cached context (decode is
- * memory bound, Sec. III-B, Eq. 12); a prefill-completed request is handed to
- * a D-instance together with its KV cache (Sec. III-B, Sec. IV-C), for which
+ * memory bound, Sec. IV-B, Eq. 12); a prefill-completed request is handed to
+ * a D-instance together with its KV cache (Sec. IV-B, Sec. V-C), for which
  * the packer gathers the request's pages into one contiguous buffer.
  *
  * Conventions shared by every entry point
@@ -135,7 +135,7 @@ size_t dopd_decode_workspace_size(const dopd_attn_shape* shape,
 
 /*
  * Handoff pack of prefill-completed requests (the KV blocks that the
- * Connector moves from a P-instance to a D-instance, Sec. IV-C): handoff n
+ * Connector moves from a P-instance to a D-instance, Sec. V-C): handoff n
  * (request req_ids[n], seq_lens[n] cached tokens) is written to
  *   out[out_offsets[n] + (((layer*2 + c)*Hkv + h)*len + t)*d + e]
  * with c = 0 for K and 1 for V, i.e. (layer, K/V, head, token, dim) order.

@@ -15,7 +15,7 @@
  *   over the j < ctx cached tokens of a request for decode.
  *
  *   The K/V cache lives in fixed-size blocks addressed per request (the
- *   paper's KV-cache blocks moved between instances, Sec. I and Sec. IV-C).
+ *   paper's KV-cache blocks moved between instances, Sec. I and Sec. V-C).
  *   Layouts: k_pool[page][Hkv][16][d], v_pool[page][Hkv][d][16];
  *   page_table[r][i] = physical page of logical page i of request r.
  *

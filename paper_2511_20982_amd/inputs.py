@@ -12,15 +12,15 @@ Storage conventions (shared by every consumer):
 * Fresh tokens (prefill inputs, new decode tokens) are token-major:
   Q ``[T][Hq][d]``, K/V ``[T][Hkv][d]``.
 * Paged cache, one pool per layer (the K/V cache blocks of the paper's
-  disaggregated design, Sec. I and the Connector of Sec. IV):
+  disaggregated design, Sec. I and the Connector of Sec. V-C):
   ``k_pool[page][Hkv][page_size][d]`` (token-major within a page) and
   ``v_pool[page][Hkv][d][page_size]`` (dim-major within a page).
 * ``page_table[r][i]`` is the physical page of request ``r``'s logical page
   ``i``; padding is -1.
 * Unused pages and unused tail slots hold NaN (bf16 0x7FC0, fp32 quiet NaN).
 
-Length laws (the paper's heavy-tailed input lengths, Sec. III-A, stand-ins
-for the production traces of the evaluation, Sec. V-A):
+Length laws (the paper's heavy-tailed input lengths, Sec. IV-A and Eq. 9,
+stand-ins for the production traces of the evaluation, Sec. VI-A):
 lognormal ``clip(rint(exp(N(ln median, sigma^2))), lo, hi)`` and a bimodal
 short/long mix.
 """
