@@ -175,8 +175,26 @@ dopd_status dopd_prefill_attn(const dopd_attn_shape* s, const void* q, const voi
   a.hkv = hkv;
   a.max_tiles = (max_len + dopd::kPfBM - 1) / dopd::kPfBM;
   a.scale_log2 = s->softmax_scale * dopd::kLog2e;
-  const int64_t blocks = bf16_items * hq;
-  if (blocks > INT32_MAX) return DOPD_ERR_INVALID_SHAPE;
+  const int64_t items = bf16_items * hq;
+  if (items > INT32_MAX / 2) return DOPD_ERR_INVALID_SHAPE;
+  int64_t blocks = items;
+  a.xcd_order = 0;
+  a.n_items = (int)items;
+  a.tiles_total = (int)bf16_items;
+  a.per_xcd = 0;
+  std::memset(a.ord, 0, sizeof(a.ord));
+  if (nreq <= dopd::kPfMaxOrdered) {
+    // requests by decreasing length (stable), dealt to XCDs in contiguous slices
+    int order[dopd::kPfMaxOrdered];
+    for (int32_t r = 0; r < nreq; ++r) order[r] = r;
+    std::stable_sort(order, order + nreq, [&](int x, int y) {
+      return cu_host[x + 1] - cu_host[x] > cu_host[y + 1] - cu_host[y];
+    });
+    for (int32_t r = 0; r < nreq; ++r) a.ord[r] = (uint8_t)order[r];
+    a.xcd_order = 1;
+    a.per_xcd = (int)((items + dopd::kNumXcd - 1) / dopd::kNumXcd);
+    blocks = (int64_t)a.per_xcd * dopd::kNumXcd;
+  }
   if (d == 64)
     hipLaunchKernelGGL(dopd::prefill_bf16_kernel<64>, dim3((unsigned)blocks), dim3(dopd::kPfThreads), 0, strm, a);
   else

@@ -1,21 +1,25 @@
 // Variable-length causal prefill attention, bf16 in / fp32 accumulate, gfx950.
 //
-// Workgroup = 8 waves = one (q tile of 256 rows, request, query head); each
-// wave owns 32 query rows.  K/V tiles of 64 tokens are staged in LDS (K
+// Workgroup = 4 waves = one (q tile of 128 rows, request, query head); each
+// wave owns 32 query rows; two workgroups share a CU, so the two waves on a
+// SIMD run out of phase.  K/V stages of 64 keys are staged in LDS (K
 // token-major, V transposed to dim-major on the way in), double-buffered, and
-// shared by the eight waves.  Per tile and wave:
+// shared by the four waves.  Per stage and wave:
 //
 //   S^T[64 tok][32 q] = K[64][d] . Q^T[d][32]       2 x (d/16) v_mfma_f32_32x32x16_bf16
 //   O^T[d][32 q]     += V^T[d][64] . P^T[64][32]    (d/32) x 4  v_mfma_f32_32x32x16_bf16
 //
 // Computing the transposed products keeps a whole query row inside one lane
-// pair, so the online-softmax row max and row sum need a single cross-lane
-// step, and the MFMA output of S^T is already the B operand of the P.V MFMA
-// (the token order of the contraction is matched on the V^T LDS reads).
-// Scores are scaled into the exp2 domain; only tiles on the diagonal or past
-// the end of the request are masked, with a select (never a multiply).
-// Work items are issued heaviest first (latest q tiles of every request
-// first) so long prompts do not leave a tail.
+// pair, so the online-softmax row max needs one lane swap, and the MFMA output
+// of S^T is already the B operand of the P.V MFMA (the token order of the
+// contraction is matched on the V^T LDS reads).  LDS operands are read ahead
+// of their MFMAs (pinned scheduling groups); rows are padded so that reads and
+// writes are free of bank conflicts.  Scores are scaled into the exp2 domain
+// inside one fma; only stages on the diagonal or past the end of the request
+// are masked, with a select (never a multiply).
+// Work order: with at most 64 requests, each XCD takes a contiguous slice of
+// (KV head, request longest first, q tile descending) so the q tiles that read
+// the same K/V run together under one L2; otherwise heaviest q tiles first.
 #pragma once
 #include "common.hpp"
 
@@ -30,11 +34,21 @@ struct PrefillArgs {
   const int32_t* cu;   // [nreq + 1]
   int nreq, hq, hkv, max_tiles;
   float scale_log2;
+  // XCD-aware order (used when nreq <= kPfMaxOrdered): the work list is
+  // (KV head, request by decreasing length, q tile descending, query head of
+  // the group); XCD x = workgroup % 8 takes the contiguous slice
+  // [x * per_xcd, (x+1) * per_xcd), so the q tiles that share a request's K/V
+  // run together on one XCD and share its L2.
+  int xcd_order, n_items, per_xcd, tiles_total;
+  uint8_t ord[64];     // requests by decreasing length
 };
 
-constexpr int kPfBM = 256;  // query rows per workgroup (32 per wave)
+constexpr int kPfMaxOrdered = 64;
+constexpr int kNumXcd = 8;
+
+constexpr int kPfBM = 128;  // query rows per workgroup (32 per wave)
 constexpr int kPfThreads = kPfBM / 32 * 64;
-constexpr int kPfBN = 64;   // keys per LDS tile
+constexpr int kPfBN = 64;   // keys per LDS stage (computed as 64-key sub-tiles)
 
 // Number of BM-row q tiles of request rr.
 __device__ __forceinline__ int pf_tiles(const int32_t* cu, int rr) {
@@ -43,8 +57,8 @@ __device__ __forceinline__ int pf_tiles(const int32_t* cu, int rr) {
 
 // Maps a workgroup index to (q tile, request, head), q tiles in decreasing
 // index order (tile i of a request attends to ~ (i+1) key tiles).
-__device__ __forceinline__ bool pf_find_item(const PrefillArgs& a, int b, int& tile, int& req,
-                                             int& head) {
+__device__ __forceinline__ bool pf_find_item_lpt(const PrefillArgs& a, int b, int& tile,
+                                                 int& req, int& head) {
   const int l = lane_id();
   const bool small = a.nreq <= 64;
   const int nt_l = (small && l < a.nreq) ? pf_tiles(a.cu, l) : 0;
@@ -70,11 +84,41 @@ __device__ __forceinline__ bool pf_find_item(const PrefillArgs& a, int b, int& t
   return false;
 }
 
+// XCD-aware mapping (see PrefillArgs).
+__device__ __forceinline__ bool pf_find_item_xcd(const PrefillArgs& a, int b, int& tile,
+                                                 int& req, int& head) {
+  const int x = b % kNumXcd, j = b / kNumXcd;
+  const int n = x * a.per_xcd + j;
+  if (j >= a.per_xcd || n >= a.n_items) return false;
+  const int g = a.hq / a.hkv;
+  const int per_kvh = g * a.tiles_total;
+  const int kvh = n / per_kvh;
+  const int rem = n - kvh * per_kvh;
+  const int l = lane_id();
+  const int rr = l < a.nreq ? a.ord[l] : 0;
+  const int nt = l < a.nreq ? pf_tiles(a.cu, rr) : 0;
+  const int cnt = g * nt;
+  const int incl = wave_inclusive_scan(cnt);
+  const unsigned long long hit = __ballot(rem < incl);
+  const int k = __ffsll((long long)hit) - 1;
+  const int local = rem - __shfl(incl - cnt, k, 64);
+  req = __shfl(rr, k, 64);
+  tile = __shfl(nt, k, 64) - 1 - local / g;
+  head = kvh * g + local % g;
+  return true;
+}
+
+__device__ __forceinline__ bool pf_find_item(const PrefillArgs& a, int b, int& tile, int& req,
+                                             int& head) {
+  return a.xcd_order ? pf_find_item_xcd(a, b, tile, req, head)
+                     : pf_find_item_lpt(a, b, tile, req, head);
+}
+
 template <int D>
 __global__ __launch_bounds__(kPfThreads, 2) void prefill_bf16_kernel(PrefillArgs a) {
-  constexpr int BM = kPfBM, BN = kPfBN;
+  constexpr int BM = kPfBM, BN = kPfBN, SUB = 64;
   constexpr int KP = D + 8;      // padded K row (elements)
-  constexpr int VP = BN + 8;     // padded V^T row (elements)
+  constexpr int VP = BN + 4;     // padded V^T row (elements): 2 dwords of skew per row
   constexpr int KS = D / 16;     // k-steps of the QK MFMA
   constexpr int ET = D / 32;     // O^T tiles of 32 dims
   constexpr int CPR = D / 8;     // 16-byte chunks per K/V row
@@ -120,7 +164,7 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_bf16_kernel(PrefillArgs
   const uint16_t* kg = a.k + (int64_t)seq0 * kv_row + (int64_t)kvh * D;
   const uint16_t* vg = a.v + (int64_t)seq0 * kv_row + (int64_t)kvh * D;
 
-  const int v_tg = tid % 16, v_col = tid / 16;  // V staging: tokens 4*v_tg.., dims 8*v_col..
+  const int v_tg = tid % (BN / 4), v_col = tid / (BN / 4);  // V staging: tokens 4*v_tg.., dims 8*v_col..
   u32x4 rk[KCH], rv[4];                          // global -> LDS staging registers
   // Rows past the end of the request are read from its last token instead
   // (always in bounds and finite); their scores are masked and their P is 0.
@@ -175,23 +219,20 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_bf16_kernel(PrefillArgs
   // skipped for most tiles.  The result is the same softmax (the final O/l
   // uses the same m throughout).
   constexpr float kLazy = 8.f;
+  // Last key this lane's row may see (causal and end of request).
+  const int last_key = min(myq, kv_end - 1);
 
-  f32x16 st[2];   // S^T of the tile being scored
-  bf16x8 pb[4];   // P^T of the tile waiting for its P.V product
-  auto skip_tile = [&](int j) { return !wave_active || j * BN > row_w + 31; };
-
-  // Operands are read from LDS a whole k-chain (or e-row) at a time before the
-  // MFMAs that use them, so LDS latency overlaps the matrix work instead of
-  // stalling every MFMA.
-  // Operands are read from LDS ahead of the MFMAs that use them (scheduling
-  // groups pin the order), so LDS latency overlaps the matrix work instead of
-  // stalling every MFMA.
+  f32x16 st[2];   // S^T of the 64-key sub-tile being scored
+  bf16x8 pb[4];   // its P^T, the B operands of the four P.V k-steps
   constexpr int kDsRead = 0x100, kMfma = 0x008;
-  auto qk = [&](int j) {  // st = S^T of tile j, K from sK[j & 1]
+
+  // Operands are read from LDS ahead of the MFMAs that use them (scheduling
+  // groups pin the order), so LDS latency overlaps the matrix work.
+  auto qk = [&](int buf, int sub) {  // st = S^T of keys [64 sub, 64 sub + 64) of the stage
     bf16x8 ka[2][KS];
 #pragma unroll
     for (int tt = 0; tt < 2; ++tt) {
-      const uint16_t* kr = &sK[j & 1][(32 * tt + (l & 31)) * KP + 8 * hi];
+      const uint16_t* kr = &sK[buf][(SUB * sub + 32 * tt + (l & 31)) * KP + 8 * hi];
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) ka[tt][ks] = *reinterpret_cast<const bf16x8*>(kr + 16 * ks);
     }
@@ -199,13 +240,11 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_bf16_kernel(PrefillArgs
     for (int tt = 0; tt < 2; ++tt)
 #pragma unroll
       for (int x = 0; x < 16; ++x) st[tt][x] = 0.f;
-    // the two accumulator chains alternate so consecutive MFMAs are independent
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks)
 #pragma unroll
       for (int tt = 0; tt < 2; ++tt)
         st[tt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[tt][ks], qop[ks], st[tt], 0, 0, 0);
-    // reads run two k-steps ahead of the MFMAs that consume them
     __builtin_amdgcn_sched_group_barrier(kDsRead, 4, 0);
 #pragma unroll
     for (int ks = 0; ks < KS - 2; ++ks) {
@@ -214,15 +253,15 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_bf16_kernel(PrefillArgs
     }
     __builtin_amdgcn_sched_group_barrier(kMfma, 4, 0);
   };
-  auto pv = [&](int j) {  // O^T += V^T P^T of tile j, V from sV[j & 1]
-    // k-step (tt, hh): k-slot 8hi + jj <-> token 32tt + 16hh + 8(jj/4) + 4hi + jj%4
+  auto pv = [&](int buf, int sub) {  // O^T += V^T P^T of the sub-tile
+    // k-step (tt, hh): k-slot 8hi + jj <-> key 32tt + 16hh + 8(jj/4) + 4hi + jj%4
     u32x4 va[4][ET];
 #pragma unroll
     for (int kk = 0; kk < 4; ++kk) {
-      const int tcol = 32 * (kk >> 1) + 16 * (kk & 1) + 4 * hi;
+      const int tcol = SUB * sub + 32 * (kk >> 1) + 16 * (kk & 1) + 4 * hi;
 #pragma unroll
       for (int et = 0; et < ET; ++et) {
-        const uint16_t* vr = &sV[j & 1][(32 * et + (l & 31)) * VP + tcol];
+        const uint16_t* vr = &sV[buf][(32 * et + (l & 31)) * VP + tcol];
         const u32x2 lo = *reinterpret_cast<const u32x2*>(vr);
         const u32x2 hi2 = *reinterpret_cast<const u32x2*>(vr + 8);
         va[kk][et] = u32x4{lo[0], lo[1], hi2[0], hi2[1]};
@@ -234,7 +273,6 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_bf16_kernel(PrefillArgs
       for (int et = 0; et < ET; ++et)
         oacc[et] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, va[kk][et]),
                                                            pb[kk], oacc[et], 0, 0, 0);
-    // one k-step of reads ahead of its MFMAs
     __builtin_amdgcn_sched_group_barrier(kDsRead, ET, 0);
 #pragma unroll
     for (int kk = 0; kk < 3; ++kk)
@@ -245,21 +283,19 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_bf16_kernel(PrefillArgs
       }
     __builtin_amdgcn_sched_group_barrier(kMfma, ET, 0);
   };
-  auto softmax = [&](int j) {  // st (tile j) -> pb, updating m_run, l_run (and O lazily)
-    const int kv0 = j * BN;
+  auto softmax = [&](int kv0) {  // st (keys kv0 ..) -> pb, updating m_run, l_run (and O lazily)
     // lane holds S^T[t = kv0 + 32tt + 8(x/4) + 4hi + x%4][q = myq]
     if (!pos_scale) {
 #pragma unroll
       for (int tt = 0; tt < 2; ++tt) st[tt] *= c_in;
     }
-    if ((kv0 + BN - 1 > row_w) || (kv0 + BN > kv_end)) {  // diagonal or ragged tile
+    if (kv0 + SUB - 1 > row_w || kv0 + SUB > kv_end) {  // diagonal or ragged sub-tile
+      const int lim = last_key - kv0 - 4 * hi;  // mask offsets beyond it
 #pragma unroll
       for (int tt = 0; tt < 2; ++tt)
 #pragma unroll
-        for (int x = 0; x < 16; ++x) {
-          const int t = kv0 + 32 * tt + 8 * (x >> 2) + 4 * hi + (x & 3);
-          if (t > myq || t >= kv_end) st[tt][x] = -INFINITY;
-        }
+        for (int x = 0; x < 16; ++x)
+          if (32 * tt + 8 * (x >> 2) + (x & 3) > lim) st[tt][x] = -INFINITY;
     }
     float mx = fmaxf(st[0][0], st[1][0]);
 #pragma unroll
@@ -269,7 +305,7 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_bf16_kernel(PrefillArgs
                                                        false, false);
       mx = fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1]));  // max with lane ^ 32
     }
-    const float m_tile = mx * c_eff;  // finite: key 0 is seen in the first tile
+    const float m_tile = mx * c_eff;  // finite: key 0 is seen in the first sub-tile
     if (__ballot(m_tile > m_run + kLazy)) {  // wave-uniform
       const float m_new = fmaxf(m_run, m_tile);
       const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
@@ -290,31 +326,31 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_bf16_kernel(PrefillArgs
     l_run += psum;
   };
 
-  // Pipeline: K runs one tile ahead of V in LDS (buffers alternate by tile
-  // parity).  Iteration j issues the Q.K MFMAs of tile j+1 and the P.V MFMAs of
-  // tile j back to back, then computes the softmax of tile j+1 on the VALU
-  // while those MFMAs drain, so matrix and vector work of one wave overlap.
+  // Stages of 128 keys, double-buffered in LDS; the next stage's global loads
+  // are in flight while the current one is computed as two 64-key sub-tiles;
+  // one barrier per stage.
   gload_k(0);
   gload_v(0);
   lstore_k(0);
   lstore_v(0);
-  gload_k(BN);
-  lstore_k(1);
   __syncthreads();
-  if (!skip_tile(0)) {
-    qk(0);
-    softmax(0);
-  }
-  __syncthreads();  // everyone has read K tile 0 before its buffer is refilled
   for (int j = 0; j < ntiles; ++j) {
-    gload_k((j + 2) * BN);  // unconditional: past the end it re-reads the last row
+    const int cur = j & 1;
+    gload_k((j + 1) * BN);  // unconditional: past the end it re-reads the last row
     gload_v((j + 1) * BN);
-    const bool more = j + 1 < ntiles;
-    if (more && !skip_tile(j + 1)) qk(j + 1);
-    if (!skip_tile(j)) pv(j);
-    if (more && !skip_tile(j + 1)) softmax(j + 1);
-    if (j + 2 < ntiles) lstore_k(j & 1);        // K tile j+2 replaces K tile j
-    if (more) lstore_v((j + 1) & 1);             // V tile j+1 replaces V tile j-1
+#pragma unroll
+    for (int sub = 0; sub < BN / SUB; ++sub) {
+      const int kv0 = j * BN + SUB * sub;
+      if (wave_active && kv0 < kv_end && kv0 <= row_w + 31) {  // some key visible to this wave
+        qk(cur, sub);
+        softmax(kv0);
+        pv(cur, sub);
+      }
+    }
+    if (j + 1 < ntiles) {
+      lstore_k(cur ^ 1);  // that buffer was last read before the previous barrier
+      lstore_v(cur ^ 1);
+    }
     __syncthreads();
   }
 
