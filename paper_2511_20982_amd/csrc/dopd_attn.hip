@@ -215,17 +215,29 @@ dopd_status dopd_kv_write(const dopd_attn_shape* s, const void* k_new, const voi
     return DOPD_ERR_NULL_POINTER;
   // Touched pages per request <= n/16 + 2, so this bounds the item count.
   const int64_t blocks = (int64_t)total_new / dopd::kPage + 2 * (int64_t)nreq + 1;
-  if (blocks > INT32_MAX) return DOPD_ERR_INVALID_SHAPE;
+  if (blocks > INT32_MAX || s->num_kv_heads > 65535) return DOPD_ERR_INVALID_SHAPE;
   hipStream_t strm = as_stream(stream);
   const int hkv = s->num_kv_heads, d = s->head_dim;
-  if (s->dtype == DOPD_BF16)
-    hipLaunchKernelGGL(dopd::kv_write_kernel<uint16_t>, dim3((unsigned)blocks), dim3(256), 0, strm,
-                       (const uint16_t*)k_new, (const uint16_t*)v_new, (uint16_t*)k_pool,
-                       (uint16_t*)v_pool, pt, pt_stride, cu_new, start_pos, nreq, hkv, d);
-  else
-    hipLaunchKernelGGL(dopd::kv_write_kernel<uint32_t>, dim3((unsigned)blocks), dim3(256), 0, strm,
-                       (const uint32_t*)k_new, (const uint32_t*)v_new, (uint32_t*)k_pool,
-                       (uint32_t*)v_pool, pt, pt_stride, cu_new, start_pos, nreq, hkv, d);
+  const dim3 grid((unsigned)blocks, (unsigned)hkv), block(dopd::kKvwThreads);
+  if (s->dtype == DOPD_BF16) {
+    auto* kn = (const uint16_t*)k_new; auto* vn = (const uint16_t*)v_new;
+    auto* kp = (uint16_t*)k_pool; auto* vp = (uint16_t*)v_pool;
+    if (d == 64)
+      hipLaunchKernelGGL((dopd::kv_write_kernel<uint16_t, 64>), grid, block, 0, strm, kn, vn, kp, vp, pt,
+                         pt_stride, cu_new, start_pos, nreq, hkv);
+    else
+      hipLaunchKernelGGL((dopd::kv_write_kernel<uint16_t, 128>), grid, block, 0, strm, kn, vn, kp, vp, pt,
+                         pt_stride, cu_new, start_pos, nreq, hkv);
+  } else {
+    auto* kn = (const uint32_t*)k_new; auto* vn = (const uint32_t*)v_new;
+    auto* kp = (uint32_t*)k_pool; auto* vp = (uint32_t*)v_pool;
+    if (d == 64)
+      hipLaunchKernelGGL((dopd::kv_write_kernel<uint32_t, 64>), grid, block, 0, strm, kn, vn, kp, vp, pt,
+                         pt_stride, cu_new, start_pos, nreq, hkv);
+    else
+      hipLaunchKernelGGL((dopd::kv_write_kernel<uint32_t, 128>), grid, block, 0, strm, kn, vn, kp, vp, pt,
+                         pt_stride, cu_new, start_pos, nreq, hkv);
+  }
   return launch_status();
 }
 
