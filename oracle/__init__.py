@@ -35,8 +35,9 @@ def _lib():
         lib.oracle_decode.argtypes = [i32, i32, i32, i32, C.c_float, P, P, P, P, i32, P, i32, P, P]
         lib.oracle_kv_write.argtypes = [i32, i32, i32, P, P, P, P, P, i32, P, P, i32]
         lib.oracle_pack.argtypes = [i32, i32, i32, i32, P, P, i32, P, i32, P, P, P, i32, P]
+        lib.oracle_unpack.argtypes = [i32, i32, i32, i32, P, P, P, P, i32, P, P, i32, P, i32]
         for f in (lib.oracle_prefill, lib.oracle_prefill_rows, lib.oracle_decode,
-                  lib.oracle_kv_write, lib.oracle_pack):
+                  lib.oracle_kv_write, lib.oracle_pack, lib.oracle_unpack):
             f.restype = i32
         _LIB = lib
     return _LIB
@@ -132,3 +133,16 @@ def pack(k_pool, v_pool, num_layers, page_table, req_ids, seq_lens, out_offsets)
     _lib().oracle_pack(k_pool.itemsize, hkv, d, num_layers, _p(k_pool), _p(v_pool), num_pages,
                        _p(pt), pt.shape[1], _p(req), _p(lens), _p(off), len(req), _p(out))
     return out
+
+
+def unpack(buf, in_offsets, req_ids, seq_lens, k_pool, v_pool, num_layers, page_table):
+    """Returns new (k_pool, v_pool) copies with the handoff buffer scattered in."""
+    buf = _c(buf)
+    kp, vp = k_pool.copy(), v_pool.copy()
+    pt = _c(page_table, np.int32)
+    req, lens = _c(req_ids, np.int32), _c(seq_lens, np.int32)
+    off = _c(in_offsets, np.int64)
+    d, hkv, num_pages = kp.shape[-1], kp.shape[-3], kp.shape[-4]
+    _lib().oracle_unpack(kp.itemsize, hkv, d, num_layers, _p(buf), _p(off), _p(req), _p(lens),
+                         len(req), _p(kp), _p(vp), num_pages, _p(pt), pt.shape[1])
+    return kp, vp

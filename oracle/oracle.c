@@ -241,3 +241,39 @@ int oracle_pack(int esize, int hkv, int d, int num_layers, const void *k_pool,
   }
   return 0;
 }
+
+/* Handoff unpack on the receiving instance: the inverse index map of
+ * oracle_pack.  Element (layer, c, h, t, e) of handoff n, read from
+ * in[off[n] + (((layer*2 + c)*Hkv + h)*len + t)*d + e], goes to page
+ * page_table[r*stride + t/16], slot t % 16 of request r = req_ids[n] in the
+ * destination pools.  Slots past len are left untouched.  Bit copy. */
+int oracle_unpack(int esize, int hkv, int d, int num_layers, const void *in,
+                  const int64_t *off, const int32_t *req_ids, const int32_t *seq_lens, int nh,
+                  void *k_pool, void *v_pool, int num_pages, const int32_t *page_table,
+                  int pt_stride) {
+  for (int n = 0; n < nh; ++n) {
+    const int r = req_ids[n], len = seq_lens[n];
+    for (int layer = 0; layer < num_layers; ++layer)
+      for (int c = 0; c < 2; ++c)
+        for (int h = 0; h < hkv; ++h)
+          for (int t = 0; t < len; ++t) {
+            const int64_t page = page_table[(int64_t)r * pt_stride + t / OR_PAGE];
+            const int slot = t % OR_PAGE;
+            const int64_t lp = (int64_t)layer * num_pages + page;
+            for (int e = 0; e < d; ++e) {
+              const int64_t src = off[n] + ((((int64_t)layer * 2 + c) * hkv + h) * len + t) * d + e;
+              int64_t dst;
+              void *pool;
+              if (c == 0) {
+                dst = ((lp * hkv + h) * OR_PAGE + slot) * d + e;
+                pool = k_pool;
+              } else {
+                dst = ((lp * hkv + h) * d + e) * OR_PAGE + slot;
+                pool = v_pool;
+              }
+              memcpy((char *)pool + dst * esize, (const char *)in + src * esize, esize);
+            }
+          }
+  }
+  return 0;
+}

@@ -37,6 +37,9 @@ MUTANTS = {
                              "const int64_t vd = ((page * hkv + h) * OR_PAGE + slot) * d + e;")],
     "write_wrong_source_row": [("const int64_t tok = cu_new[r] + i;", "const int64_t tok = cu_new[r] + (i ? i - 1 : 0);")],
     "pack_kv_swapped": [("if (c == 0) {\n                src", "if (c == 1) {\n                src")],
+    "unpack_kv_swapped": [("if (c == 0) {\n                dst", "if (c == 1) {\n                dst")],
+    "unpack_slot_off_by_one": [("const int slot = t % OR_PAGE;\n            const int64_t lp = (int64_t)layer * num_pages + page;\n            for (int e = 0; e < d; ++e) {\n              const int64_t src = off[n]",
+                                "const int slot = (t + 1) % OR_PAGE;\n            const int64_t lp = (int64_t)layer * num_pages + page;\n            for (int e = 0; e < d; ++e) {\n              const int64_t src = off[n]")],
     "pack_token_dim_transposed": [("const int64_t dst = off[n] + ((((int64_t)layer * 2 + c) * hkv + h) * len + t) * d + e;",
                                    "const int64_t dst = off[n] + ((((int64_t)layer * 2 + c) * hkv + h) * d + e) * len + t;")],
 }
@@ -59,7 +62,7 @@ def _load(path):
     lib = ctypes.CDLL(path)
     real = oracle._lib()
     for f in ("oracle_prefill", "oracle_prefill_rows", "oracle_decode", "oracle_kv_write",
-              "oracle_pack"):
+              "oracle_pack", "oracle_unpack"):
         getattr(lib, f).argtypes = getattr(real, f).argtypes
         getattr(lib, f).restype = getattr(real, f).restype
     return lib
@@ -154,8 +157,28 @@ def chk_closed_forms():
     return _close(out[:, 0], mean, 1e-13) and _close(lse[:, 0], np.log(np.arange(1, L + 1)), 1e-13)
 
 
+def chk_unpack_matches_write():
+    # unpack of a packed buffer into a fresh pool equals writing the same tokens
+    rng = np.random.default_rng(24)
+    lens = np.array([21, 3], np.int32)
+    hkv, d = 2, 8
+    pt, num_pages = I.allocate_pages(rng, lens, pool_pages=5)
+    kp, vp = I.empty_pools(num_pages, hkv, d, "bf16")
+    knew = I.normal(rng, (int(lens.sum()), hkv, d), "bf16")
+    vnew = I.normal(rng, (int(lens.sum()), hkv, d), "bf16")
+    cu = I.cu_from_lens(lens)
+    kw, vw = oracle.kv_write(knew, vnew, kp, vp, pt, cu, np.zeros(2, np.int32))
+    off = I.handoff_offsets(lens, 1, hkv, d)
+    buf = np.concatenate([np.stack([knew[cu[r]:cu[r + 1]].transpose(1, 0, 2),
+                                    vnew[cu[r]:cu[r + 1]].transpose(1, 0, 2)]).reshape(-1)
+                          for r in range(2)])
+    ku, vu = oracle.unpack(buf, off, np.arange(2), lens, kp, vp, 1, pt)
+    return bool(np.array_equal(ku, kw) and np.array_equal(vu, vw))
+
+
 CHECKS = [chk_prefill_brute, chk_prefill_sdpa, chk_lse, chk_decode_brute,
-          chk_last_row_equals_decode, chk_write_pack_transpose, chk_closed_forms]
+          chk_last_row_equals_decode, chk_write_pack_transpose, chk_closed_forms,
+          chk_unpack_matches_write]
 
 
 def _run_checks():

@@ -263,3 +263,30 @@ def test_pack_multi_layer_order():
     assert np.array_equal(blk[1, 1, 0, 3], vp[1, 2, 0, :, 3])
     blk2 = out[off[1]:off[2]].reshape(L, 2, hkv, 7, d)
     assert np.array_equal(blk2[0, 1, 1, 6], vp[0, 1, 1, :, 6])
+
+
+def test_unpack_inverts_pack_into_another_page_order():
+    # P -> D handoff: pack from one pool, unpack into a pool with another page
+    # permutation; every written slot matches, every other slot keeps its poison,
+    # and decode over both caches is bit-identical.
+    rng = np.random.default_rng(23)
+    lens = np.array([37, 16, 1], np.int32)
+    hkv, d, layers = 2, 8, 2
+    pt_a, n_a = I.allocate_pages(rng, lens, pool_pages=9)
+    pt_b, n_b = I.allocate_pages(rng, lens, pool_pages=11)
+    ka, va = I.empty_pools(n_a, hkv, d, "bf16", num_layers=layers)
+    for layer in range(layers):
+        I.fill_live_slots(rng, ka[layer], va[layer], pt_a, lens, "bf16")
+    off = I.handoff_offsets(lens, layers, hkv, d)
+    req = np.arange(3, dtype=np.int32)
+    buf = oracle.pack(ka, va, layers, pt_a, req, lens, off)
+    kb0, vb0 = I.empty_pools(n_b, hkv, d, "bf16", num_layers=layers)
+    kb, vb = oracle.unpack(buf, off, req, lens, kb0, vb0, layers, pt_b)
+    assert np.array_equal(oracle.pack(kb, vb, layers, pt_b, req, lens, off), buf)
+    live = (~np.isnan(I.bf16_bits_to_f32(kb))).sum()
+    assert live == layers * int(lens.sum()) * hkv * d
+    q = I.normal(rng, (3, 4, d), "bf16")
+    for layer in range(layers):
+        oa, la = oracle.decode(q, ka[layer], va[layer], pt_a, lens, 0.35)
+        ob, lb = oracle.decode(q, kb[layer], vb[layer], pt_b, lens, 0.35)
+        assert np.array_equal(oa, ob) and np.array_equal(la, lb)
