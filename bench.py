@@ -41,12 +41,13 @@ KERNEL_SOURCES = ("paper_2511_20982_amd/csrc/dopd_attn.hip",
                   "paper_2511_20982_amd/csrc/kernels/decode_bf16.hpp",
                   "paper_2511_20982_amd/csrc/kernels/prefill_bf16.hpp",
                   "paper_2511_20982_amd/csrc/kernels/kv_write.hpp",
-                  "paper_2511_20982_amd/csrc/kernels/kv_pack.hpp")
+                  "paper_2511_20982_amd/csrc/kernels/kv_pack.hpp",
+                  "paper_2511_20982_amd/csrc/kernels/kv_unpack.hpp")
 # Kernels behind each timed call (the decode call is a split kernel plus, when
 # some context exceeds one split, a merge kernel).
 CALL_KERNELS = {"decode": ("decode_split_kernel", "decode_merge_kernel"),
                 "prefill": ("prefill_bf16_kernel",), "kv_write": ("kv_write_kernel",),
-                "pack": ("kv_pack_kernel",)}
+                "pack": ("kv_pack_kernel",), "unpack": ("kv_unpack_kernel",)}
 
 WORKLOADS = {
     "mixed": ("mixed P/D step + handoff: prefill 8x512, decode 192 req ctx lognormal(2048,0.7) "
@@ -57,6 +58,9 @@ WORKLOADS = {
                 "32/32 heads, d128, bf16", 3),
     "decode_gqa": ("decode, GQA 70B-shaped: B256, 64/8 heads, d128, bf16, ctx 80% U[100,500] + "
                    "20% U[4096,16384]", 4),
+    "handoff": ("P->D handoff on one GPU: pack 8 prefilled requests x 512 tokens from the P pool, "
+                "unpack into a D pool with another page order; 28/4 heads, d128, bf16, "
+                "--pack-layers layers", 5),
 }
 
 
@@ -349,6 +353,46 @@ def main():
 
         work = {"decode": ("GB/s", decode_bytes(w.context_lens, w.hq, w.hkv, w.d))}
         dominant = "decode"
+    elif args.workload == "handoff":
+        L = args.pack_layers
+        n_dec, n_pre = len(w.context_lens), len(w.prefill_lens)
+        kp = torch.empty((L,) + w.k_pool.shape, dtype=torch.bfloat16, device=dev)
+        vp = torch.empty((L,) + w.v_pool.shape, dtype=torch.bfloat16, device=dev)
+        kp[0].copy_(A.to_device(w.k_pool))
+        vp[0].copy_(A.to_device(w.v_pool))
+        pt = A.to_device(w.page_table)
+        stride = w.page_table.shape[1]
+        # fill the prefilled requests' pages (untimed), then replicate the layer
+        A.dopd_kv_write(shape, A.to_device(w.k), A.to_device(w.v), kp[0], vp[0], w.num_pages,
+                        pt[n_dec:], stride, A.to_device(w.cu_seqlens),
+                        torch.zeros(n_pre, dtype=torch.int32, device=dev), n_pre,
+                        int(w.cu_seqlens[-1]))
+        for layer in range(1, L):
+            kp[layer].copy_(kp[0])
+            vp[layer].copy_(vp[0])
+        # receiving pool: same requests, another random page order
+        pt_d_np, pages_d = I.allocate_pages(np.random.default_rng(w.seed + 1000), w.handoff_lens)
+        kd = torch.zeros((L, pages_d, w.hkv, 16, w.d), dtype=torch.bfloat16, device=dev)
+        vd = torch.zeros((L, pages_d, w.hkv, w.d, 16), dtype=torch.bfloat16, device=dev)
+        pt_d = A.to_device(pt_d_np)
+        offs_np = I.handoff_offsets(w.handoff_lens, L, w.hkv, w.d)
+        offs = A.to_device(offs_np)
+        hreq, hlen = A.to_device(w.handoff_reqs), A.to_device(w.handoff_lens)
+        dreq = torch.arange(n_pre, dtype=torch.int32, device=dev)
+        buf = torch.empty(int(offs_np[-1]), dtype=torch.bfloat16, device=dev)
+        tm = {"pack": Timer(torch, sA), "unpack": Timer(torch, sA)}
+
+        def step():
+            with tm["pack"]:
+                A.dopd_kv_pack_for_handoff(shape, L, kp, vp, w.num_pages, pt, stride, hreq, hlen,
+                                           w.handoff_lens, offs, n_pre, buf, sA)
+            with tm["unpack"]:
+                A.dopd_kv_unpack_from_handoff(shape, L, buf, offs, dreq, hlen, w.handoff_lens,
+                                              n_pre, kd, vd, pages_d, pt_d, pt_d_np.shape[1], sA)
+
+        work = {"pack": ("GB/s", pack_bytes(w.handoff_lens, L, w.hkv, w.d)),
+                "unpack": ("GB/s", pack_bytes(w.handoff_lens, L, w.hkv, w.d))}
+        dominant = "unpack"
     else:  # prefill + write
         q, k, v = A.to_device(w.q), A.to_device(w.k), A.to_device(w.v)
         cu = A.to_device(w.cu_seqlens)
@@ -413,7 +457,7 @@ def main():
     # ---- CPU baseline: the fp64 oracle on host cores, plus a parity spot check
     cpu = None
     parity = None
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and args.workload != "handoff":
         import oracle
         threads = int(os.environ.get("OMP_NUM_THREADS", "0")) or len(os.sched_getaffinity(0))
         os.environ.setdefault("OMP_NUM_THREADS", str(threads))
@@ -475,7 +519,7 @@ def main():
         "data": "synthetic",
         "config": {"workload": desc, "seed": int(w.seed), "split_tokens": args.split,
                    "streams": args.streams if args.workload == "mixed" else 1,
-                   "pack_layers": args.pack_layers if args.workload == "mixed" else None},
+                   "pack_layers": args.pack_layers if args.workload in ("mixed", "handoff") else None},
         "roofline": roofline,
         "kernels": kern,
         "cpu_baseline": cpu,

@@ -152,6 +152,25 @@ dopd_status dopd_kv_pack_for_handoff(const dopd_attn_shape* shape, int32_t num_l
                                      int32_t num_handoff, void* out, void* stream);
 
 /*
+ * Handoff unpack on the receiving (D) instance, the inverse of
+ * dopd_kv_pack_for_handoff (the KV blocks the Connector delivers, Sec. V-C):
+ * element (layer, c, h, t, e) of handoff n, read from
+ *   in[in_offsets[n] + (((layer*2 + c)*Hkv + h)*len + t)*d + e],  len = seq_lens[n],
+ * is written to slot t % 16 of page page_table[req_ids[n]*stride + t/16] of
+ * the local pools (c = 0: k_pool, 1: v_pool; both with a leading layer
+ * dimension of num_pages pages).  Tail slots of the last page are not
+ * touched.  req_ids, seq_lens [num_handoff], in_offsets [num_handoff] (int64
+ * element offsets) are device arrays; seq_lens_host sizes the launch.  Bit copy.
+ */
+dopd_status dopd_kv_unpack_from_handoff(const dopd_attn_shape* shape, int32_t num_layers,
+                                        const void* in, const int64_t* in_offsets,
+                                        const int32_t* req_ids, const int32_t* seq_lens,
+                                        const int32_t* seq_lens_host, int32_t num_handoff,
+                                        void* k_pool, void* v_pool, int32_t num_pages,
+                                        const int32_t* page_table, int32_t page_table_stride,
+                                        void* stream);
+
+/*
  * Host check of a page table copy: for each request r, the entries
  * page_table_host[r*stride + i], i < ceil(lens_host[r]/16), must lie in
  * [0, num_pages).  Returns DOPD_OK or DOPD_ERR_INVALID_SHAPE.

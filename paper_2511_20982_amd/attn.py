@@ -25,7 +25,8 @@ PAGE_SIZE = 16
 
 EXPORTS = (
     "dopd_prefill_attn", "dopd_kv_write", "dopd_decode_attn", "dopd_decode_workspace_size",
-    "dopd_kv_pack_for_handoff", "dopd_validate_page_table_host", "dopd_status_string",
+    "dopd_kv_pack_for_handoff", "dopd_kv_unpack_from_handoff", "dopd_validate_page_table_host",
+    "dopd_status_string",
     "dopd_last_hip_error",
 )
 
@@ -70,12 +71,14 @@ def lib():
         L.dopd_decode_workspace_size.argtypes = [SP, P, i32, i32]
         L.dopd_decode_workspace_size.restype = sz
         L.dopd_kv_pack_for_handoff.argtypes = [SP, i32, P, P, i32, P, i32, P, P, P, P, i32, P, P]
+        L.dopd_kv_unpack_from_handoff.argtypes = [SP, i32, P, P, P, P, P, i32, P, P, i32, P, i32, P]
         L.dopd_validate_page_table_host.argtypes = [P, i32, i32, P, i32]
         L.dopd_status_string.argtypes = [i32]
         L.dopd_status_string.restype = C.c_char_p
         L.dopd_last_hip_error.restype = i32
         for f in ("dopd_prefill_attn", "dopd_kv_write", "dopd_decode_attn",
-                  "dopd_kv_pack_for_handoff", "dopd_validate_page_table_host"):
+                  "dopd_kv_pack_for_handoff", "dopd_kv_unpack_from_handoff",
+                  "dopd_validate_page_table_host"):
             getattr(L, f).restype = i32
         _LIB = L
     return _LIB
@@ -160,6 +163,18 @@ def dopd_kv_pack_for_handoff(shape, num_layers, k_pool, v_pool, num_pages, page_
                                           _dptr(seq_lens), _hptr(lens_h), _dptr(out_offsets),
                                           int(num_handoff), _dptr(out), _stream(stream)),
            "dopd_kv_pack_for_handoff")
+
+
+def dopd_kv_unpack_from_handoff(shape, num_layers, buf, in_offsets, req_ids, seq_lens,
+                                seq_lens_host, num_handoff, k_pool, v_pool, num_pages, page_table,
+                                page_table_stride, stream=None):
+    lens_h = _host_i32(seq_lens_host)
+    _check(lib().dopd_kv_unpack_from_handoff(C.byref(shape), int(num_layers), _dptr(buf),
+                                             _dptr(in_offsets), _dptr(req_ids), _dptr(seq_lens),
+                                             _hptr(lens_h), int(num_handoff), _dptr(k_pool),
+                                             _dptr(v_pool), int(num_pages), _dptr(page_table),
+                                             int(page_table_stride), _stream(stream)),
+           "dopd_kv_unpack_from_handoff")
 
 
 def dopd_validate_page_table_host(page_table_host, page_table_stride, num_reqs, lens_host,

@@ -13,6 +13,7 @@
 #include "kernels/common.hpp"
 #include "kernels/decode_bf16.hpp"
 #include "kernels/kv_pack.hpp"
+#include "kernels/kv_unpack.hpp"
 #include "kernels/kv_write.hpp"
 #include "kernels/prefill_bf16.hpp"
 
@@ -354,6 +355,56 @@ dopd_status dopd_kv_pack_for_handoff(const dopd_attn_shape* s, int32_t num_layer
     hipLaunchKernelGGL(dopd::kv_pack_kernel<uint32_t>, grid, dim3(256), 0, strm,
                        (const uint32_t*)k_pool, (const uint32_t*)v_pool, num_pages, pt, pt_stride,
                        req_ids, seq_lens, out_offsets, s->num_kv_heads, s->head_dim, (uint32_t*)out);
+  return launch_status();
+}
+
+// ---------------------------------------------------------------- handoff unpack
+dopd_status dopd_kv_unpack_from_handoff(const dopd_attn_shape* s, int32_t num_layers,
+                                        const void* in, const int64_t* in_offsets,
+                                        const int32_t* req_ids, const int32_t* seq_lens,
+                                        const int32_t* seq_lens_host, int32_t num_handoff,
+                                        void* k_pool, void* v_pool, int32_t num_pages,
+                                        const int32_t* pt, int32_t pt_stride, void* stream) {
+  dopd_status st = check_shape(s);
+  if (st != DOPD_OK) return st;
+  if (num_layers < 1 || num_pages < 0 || pt_stride < 0 || num_handoff < 0)
+    return DOPD_ERR_INVALID_SHAPE;
+  if (num_handoff == 0) return DOPD_OK;
+  if (!in || !in_offsets || !req_ids || !seq_lens || !seq_lens_host || !k_pool || !v_pool || !pt)
+    return DOPD_ERR_NULL_POINTER;
+  int max_len = 0;
+  for (int32_t n = 0; n < num_handoff; ++n) {
+    if (seq_lens_host[n] < 0) return DOPD_ERR_INVALID_SHAPE;
+    if ((int64_t)(seq_lens_host[n] + dopd::kPage - 1) / dopd::kPage > pt_stride)
+      return DOPD_ERR_INVALID_SHAPE;
+    max_len = std::max(max_len, seq_lens_host[n]);
+  }
+  if (max_len == 0) return DOPD_OK;
+  const int64_t zdim = (int64_t)num_layers * 2 * s->num_kv_heads;
+  if (zdim > 65535 || num_handoff > 65535) return DOPD_ERR_INVALID_SHAPE;
+  dim3 grid((unsigned)((max_len + dopd::kPage - 1) / dopd::kPage), (unsigned)num_handoff,
+            (unsigned)zdim);
+  hipStream_t strm = as_stream(stream);
+  const int hkv = s->num_kv_heads;
+  if (s->dtype == DOPD_BF16) {
+    auto* src = (const uint16_t*)in;
+    auto* kp = (uint16_t*)k_pool; auto* vp = (uint16_t*)v_pool;
+    if (s->head_dim == 64)
+      hipLaunchKernelGGL((dopd::kv_unpack_kernel<uint16_t, 64>), grid, dim3(256), 0, strm, src,
+                         in_offsets, req_ids, seq_lens, kp, vp, num_pages, pt, pt_stride, hkv);
+    else
+      hipLaunchKernelGGL((dopd::kv_unpack_kernel<uint16_t, 128>), grid, dim3(256), 0, strm, src,
+                         in_offsets, req_ids, seq_lens, kp, vp, num_pages, pt, pt_stride, hkv);
+  } else {
+    auto* src = (const uint32_t*)in;
+    auto* kp = (uint32_t*)k_pool; auto* vp = (uint32_t*)v_pool;
+    if (s->head_dim == 64)
+      hipLaunchKernelGGL((dopd::kv_unpack_kernel<uint32_t, 64>), grid, dim3(256), 0, strm, src,
+                         in_offsets, req_ids, seq_lens, kp, vp, num_pages, pt, pt_stride, hkv);
+    else
+      hipLaunchKernelGGL((dopd::kv_unpack_kernel<uint32_t, 128>), grid, dim3(256), 0, strm, src,
+                         in_offsets, req_ids, seq_lens, kp, vp, num_pages, pt, pt_stride, hkv);
+  }
   return launch_status();
 }
 

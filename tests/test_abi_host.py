@@ -127,3 +127,16 @@ def test_validate_page_table_host(lib):
     assert A.dopd_validate_page_table_host(pt, 3, 2, [20, 17], 4) == A.DOPD_ERR_INVALID_SHAPE
     assert A.dopd_validate_page_table_host(pt, 3, 2, [20, 16], 3) == A.DOPD_ERR_INVALID_SHAPE
     assert A.dopd_validate_page_table_host(pt, 3, 0, [], 4) == A.DOPD_OK
+
+
+def test_unpack_host_validation(lib):
+    s = _shape()
+    p = C.c_void_p(FAKE)
+    lens = np.array([40, 600], np.int32)
+    up = lib.dopd_kv_unpack_from_handoff
+    assert up(C.byref(s), 0, p, p, p, p, A._hptr(lens), 2, p, p, 10, p, 64, None) == \
+        A.DOPD_ERR_INVALID_SHAPE                                               # no layers
+    assert up(C.byref(s), 1, p, p, p, p, A._hptr(lens), 2, p, p, 10, p, 8, None) == \
+        A.DOPD_ERR_INVALID_SHAPE                                               # table too narrow
+    assert up(C.byref(s), 1, p, p, p, p, None, 2, p, p, 10, p, 64, None) == A.DOPD_ERR_NULL_POINTER
+    assert up(C.byref(s), 1, p, p, p, p, A._hptr(lens), 0, p, p, 10, p, 64, None) == A.DOPD_OK

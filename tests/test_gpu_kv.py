@@ -105,3 +105,71 @@ def test_write_then_pack_round_trip_is_a_transpose():
         a, b = cu[r], cu[r + 1]
         expect = np.stack([knew[a:b].transpose(1, 0, 2), vnew[a:b].transpose(1, 0, 2)])
         assert np.array_equal(out[off[r]:off[r + 1]], expect.reshape(-1))
+
+
+def gpu_unpack(shape, buf, offs, req, lens, k_pool, v_pool, layers, pt):
+    import torch
+    kp, vp = G.A.to_device(k_pool), G.A.to_device(v_pool)
+    num_pages = k_pool.shape[-4]
+    G.A.dopd_kv_unpack_from_handoff(shape, layers, G.A.to_device(buf), G.A.to_device(offs),
+                                    G.A.to_device(req), G.A.to_device(lens), lens, len(req), kp, vp,
+                                    num_pages, G.A.to_device(pt), pt.shape[1])
+    torch.cuda.synchronize()
+    return G.A.to_host(kp), G.A.to_host(vp)
+
+
+@pytest.mark.parametrize("dtype,d,layers", [("bf16", 128, 2), ("bf16", 64, 1), ("fp32", 64, 3),
+                                            ("fp32", 128, 1)])
+def test_unpack_bit_exact(dtype, d, layers):
+    rng = np.random.default_rng(36)
+    hkv = 4
+    lens = np.array([512, 1, 17, 31, 0, 48], np.int32)
+    pt, num_pages = I.allocate_pages(rng, lens, pool_pages=60)
+    kp, vp = I.empty_pools(num_pages, hkv, d, dtype, num_layers=layers)
+    kp[:], vp[:] = I.normal(rng, kp.shape, dtype), I.normal(rng, vp.shape, dtype)  # old contents
+    req = np.array([0, 2, 1, 5, 3, 4], np.int32)
+    seq = lens[req]
+    offs = I.handoff_offsets(seq, layers, hkv, d)
+    buf = I.normal(rng, (int(offs[-1]),), dtype)
+    ref_k, ref_v = oracle.unpack(buf, offs, req, seq, kp, vp, layers, pt)
+    gk, gv = gpu_unpack(G.A.make_shape(8, hkv, d, dtype), buf, offs, req, seq, kp, vp, layers, pt)
+    assert np.array_equal(gk.view(np.uint8), ref_k.view(np.uint8))
+    assert np.array_equal(gv.view(np.uint8), ref_v.view(np.uint8))
+
+
+def test_unpack_unaligned_offsets():
+    rng = np.random.default_rng(37)
+    hkv, d = 2, 64
+    lens = np.array([20, 9], np.int32)
+    pt, num_pages = I.allocate_pages(rng, lens, pool_pages=4)
+    kp, vp = I.empty_pools(num_pages, hkv, d, "bf16")
+    offs = I.handoff_offsets(lens, 1, hkv, d) + 3
+    buf = I.normal(rng, (int(offs[-1]),), "bf16")
+    req = np.arange(2, dtype=np.int32)
+    ref_k, ref_v = oracle.unpack(buf, offs, req, lens, kp, vp, 1, pt)
+    gk, gv = gpu_unpack(G.A.make_shape(2, hkv, d), buf, offs, req, lens, kp, vp, 1, pt)
+    assert np.array_equal(gk, ref_k) and np.array_equal(gv, ref_v)
+
+
+def test_handoff_round_trip_decode_bit_identical():
+    """P -> D on one GPU: pack from pool A, unpack into a pool B with another page
+    order; decode on both caches gives bit-identical outputs."""
+    rng = np.random.default_rng(38)
+    hq, hkv, d = 28, 4, 128
+    lens = np.array([512, 700, 33, 1], np.int32)
+    pt_a, n_a = I.allocate_pages(rng, lens)
+    pt_b, n_b = I.allocate_pages(rng, lens, pool_pages=n_a + 7)
+    ka, va = I.empty_pools(n_a, hkv, d, "bf16")
+    I.fill_live_slots(rng, ka, va, pt_a, lens, "bf16")
+    kb, vb = I.empty_pools(n_b, hkv, d, "bf16")
+    req = np.arange(4, dtype=np.int32)
+    offs = I.handoff_offsets(lens, 1, hkv, d)
+    sh = G.A.make_shape(hq, hkv, d)
+    buf = G.gpu_pack(sh, ka, va, 1, pt_a, req, lens, offs)
+    gk, gv = gpu_unpack(sh, buf, offs, req, lens, kb, vb, 1, pt_b)
+    ref_k, ref_v = oracle.unpack(buf, offs, req, lens, kb, vb, 1, pt_b)
+    assert np.array_equal(gk, ref_k) and np.array_equal(gv, ref_v)
+    q = I.normal(rng, (4, hq, d), "bf16")
+    out_a, lse_a = G.gpu_decode(sh, q, ka, va, pt_a, lens, split=256)
+    out_b, lse_b = G.gpu_decode(sh, q, gk, gv, pt_b, lens, split=256)
+    assert np.array_equal(out_a, out_b) and np.array_equal(lse_a, lse_b)
