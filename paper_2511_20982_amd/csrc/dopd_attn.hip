@@ -175,8 +175,9 @@ dopd_status dopd_prefill_attn(const dopd_attn_shape* s, const void* q, const voi
   a.hq = hq;
   a.hkv = hkv;
   a.max_tiles = (max_len + dopd::kPfBM - 1) / dopd::kPfBM;
+  a.hslots = (hq + dopd::kPfHeadsPerWG - 1) / dopd::kPfHeadsPerWG;
   a.scale_log2 = s->softmax_scale * dopd::kLog2e;
-  const int64_t items = bf16_items * hq;
+  const int64_t items = bf16_items * a.hslots;
   if (items > INT32_MAX / 2) return DOPD_ERR_INVALID_SHAPE;
   int64_t blocks = items;
   a.xcd_order = 0;

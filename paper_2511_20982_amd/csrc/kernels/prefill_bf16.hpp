@@ -1,25 +1,32 @@
 // Variable-length causal prefill attention, bf16 in / fp32 accumulate, gfx950.
 //
-// Workgroup = 4 waves = one (q tile of 128 rows, request, query head); each
-// wave owns 32 query rows; two workgroups share a CU, so the two waves on a
-// SIMD run out of phase.  K/V stages of 64 keys are staged in LDS (K
-// token-major, V transposed to dim-major on the way in), double-buffered, and
-// shared by the four waves.  Per stage and wave:
+// Workgroup = 4 waves = one (q tile of 128 rows, request, query head) item;
+// each wave owns 32 query rows.  Two workgroups share a CU, so each SIMD runs
+// two waves whose MFMA and VALU phases overlap.
 //
+// Per 64-key tile and wave:
 //   S^T[64 tok][32 q] = K[64][d] . Q^T[d][32]       2 x (d/16) v_mfma_f32_32x32x16_bf16
 //   O^T[d][32 q]     += V^T[d][64] . P^T[64][32]    (d/32) x 4  v_mfma_f32_32x32x16_bf16
+// Computing the transposed products keeps a query row inside one lane pair,
+// and the S^T accumulator is directly the P^T B operand of the P.V MFMA (the
+// key order of the contraction is matched by the V^T reads).
 //
-// Computing the transposed products keeps a whole query row inside one lane
-// pair, so the online-softmax row max needs one lane swap, and the MFMA output
-// of S^T is already the B operand of the P.V MFMA (the token order of the
-// contraction is matched on the V^T LDS reads).  LDS operands are read ahead
-// of their MFMAs (pinned scheduling groups); rows are padded so that reads and
-// writes are free of bank conflicts.  Scores are scaled into the exp2 domain
-// inside one fma; only stages on the diagonal or past the end of the request
-// are masked, with a select (never a multiply).
+// K and V tiles move from global memory straight into LDS (buffer loads with
+// the LDS destination, no registers), double-buffered; K is one tile ahead of
+// V so that a step computes S^T of tile j + 1 on the MFMAs while the VALU
+// forms P of tile j.  V stays token-major in LDS and the V^T operand is
+// gathered with the transposing LDS read.
+//
+// Softmax: exp2 with the scale folded into one fma; P is rounded to bf16 for
+// the P.V product and the row sum l adds the rounded values.  In the steady
+// state no row max is taken: p is formed against the running max and only a
+// row sum beyond 2^20 (a tile far above it) takes the tile max, rescales O
+// and l and forms p again.  Diagonal and ragged tiles take the max and mask
+// with a select.
 // Work order: with at most 64 requests, each XCD takes a contiguous slice of
-// (KV head, request longest first, q tile descending) so the q tiles that read
-// the same K/V run together under one L2; otherwise heaviest q tiles first.
+// (KV head, request longest first, q tile descending, query head) so the q tiles
+// that read the same K/V run together under one L2; otherwise heaviest q
+// tiles first.
 #pragma once
 #include "common.hpp"
 
@@ -33,10 +40,11 @@ struct PrefillArgs {
   float* lse;          // [T][Hq] or null
   const int32_t* cu;   // [nreq + 1]
   int nreq, hq, hkv, max_tiles;
+  int hslots;          // head slots = ceil(hq / kPfHeadsPerWG)
   float scale_log2;
   // XCD-aware order (used when nreq <= kPfMaxOrdered): the work list is
-  // (KV head, request by decreasing length, q tile descending, query head of
-  // the group); XCD x = workgroup % 8 takes the contiguous slice
+  // (slot block, request by decreasing length, q tile descending, slot of the
+  // block); XCD x = workgroup % 8 takes the contiguous slice
   // [x * per_xcd, (x+1) * per_xcd), so the q tiles that share a request's K/V
   // run together on one XCD and share its L2.
   int xcd_order, n_items, per_xcd, tiles_total;
@@ -46,19 +54,20 @@ struct PrefillArgs {
 constexpr int kPfMaxOrdered = 64;
 constexpr int kNumXcd = 8;
 
-constexpr int kPfBM = 128;  // query rows per workgroup (32 per wave)
-constexpr int kPfThreads = kPfBM / 32 * 64;
-constexpr int kPfBN = 64;   // keys per LDS stage (computed as 64-key sub-tiles)
+constexpr int kPfBM = 128;          // query rows per workgroup (32 per wave)
+constexpr int kPfHeadsPerWG = 1;    // heads per workgroup
+constexpr int kPfThreads = kPfHeadsPerWG * (kPfBM / 32) * 64;
+constexpr int kPfBN = 64;           // keys per tile
 
 // Number of BM-row q tiles of request rr.
 __device__ __forceinline__ int pf_tiles(const int32_t* cu, int rr) {
   return (cu[rr + 1] - cu[rr] + kPfBM - 1) / kPfBM;
 }
 
-// Maps a workgroup index to (q tile, request, head), q tiles in decreasing
-// index order (tile i of a request attends to ~ (i+1) key tiles).
+// Maps a workgroup index to (q tile, request, head slot), q tiles in
+// decreasing index order (tile i of a request attends to ~ (i+1) key tiles).
 __device__ __forceinline__ bool pf_find_item_lpt(const PrefillArgs& a, int b, int& tile,
-                                                 int& req, int& head) {
+                                                 int& req, int& slot) {
   const int l = lane_id();
   const bool small = a.nreq <= 64;
   const int nt_l = (small && l < a.nreq) ? pf_tiles(a.cu, l) : 0;
@@ -67,308 +76,395 @@ __device__ __forceinline__ bool pf_find_item_lpt(const PrefillArgs& a, int b, in
       const int nt = small ? nt_l : ((r0 + l < a.nreq) ? pf_tiles(a.cu, r0 + l) : 0);
       const unsigned long long hit = __ballot(nt > i);
       const int cnt = __popcll(hit);
-      if (b < cnt * a.hq) {
-        const int kth = b / a.hq;
+      if (b < cnt * a.hslots) {
+        const int kth = b / a.hslots;
         // position of the kth set bit
         const int before = __builtin_amdgcn_mbcnt_hi((uint32_t)(hit >> 32),
                                                      __builtin_amdgcn_mbcnt_lo((uint32_t)hit, 0u));
         const unsigned long long sel = __ballot(nt > i && before == kth);
         req = r0 + __ffsll((long long)sel) - 1;
-        head = b % a.hq;
+        slot = b % a.hslots;
         tile = i;
         return true;
       }
-      b -= cnt * a.hq;
+      b -= cnt * a.hslots;
     }
   }
   return false;
 }
 
-// XCD-aware mapping (see PrefillArgs).
+// XCD-aware mapping (see PrefillArgs).  Slots are grouped in blocks of the
+// slots that read one KV head (GQA) when the group size allows it.
 __device__ __forceinline__ bool pf_find_item_xcd(const PrefillArgs& a, int b, int& tile,
-                                                 int& req, int& head) {
+                                                 int& req, int& slot) {
   const int x = b % kNumXcd, j = b / kNumXcd;
   const int n = x * a.per_xcd + j;
   if (j >= a.per_xcd || n >= a.n_items) return false;
   const int g = a.hq / a.hkv;
-  const int per_kvh = g * a.tiles_total;
-  const int kvh = n / per_kvh;
-  const int rem = n - kvh * per_kvh;
+  const int gs = (g % kPfHeadsPerWG == 0) ? g / kPfHeadsPerWG : 1;  // slots per block
+  const int per_blk = gs * a.tiles_total;
+  const int blk = n / per_blk;
+  const int rem = n - blk * per_blk;
   const int l = lane_id();
   const int rr = l < a.nreq ? a.ord[l] : 0;
   const int nt = l < a.nreq ? pf_tiles(a.cu, rr) : 0;
-  const int cnt = g * nt;
+  const int cnt = gs * nt;
   const int incl = wave_inclusive_scan(cnt);
   const unsigned long long hit = __ballot(rem < incl);
   const int k = __ffsll((long long)hit) - 1;
   const int local = rem - __shfl(incl - cnt, k, 64);
   req = __shfl(rr, k, 64);
-  tile = __shfl(nt, k, 64) - 1 - local / g;
-  head = kvh * g + local % g;
+  tile = __shfl(nt, k, 64) - 1 - local / gs;
+  slot = blk * gs + local % gs;
   return true;
 }
 
 __device__ __forceinline__ bool pf_find_item(const PrefillArgs& a, int b, int& tile, int& req,
-                                             int& head) {
-  return a.xcd_order ? pf_find_item_xcd(a, b, tile, req, head)
-                     : pf_find_item_lpt(a, b, tile, req, head);
+                                             int& slot) {
+  return a.xcd_order ? pf_find_item_xcd(a, b, tile, req, slot)
+                     : pf_find_item_lpt(a, b, tile, req, slot);
 }
 
 template <int D>
 __global__ __launch_bounds__(kPfThreads, 2) void prefill_bf16_kernel(PrefillArgs a) {
-  constexpr int BM = kPfBM, BN = kPfBN, SUB = 64;
-  constexpr int KP = D + 8;      // padded K row (elements)
-  constexpr int VP = BN + 4;     // padded V^T row (elements): 2 dwords of skew per row
+  constexpr int BM = kPfBM, BN = kPfBN;
   constexpr int KS = D / 16;     // k-steps of the QK MFMA
   constexpr int ET = D / 32;     // O^T tiles of 32 dims
   constexpr int CPR = D / 8;     // 16-byte chunks per K/V row
-  constexpr int NTH = kPfThreads;
-  constexpr int KCH = BN * CPR / NTH;   // K chunks staged per thread
-  constexpr int VTH = (BN / 4) * CPR;   // threads staging V (4 tokens x 8 dims each)
-  __shared__ __attribute__((aligned(16))) uint16_t sK[2][BN * KP];
-  __shared__ __attribute__((aligned(16))) uint16_t sV[2][D * VP];
+  constexpr int KQW = BN * CPR / kPfThreads;   // 16-byte chunks of a K (or V) tile per thread
+  // One array per (K/V, buffer): with compile-time buffer choices the
+  // compiler can tell that LDS reads of one buffer never alias the in-flight
+  // global->LDS loads into another, and does not wait for them.
+  __shared__ __attribute__((aligned(16))) uint16_t sK0[BN * D], sK1[BN * D];
+  __shared__ __attribute__((aligned(16))) uint16_t sV0[BN * D], sV1[BN * D];
+  auto kbuf = [&](int b) { return b ? sK1 : sK0; };
+  auto vbuf = [&](int b) { return b ? sV1 : sV0; };
 
-  const int tid = threadIdx.x, l = lane_id(), w = tid >> 6;
   int tile, r, h;
   if (!pf_find_item(a, blockIdx.x, tile, r, h)) return;  // uniform across the workgroup
-  const int g = a.hq / a.hkv, kvh = h / g;
-  const int seq0 = a.cu[r], L = a.cu[r + 1] - seq0;
-  const int q0 = tile * BM;
-  const int kv_end = min(L, q0 + BM);
-  const int ntiles = (kv_end + BN - 1) / BN;
-  const int row_w = q0 + 32 * w;            // first query row of this wave
-  const int myq = row_w + (l & 31);         // this lane's query row
-  const bool wave_active = row_w < L;
-  const int hi = l >> 5;                    // lane half
-
-  // Q^T operand, B of the QK MFMA: lane holds Q[myq][16ks + 8hi + 0..7].
-  bf16x8 qop[KS];
+  // The item is wave-uniform; say so, so that what derives from it stays scalar.
+  tile = __builtin_amdgcn_readfirstlane(tile);
+  r = __builtin_amdgcn_readfirstlane(r);
+  h = __builtin_amdgcn_readfirstlane(h);
   {
-    const bool ok = myq < L;
-    const uint16_t* qp = a.q + ((int64_t)(seq0 + (ok ? myq : 0)) * a.hq + h) * D + 8 * hi;
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-      u32x4 x = ok ? *reinterpret_cast<const u32x4*>(qp + 16 * ks) : u32x4{0, 0, 0, 0};
-      qop[ks] = __builtin_bit_cast(bf16x8, x);
-    }
-  }
+    const int tid = threadIdx.x, l = lane_id();
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int g = a.hq / a.hkv, kvh = h / g;
+    const int seq0 = a.cu[r], L = a.cu[r + 1] - seq0;
+    const int q0 = tile * BM;
+    const int kv_end = min(L, q0 + BM);
+    const int ntiles = (kv_end + BN - 1) / BN;
+    const int row_w = q0 + 32 * w;            // first query row of this wave
+    const int myq = row_w + (l & 31);         // this lane's query row
+    const bool wave_active = row_w < L;
+    const int hi = l >> 5;                    // lane half
 
-  f32x16 oacc[ET];
-#pragma unroll
-  for (int et = 0; et < ET; ++et)
-#pragma unroll
-    for (int x = 0; x < 16; ++x) oacc[et][x] = 0.f;
-  float m_run = -INFINITY, l_run = 0.f;
-
-  const int64_t kv_row = (int64_t)a.hkv * D;  // elements between consecutive tokens
-  const uint16_t* kg = a.k + (int64_t)seq0 * kv_row + (int64_t)kvh * D;
-  const uint16_t* vg = a.v + (int64_t)seq0 * kv_row + (int64_t)kvh * D;
-
-  const int v_tg = tid % (BN / 4), v_col = tid / (BN / 4);  // V staging: tokens 4*v_tg.., dims 8*v_col..
-  u32x4 rk[KCH], rv[4];                          // global -> LDS staging registers
-  // Rows past the end of the request are read from its last token instead
-  // (always in bounds and finite); their scores are masked and their P is 0.
-  auto gload_k = [&](int kv0) {
-#pragma unroll
-    for (int u = 0; u < KCH; ++u) {
-      const int ch = tid + NTH * u, t = ch / CPR, col = ch % CPR;
-      const int tok = min(kv0 + t, kv_end - 1);
-      rk[u] = *reinterpret_cast<const u32x4*>(kg + (int64_t)tok * kv_row + 8 * col);
-    }
-  };
-  auto gload_v = [&](int kv0) {
-    if (tid < VTH) {
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const int tok = min(kv0 + 4 * v_tg + u, kv_end - 1);
-        rv[u] = *reinterpret_cast<const u32x4*>(vg + (int64_t)tok * kv_row + 8 * v_col);
-      }
-    }
-  };
-  auto lstore_k = [&](int buf) {
-#pragma unroll
-    for (int u = 0; u < KCH; ++u) {
-      const int ch = tid + NTH * u, t = ch / CPR, col = ch % CPR;
-      *reinterpret_cast<u32x4*>(&sK[buf][t * KP + 8 * col]) = rk[u];
-    }
-  };
-  auto lstore_v = [&](int buf) {
-    if (tid < VTH) {
-      // 4 tokens x 8 dims -> 8 dim rows of 4 tokens: byte permutes pick the
-      // low (even dim) or high (odd dim) bf16 of two token words.
-#pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        const int wd = i >> 1;
-        const uint32_t sel = (i & 1) ? 0x07060302u : 0x05040100u;
-        u32x2 x;
-        x[0] = __builtin_amdgcn_perm(rv[1][wd], rv[0][wd], sel);
-        x[1] = __builtin_amdgcn_perm(rv[3][wd], rv[2][wd], sel);
-        *reinterpret_cast<u32x2*>(&sV[buf][(8 * v_col + i) * VP + 4 * v_tg]) = x;
-      }
-    }
-  };
-
-  // Scores stay raw until the exponent: p = 2^(s*c - m) as one fma, with the
-  // running max m kept in the scaled domain.  For c <= 0 the scores are scaled
-  // first and c is taken as 1, so the max is always taken on the exponent.
-  const float c_in = a.scale_log2;
-  const bool pos_scale = c_in > 0.f;
-  const float c_eff = pos_scale ? c_in : 1.f;
-  // Lazy rescaling: the running max only moves when a new tile raises it by
-  // more than kLazy (log2 units), so P <= 2^kLazy and the O/l rescale is
-  // skipped for most tiles.  The result is the same softmax (the final O/l
-  // uses the same m throughout).
-  constexpr float kLazy = 8.f;
-  // Last key this lane's row may see (causal and end of request).
-  const int last_key = min(myq, kv_end - 1);
-
-  f32x16 st[2];   // S^T of the 64-key sub-tile being scored
-  bf16x8 pb[4];   // its P^T, the B operands of the four P.V k-steps
-  constexpr int kDsRead = 0x100, kMfma = 0x008;
-
-  // Operands are read from LDS ahead of the MFMAs that use them (scheduling
-  // groups pin the order), so LDS latency overlaps the matrix work.
-  auto qk = [&](int buf, int sub) {  // st = S^T of keys [64 sub, 64 sub + 64) of the stage
-    bf16x8 ka[2][KS];
-#pragma unroll
-    for (int tt = 0; tt < 2; ++tt) {
-      const uint16_t* kr = &sK[buf][(SUB * sub + 32 * tt + (l & 31)) * KP + 8 * hi];
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks) ka[tt][ks] = *reinterpret_cast<const bf16x8*>(kr + 16 * ks);
-    }
-#pragma unroll
-    for (int tt = 0; tt < 2; ++tt)
-#pragma unroll
-      for (int x = 0; x < 16; ++x) st[tt][x] = 0.f;
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks)
-#pragma unroll
-      for (int tt = 0; tt < 2; ++tt)
-        st[tt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[tt][ks], qop[ks], st[tt], 0, 0, 0);
-    __builtin_amdgcn_sched_group_barrier(kDsRead, 4, 0);
-#pragma unroll
-    for (int ks = 0; ks < KS - 2; ++ks) {
-      __builtin_amdgcn_sched_group_barrier(kMfma, 2, 0);
-      __builtin_amdgcn_sched_group_barrier(kDsRead, 2, 0);
-    }
-    __builtin_amdgcn_sched_group_barrier(kMfma, 4, 0);
-  };
-  auto pv = [&](int buf, int sub) {  // O^T += V^T P^T of the sub-tile
-    // k-step (tt, hh): k-slot 8hi + jj <-> key 32tt + 16hh + 8(jj/4) + 4hi + jj%4
-    u32x4 va[4][ET];
-#pragma unroll
-    for (int kk = 0; kk < 4; ++kk) {
-      const int tcol = SUB * sub + 32 * (kk >> 1) + 16 * (kk & 1) + 4 * hi;
-#pragma unroll
-      for (int et = 0; et < ET; ++et) {
-        const uint16_t* vr = &sV[buf][(32 * et + (l & 31)) * VP + tcol];
-        const u32x2 lo = *reinterpret_cast<const u32x2*>(vr);
-        const u32x2 hi2 = *reinterpret_cast<const u32x2*>(vr + 8);
-        va[kk][et] = u32x4{lo[0], lo[1], hi2[0], hi2[1]};
-      }
-    }
-#pragma unroll
-    for (int kk = 0; kk < 4; ++kk)
-#pragma unroll
-      for (int et = 0; et < ET; ++et)
-        oacc[et] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, va[kk][et]),
-                                                           pb[kk], oacc[et], 0, 0, 0);
-    __builtin_amdgcn_sched_group_barrier(kDsRead, ET, 0);
-#pragma unroll
-    for (int kk = 0; kk < 3; ++kk)
-#pragma unroll
-      for (int et = 0; et < ET; ++et) {
-        __builtin_amdgcn_sched_group_barrier(kMfma, 1, 0);
-        __builtin_amdgcn_sched_group_barrier(kDsRead, 1, 0);
-      }
-    __builtin_amdgcn_sched_group_barrier(kMfma, ET, 0);
-  };
-  auto softmax = [&](int kv0) {  // st (keys kv0 ..) -> pb, updating m_run, l_run (and O lazily)
-    // lane holds S^T[t = kv0 + 32tt + 8(x/4) + 4hi + x%4][q = myq]
-    if (!pos_scale) {
-#pragma unroll
-      for (int tt = 0; tt < 2; ++tt) st[tt] *= c_in;
-    }
-    if (kv0 + SUB - 1 > row_w || kv0 + SUB > kv_end) {  // diagonal or ragged sub-tile
-      const int lim = last_key - kv0 - 4 * hi;  // mask offsets beyond it
-#pragma unroll
-      for (int tt = 0; tt < 2; ++tt)
-#pragma unroll
-        for (int x = 0; x < 16; ++x)
-          if (32 * tt + 8 * (x >> 2) + (x & 3) > lim) st[tt][x] = -INFINITY;
-    }
-    float mx = fmaxf(st[0][0], st[1][0]);
-#pragma unroll
-    for (int x = 1; x < 16; ++x) mx = fmaxf(mx, fmaxf(st[0][x], st[1][x]));
+    // Q^T operand, B of the QK MFMA: lane holds Q[myq][16ks + 8hi + 0..7].
+    bf16x8 qop[KS];
     {
+      const bool ok = myq < L;
+      const uint16_t* qp = a.q + ((int64_t)(seq0 + (ok ? myq : 0)) * a.hq + h) * D + 8 * hi;
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        u32x4 x = ok ? *reinterpret_cast<const u32x4*>(qp + 16 * ks) : u32x4{0, 0, 0, 0};
+        qop[ks] = __builtin_bit_cast(bf16x8, x);
+      }
+    }
+
+    f32x16 oacc[ET];
+#pragma unroll
+    for (int et = 0; et < ET; ++et)
+#pragma unroll
+      for (int x = 0; x < 16; ++x) oacc[et][x] = 0.f;
+    float m_run = -INFINITY, l_run = 0.f;
+
+    const int64_t kv_row = (int64_t)a.hkv * D;  // elements between consecutive tokens
+    const uint16_t* kg = a.k + (int64_t)seq0 * kv_row + (int64_t)kvh * D;
+    const uint16_t* vg = a.v + (int64_t)seq0 * kv_row + (int64_t)kvh * D;
+
+    // LDS tiles, 16-byte chunks.  K: [D/32 chunk groups][BN rows][4 slots],
+    // chunk c of row t in group c/4, slot (c%4) ^ ((t/4)%4), so that the 16
+    // rows read by 16 lanes at one chunk hit 16 distinct bank groups.  V:
+    // [D/32 dim groups][BN tokens][32 dims], token-major.  Wave instruction
+    // u of wave w fills LDS chunks [64(4u + w), +64): row 16w + l/4, chunk
+    // group u, slot l%4.
+    const int k_t = 16 * w + (l >> 2);                            // this lane's row of a tile
+    const int k_c = (l & 3) ^ ((k_t >> 2) & 3);                   // K: swizzled slot
+    const int v_c = l & 3;                                        // V: plain chunk
+    const int row_b = (int)(kv_row * 2);                          // bytes between tokens
+    const int lane_k = k_t * row_b + 16 * k_c;
+    const int lane_v = k_t * row_b + 16 * v_c;
+    // A tile load goes through a buffer descriptor whose base is the tile's
+    // first token and whose size covers its valid rows; full tiles use loop
+    // invariant lane offsets, ragged tiles clamp to the last valid row.
+    auto stage = [&](const uint16_t* g0, uint16_t* lds, int kv0, int lane_full, int chunk) {
+      const int rows = min(BN, kv_end - kv0);                   // uniform, >= 1
+      const int voff = rows == BN ? lane_full : min(k_t, rows - 1) * row_b + 16 * chunk;
+      const __amdgpu_buffer_rsrc_t rsrc = __builtin_amdgcn_make_buffer_rsrc(
+          (void*)(g0 + (int64_t)kv0 * kv_row), (short)0, (rows - 1) * row_b + 2 * D, 0x00020000);
+#pragma unroll
+      for (int u = 0; u < KQW; ++u)
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(
+            rsrc, (__attribute__((address_space(3))) void*)(lds + (4 * u + w) * 512), 16, voff,
+            64 * u, 0, 0);
+    };
+    auto load_k = [&](int buf, int kv0) { stage(kg, kbuf(buf), kv0, lane_k, k_c); };
+    auto load_v = [&](int buf, int kv0) { stage(vg, vbuf(buf), kv0, lane_v, v_c); };
+
+    // A operand of the QK MFMA: K[32 tt + l%32][16 ks + 8 hi + 0..7] = chunk
+    // 2ks + hi of row 32tt + l%32: group ks/2, slot (2(ks%2) + hi) ^ ((l/4)%4).
+    const int kr_m = hi ^ ((l >> 2) & 3);
+    const int kr_even = (l & 31) * 32 + 8 * kr_m, kr_odd = (l & 31) * 32 + 8 * (kr_m ^ 2);
+    auto kread = [&](int buf, int tt, int ks) {
+      const int off = (ks >> 1) * (BN * 32) + tt * 1024 + ((ks & 1) ? kr_odd : kr_even);
+      return *reinterpret_cast<const bf16x8*>(kbuf(buf) + off);
+    };
+    // A operand of P.V k-step kk = 2tt + hh: V^T[32 et + l%32][keys 32tt + 16hh
+    // + 8m + 4hi + 0..3, m = 0, 1], i.e. k-slot 8hi + jj <-> key
+    // 32tt + 16hh + 8(jj/4) + 4hi + jj%4, the order of the S^T accumulator.
+    // Two transposing LDS reads (4 keys each) gather it from the token-major
+    // tile: within each 16-lane group, lane i receives element i%4 of the
+    // 8-byte rows read by lanes 4j + i/4, j = 0..3; so source lane s reads key
+    // base + s/4, dims 32et + 16((l/16)%2) + 4(s%4) .. + 3, and lane i ends up
+    // with dim 32et + 16((l/16)%2) + i of keys base .. base + 3.
+    const int vr_base = 128 * hi + 32 * ((l & 15) >> 2) + 16 * ((l >> 4) & 1) + 4 * (l & 3);
+    auto vread = [&](int buf, int kk, int et) {
+      typedef short s16x4_t __attribute__((ext_vector_type(4)));
+      typedef __attribute__((address_space(3))) s16x4_t* lds_s16x4;
+      const uint16_t* p = vbuf(buf) + et * (BN * 32) + (16 * kk) * 32 + vr_base;
+      const s16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4)(p));
+      const s16x4_t hi4 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4)(p + 8 * 32));
+      const s16x4_t both[2] = {lo, hi4};
+      bf16x8 res;
+      __builtin_memcpy(&res, both, 16);
+      return res;
+    };
+
+    // Scores stay raw until the exponent: p = 2^(s*c - m) as one fma, with the
+    // running max m kept in the scaled domain.  For c <= 0 the scores are
+    // scaled first and c is taken as 1, so the max is always taken on the
+    // exponent.
+    const float c_in = a.scale_log2;
+    const bool pos_scale = c_in > 0.f;
+    const float c_eff = pos_scale ? c_in : 1.f;
+    // Lazy rescaling on masked tiles: the running max only moves when a tile
+    // raises it by more than kLazy (log2 units).
+    constexpr float kLazy = 8.f;
+    // Steady-state trigger: a half-row sum beyond 2^kSumLazy (so every p
+    // stays far below overflow while it does not fire).
+    constexpr float kSumLazy = 20.f;
+    // Last key this lane's row may see (causal and end of request).
+    const int last_key = min(myq, kv_end - 1);
+
+    f32x16 sa[2], sb[2];  // S^T of two consecutive key tiles (current / next)
+    bf16x8 pb[4];         // P^T of the current tile: B operands of the four P.V k-steps
+    constexpr int kValu = 0x002, kMfma = 0x008, kDsRead = 0x100;
+
+    auto zero2 = [&](f32x16* s) {
+#pragma unroll
+      for (int tt = 0; tt < 2; ++tt)
+#pragma unroll
+        for (int x = 0; x < 16; ++x) s[tt][x] = 0.f;
+    };
+    // Max of this lane pair's query row over the tile, in the exp2 domain
+    // (maximum, not fmaxf: no NaN quieting of the MFMA results, 3-input ops).
+    auto row_max = [&](const f32x16* s) {
+      float mx = __builtin_elementwise_maximum(s[0][0], s[1][0]);
+#pragma unroll
+      for (int x = 1; x < 16; ++x)
+        mx = __builtin_elementwise_maximum(mx, __builtin_elementwise_maximum(s[0][x], s[1][x]));
       const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx),
                                                        false, false);
-      mx = fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1]));  // max with lane ^ 32
-    }
-    const float m_tile = mx * c_eff;  // finite: key 0 is seen in the first sub-tile
-    if (__ballot(m_tile > m_run + kLazy)) {  // wave-uniform
+      return __builtin_elementwise_maximum(__uint_as_float(sw[0]), __uint_as_float(sw[1])) * c_eff;
+    };
+    auto rescale_to = [&](float m_tile) {
       const float m_new = fmaxf(m_run, m_tile);
       const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
       m_run = m_new;
       l_run *= alpha;
 #pragma unroll
       for (int et = 0; et < ET; ++et) oacc[et] *= alpha;
-    }
-    float psum = 0.f;
+    };
+    // pb = 2^(s c - m) rounded to bf16; returns this lane's half-row sum of
+    // the rounded values (the weights the P.V product uses), two at a time.
+    auto exponent = [&](const f32x16* s) {
 #pragma unroll
-    for (int tt = 0; tt < 2; ++tt)
+      for (int tt = 0; tt < 2; ++tt)
 #pragma unroll
-      for (int x = 0; x < 16; ++x) {
-        const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(st[tt][x], c_eff, -m_run));
-        psum += p;
-        pb[2 * tt + (x >> 3)][x & 7] = (__bf16)p;
+        for (int x = 0; x < 16; ++x)
+          pb[2 * tt + (x >> 3)][x & 7] =
+              (__bf16)__builtin_amdgcn_exp2f(__builtin_fmaf(s[tt][x], c_eff, -m_run));
+      typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+      const bf16x2_t ones = {(__bf16)1.f, (__bf16)1.f};
+      float ps0 = 0.f, ps1 = 0.f;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        ps0 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pb[i], pb[i], 0, 1), ones, ps0, false);
+        ps1 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pb[i], pb[i], 2, 3), ones, ps1, false);
+        ps0 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pb[i], pb[i], 4, 5), ones, ps0, false);
+        ps1 = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(pb[i], pb[i], 6, 7), ones, ps1, false);
       }
-    l_run += psum;
-  };
+      return ps0 + ps1;
+    };
+    auto qk = [&](int buf, f32x16* s) {
+      bf16x8 ka[2][KS];
+#pragma unroll
+      for (int tt = 0; tt < 2; ++tt)
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) ka[tt][ks] = kread(buf, tt, ks);
+      zero2(s);
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+        for (int tt = 0; tt < 2; ++tt)
+          s[tt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[tt][ks], qop[ks], s[tt], 0, 0, 0);
+      __builtin_amdgcn_sched_group_barrier(kDsRead, 4, 0);
+#pragma unroll
+      for (int ks = 0; ks < KS - 2; ++ks) {
+        __builtin_amdgcn_sched_group_barrier(kMfma, 2, 0);
+        __builtin_amdgcn_sched_group_barrier(kDsRead, 2, 0);
+      }
+      __builtin_amdgcn_sched_group_barrier(kMfma, 4, 0);
+    };
+    auto pv = [&](int buf) {  // O^T += V^T P^T of the tile
+      bf16x8 va[4][ET];
+#pragma unroll
+      for (int kk = 0; kk < 4; ++kk)
+#pragma unroll
+        for (int et = 0; et < ET; ++et) va[kk][et] = vread(buf, kk, et);
+#pragma unroll
+      for (int kk = 0; kk < 4; ++kk)
+#pragma unroll
+        for (int et = 0; et < ET; ++et)
+          oacc[et] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[kk][et], pb[kk], oacc[et], 0, 0, 0);
+      __builtin_amdgcn_sched_group_barrier(kDsRead, 2 * ET, 0);
+#pragma unroll
+      for (int kk = 0; kk < 3; ++kk)
+#pragma unroll
+        for (int et = 0; et < ET; ++et) {
+          __builtin_amdgcn_sched_group_barrier(kMfma, 1, 0);
+          __builtin_amdgcn_sched_group_barrier(kDsRead, 2, 0);
+        }
+      __builtin_amdgcn_sched_group_barrier(kMfma, ET, 0);
+    };
+    auto softmax_masked = [&](f32x16* s, int kv0) {
+      if (!pos_scale) {
+#pragma unroll
+        for (int tt = 0; tt < 2; ++tt) s[tt] *= c_in;
+      }
+      const int lim = last_key - kv0 - 4 * hi;  // lane holds keys kv0 + 32tt + 8(x/4) + 4hi + x%4
+#pragma unroll
+      for (int tt = 0; tt < 2; ++tt)
+#pragma unroll
+        for (int x = 0; x < 16; ++x)
+          if (32 * tt + 8 * (x >> 2) + (x & 3) > lim) s[tt][x] = -INFINITY;
+      const float m_tile = row_max(s);  // finite: every row sees key 0 in the first tile
+      if (__ballot(m_tile > m_run + kLazy)) rescale_to(m_tile);  // wave-uniform
+      l_run += exponent(s);
+    };
+    // Steady-state step, first part: the softmax of tile j on the VALU while
+    // the MFMAs compute S^T of tile j + 1 (K buffer kb).
+    auto half_qk = [&](f32x16* sc, f32x16* sn, int kb) {
+      bf16x8 ka[2][KS];
+#pragma unroll
+      for (int tt = 0; tt < 2; ++tt)
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) ka[tt][ks] = kread(kb, tt, ks);
+      zero2(sn);
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+        for (int tt = 0; tt < 2; ++tt)
+          sn[tt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[tt][ks], qop[ks], sn[tt], 0, 0, 0);
+      float psum = exponent(sc);
+      constexpr int NM = 2 * KS;  // MFMAs of this region
+      __builtin_amdgcn_sched_group_barrier(kDsRead, 4, 0);
+#pragma unroll
+      for (int i = 0; i < NM; ++i) {
+        __builtin_amdgcn_sched_group_barrier(kMfma, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(kValu, 100 / NM, 0);
+        if (i + 4 < NM) __builtin_amdgcn_sched_group_barrier(kDsRead, 1, 0);
+      }
+      if (__ballot(!(psum <= __builtin_exp2f(kSumLazy)))) {  // wave-uniform, rare
+        rescale_to(row_max(sc));
+        psum = exponent(sc);
+      }
+      l_run += psum;
+    };
 
-  // Stages of 128 keys, double-buffered in LDS; the next stage's global loads
-  // are in flight while the current one is computed as two 64-key sub-tiles;
-  // one barrier per stage.
-  gload_k(0);
-  gload_v(0);
-  lstore_k(0);
-  lstore_v(0);
-  __syncthreads();
-  for (int j = 0; j < ntiles; ++j) {
-    const int cur = j & 1;
-    gload_k((j + 1) * BN);  // unconditional: past the end it re-reads the last row
-    gload_v((j + 1) * BN);
-#pragma unroll
-    for (int sub = 0; sub < BN / SUB; ++sub) {
-      const int kv0 = j * BN + SUB * sub;
-      if (wave_active && kv0 < kv_end && kv0 <= row_w + 31) {  // some key visible to this wave
-        qk(cur, sub);
-        softmax(kv0);
-        pv(cur, sub);
-      }
-    }
-    if (j + 1 < ntiles) {
-      lstore_k(cur ^ 1);  // that buffer was last read before the previous barrier
-      lstore_v(cur ^ 1);
-    }
+    // K tile s sits in K buffer s % 2 and V tile s in V buffer s % 2; K runs
+    // one tile ahead of V.  A step j: loads K(j + 2) and V(j + 1) into the
+    // free buffers, computes S^T(j + 1) with the softmax of tile j, then
+    // O^T += V^T P^T of tile j; one barrier (which also waits for the loads).
+    load_k(0, 0);
+    if (ntiles > 1) load_k(1, BN);
+    load_v(0, 0);
     __syncthreads();
-  }
+    if (wave_active) qk(0, sa);  // every active row sees key 0
+    // The steady-state steps form p against the running max without taking
+    // the tile's max, so start it at the first tile's max (tile 0 is
+    // unmasked there).
+    if (wave_active && pos_scale && q0 > 0) m_run = row_max(sa);
 
-  if (!wave_active || myq >= L) return;
-  float l_tot = l_run + __shfl_xor(l_run, 32, 64);
-  const float inv = 1.f / l_tot;
-  // lane holds O^T[e = 32et + 8(x/4) + 4hi + x%4][myq]
-  uint16_t* op = a.out + ((int64_t)(seq0 + myq) * a.hq + h) * D + 4 * hi;
-#pragma unroll
-  for (int et = 0; et < ET; ++et)
-#pragma unroll
-    for (int gq = 0; gq < 4; ++gq) {
-      u32x2 x;
-      x[0] = pack_bf16x2(oacc[et][4 * gq] * inv, oacc[et][4 * gq + 1] * inv);
-      x[1] = pack_bf16x2(oacc[et][4 * gq + 2] * inv, oacc[et][4 * gq + 3] * inv);
-      *reinterpret_cast<u32x2*>(op + 32 * et + 8 * gq) = x;
+    // Tiles every row of the item sees in full (positive scales only).
+    const int nfull = pos_scale ? q0 / BN : 0;
+    int j = 0;
+    auto prefetch = [&](int jj, auto par) {  // K(jj + 2) -> K buffer par, V(jj + 1) -> V buffer par ^ 1
+      if (jj + 2 < ntiles) load_k(par(), (jj + 2) * BN);
+      if (jj + 1 < ntiles) load_v(par() ^ 1, (jj + 1) * BN);
+    };
+    auto even = [] { return 0; };
+    auto odd = [] { return 1; };
+    auto step_full = [&](f32x16* sc, f32x16* sn, auto par) {
+      prefetch(j, par);
+      if (wave_active) {
+        half_qk(sc, sn, par() ^ 1);
+        pv(par());
+      }
+      __syncthreads();
+    };
+    for (; j + 1 < nfull; j += 2) {
+      step_full(sa, sb, even);
+      ++j;
+      step_full(sb, sa, odd);
+      --j;
     }
-  if (a.lse && hi == 0) a.lse[(int64_t)(seq0 + myq) * a.hq + h] = (m_run + __log2f(l_tot)) * kLn2;
+    if (j < nfull) {
+      step_full(sa, sb, even);
+      ++j;
+#pragma unroll
+      for (int tt = 0; tt < 2; ++tt) sa[tt] = sb[tt];
+    }
+    // Diagonal and ragged tiles: masked softmax, then S^T of the next tile.
+    auto step_tail = [&](auto par) {
+      prefetch(j, par);
+      if (wave_active && j * BN <= row_w + 31) {  // some key of tile j visible to this wave
+        softmax_masked(sa, j * BN);
+        pv(par());
+      }
+      if (wave_active && j + 1 < ntiles && (j + 1) * BN <= row_w + 31) qk(par() ^ 1, sa);
+      __syncthreads();
+    };
+    for (; j < ntiles; ++j) {
+      if (j & 1) step_tail(odd);
+      else step_tail(even);
+    }
+    if (!wave_active || myq >= L) return;
+    float l_tot = l_run + __shfl_xor(l_run, 32, 64);
+    const float inv = 1.f / l_tot;
+    // lane holds O^T[e = 32et + 8(x/4) + 4hi + x%4][myq]
+    uint16_t* op = a.out + ((int64_t)(seq0 + myq) * a.hq + h) * D + 4 * hi;
+#pragma unroll
+    for (int et = 0; et < ET; ++et)
+#pragma unroll
+      for (int gq = 0; gq < 4; ++gq) {
+        u32x2 x;
+        x[0] = pack_bf16x2(oacc[et][4 * gq] * inv, oacc[et][4 * gq + 1] * inv);
+        x[1] = pack_bf16x2(oacc[et][4 * gq + 2] * inv, oacc[et][4 * gq + 3] * inv);
+        *reinterpret_cast<u32x2*>(op + 32 * et + 8 * gq) = x;
+      }
+    if (a.lse && hi == 0) a.lse[(int64_t)(seq0 + myq) * a.hq + h] = (m_run + __log2f(l_tot)) * kLn2;
+  }
 }
 
 }  // namespace dopd
