@@ -33,6 +33,8 @@ def _lib():
         lib.oracle_prefill_rows.argtypes = [i32, i32, i32, i32, C.c_float, P, P, P, P, i32,
                                             P, P, i32, P, P]
         lib.oracle_decode.argtypes = [i32, i32, i32, i32, C.c_float, P, P, P, P, i32, P, i32, P, P]
+        lib.oracle_prefill_paged.argtypes = [i32, i32, i32, i32, C.c_float, P, P, P, P, i32, P,
+                                             P, i32, P, P, i32, P, P]
         lib.oracle_kv_write.argtypes = [i32, i32, i32, P, P, P, P, P, i32, P, P, i32]
         lib.oracle_pack.argtypes = [i32, i32, i32, i32, P, P, i32, P, i32, P, P, P, i32, P]
         lib.oracle_unpack.argtypes = [i32, i32, i32, i32, P, P, P, P, i32, P, P, i32, P, i32]
@@ -104,6 +106,40 @@ def decode(q, k_pool, v_pool, page_table, context_lens, scale):
                               _p(pt), pt.shape[1], _p(ctx), b, _p(out), _p(lse))
     if rc:
         raise ValueError(f"oracle_decode rc={rc}")
+    return out, lse
+
+
+def prefill_paged(q, k_pool, v_pool, page_table, cu_q, prefix_lens, scale, tok=None, head=None):
+    """Chunk prefill over the paged cache (oracle.c: oracle_prefill_paged).
+
+    Request r holds prefix_lens[r] cached tokens plus the chunk rows
+    cu_q[r] .. cu_q[r+1]-1 of q[T][Hq][d], whose K/V are already in the pool;
+    chunk token i attends to cached positions 0 .. prefix_lens[r] + i.
+    Returns (out[T][Hq][d], lse[T][Hq]), or, with tok/head given, the
+    (out[n][d], lse[n]) of those (token, head) rows only."""
+    q, k_pool, v_pool = _c(q), _c(k_pool), _c(v_pool)
+    pt = _c(page_table, np.int32)
+    cu = _c(cu_q, np.int32)
+    pre = _c(prefix_lens, np.int32)
+    t, hq, d = q.shape
+    hkv = k_pool.shape[-3]
+    if tok is None:
+        tk = hd = None
+        nrows = 0
+        out = np.zeros((t, hq, d), np.float64)
+        lse = np.zeros((t, hq), np.float64)
+    else:
+        tk, hd = _c(tok, np.int32), _c(head, np.int32)
+        nrows = len(tk)
+        out = np.zeros((nrows, d), np.float64)
+        lse = np.zeros((nrows,), np.float64)
+    rc = _lib().oracle_prefill_paged(_dt(q), hq, hkv, d, float(scale), _p(q), _p(k_pool),
+                                     _p(v_pool), _p(pt), pt.shape[1], _p(cu), _p(pre), len(pre),
+                                     _p(tk) if tk is not None else None,
+                                     _p(hd) if hd is not None else None, nrows, _p(out),
+                                     _p(lse))
+    if rc:
+        raise ValueError(f"oracle_prefill_paged rc={rc}")
     return out, lse
 
 

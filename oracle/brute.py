@@ -66,3 +66,29 @@ def decode(q, k_pool, v_pool, page_table, context_lens, scale):
             out[r, h] = attention_dense(qf[r, h][None, :], kk[:, h // g], vv[:, h // g],
                                         sigma, False)[0]
     return out
+
+
+def prefill_paged(q, k_pool, v_pool, page_table, cu_q, prefix_lens, scale):
+    """Chunk prefill over the paged cache as dense masked algebra: request r's
+    cached sequence (prefix + chunk, already in the pools) is gathered whole,
+    and chunk row i may see key j iff j <= prefix_lens[r] + i (the chunk sits
+    at the end of the cache)."""
+    qf = widen(q)
+    sigma = float(np.float32(scale))
+    hq, hkv = q.shape[1], k_pool.shape[1]
+    g = hq // hkv
+    out = np.zeros_like(qf)
+    for r in range(len(cu_q) - 1):
+        a, b = int(cu_q[r]), int(cu_q[r + 1])
+        n, pre = b - a, int(prefix_lens[r])
+        if n == 0:
+            continue
+        kk, vv = gather_context(k_pool, v_pool, page_table, r, pre + n)
+        kk, vv = widen(kk), widen(vv)
+        rows = np.arange(n)[:, None] + pre
+        cols = np.arange(pre + n)[None, :]
+        for h in range(hq):
+            s = sigma * (qf[a:b, h] @ kk[:, h // g].T)
+            s = np.where(cols > rows, -np.inf, s)
+            out[a:b, h] = softmax_rows(s) @ vv[:, h // g]
+    return out

@@ -182,6 +182,66 @@ int oracle_decode(int dtype, int hq, int hkv, int d, float scale, const void *q,
   return 0;
 }
 
+/* Prefill of a chunk over the paged cache (a prompt processed in chunks, or a
+ * request that already holds a cached prefix): request r has prefix_lens[r]
+ * cached tokens and a chunk of n_r = cu_q[r+1] - cu_q[r] new tokens whose K/V
+ * are already written at positions prefix_lens[r] .. + n_r - 1.  Chunk token i
+ * (query row cu_q[r] + i, position prefix_lens[r] + i) attends to the cached
+ * positions 0 .. prefix_lens[r] + i: causal with the chunk aligned to the end
+ * of the cache.  q/out [T][Hq][d], lse [T][Hq].  With rows != NULL only the
+ * nrows (token, head) pairs tok[n], head[n] are computed, into out[n][d] and
+ * lse[n]. */
+int oracle_prefill_paged(int dtype, int hq, int hkv, int d, float scale, const void *q,
+                         const void *k_pool, const void *v_pool, const int32_t *page_table,
+                         int pt_stride, const int32_t *cu_q, const int32_t *prefix_lens,
+                         int nreq, const int32_t *tok, const int32_t *head, int nrows,
+                         double *out, double *lse) {
+  if (hkv <= 0 || hq % hkv) return 1;
+  const int g = hq / hkv;
+  const double sigma = (double)scale;
+  int maxlen = 0;
+  for (int r = 0; r < nreq; ++r) {
+    const int len = prefix_lens[r] + cu_q[r + 1] - cu_q[r];
+    if (len > maxlen) maxlen = len;
+  }
+  const int64_t T = cu_q[nreq];
+  const int64_t total = tok ? nrows : T * hq;
+  int bad = 0;
+#pragma omp parallel
+  {
+    double *sc = (double *)malloc(sizeof(double) * (maxlen + 1));
+    int64_t *koff = (int64_t *)malloc(sizeof(int64_t) * (maxlen + 1));
+    int64_t *voff = (int64_t *)malloc(sizeof(int64_t) * (maxlen + 1));
+#pragma omp for schedule(dynamic, 1)
+    for (int64_t n = 0; n < total; ++n) {
+      const int64_t t = tok ? tok[n] : n / hq;
+      const int h = tok ? head[n] : (int)(n % hq);
+      int r = 0;
+      while (r < nreq && cu_q[r + 1] <= t) ++r;
+      if (t < 0 || r == nreq || h < 0 || h >= hq) {
+#pragma omp atomic write
+        bad = 1;
+        continue;
+      }
+      const int c = h / g;
+      const int nkeys = prefix_lens[r] + (int)(t - cu_q[r]) + 1;
+      for (int j = 0; j < nkeys; ++j) {
+        const int64_t page = page_table[(int64_t)r * pt_stride + j / OR_PAGE];
+        const int slot = j % OR_PAGE;
+        koff[j] = ((page * hkv + c) * OR_PAGE + slot) * d;
+        voff[j] = (page * hkv + c) * (int64_t)d * OR_PAGE + slot;
+      }
+      const int64_t orow = tok ? n : t * hq + h;
+      attend_row(dtype, d, sigma, q, (t * hq + h) * d, k_pool, koff, 1, v_pool, voff, OR_PAGE,
+                 nkeys, sc, out + orow * d, lse ? lse + orow : NULL);
+    }
+    free(sc);
+    free(koff);
+    free(voff);
+  }
+  return bad ? 2 : 0;
+}
+
 /* Paged write: for request r, new tokens at logical positions
  * p in [start[r], start[r] + n_r) with n_r = cu_new[r+1]-cu_new[r] come from
  * rows cu_new[r] + (p - start[r]) of k_new/v_new[T][Hkv][d].  Bit copy. */

@@ -40,6 +40,14 @@ MUTANTS = {
     "unpack_kv_swapped": [("if (c == 0) {\n                dst", "if (c == 1) {\n                dst")],
     "unpack_slot_off_by_one": [("const int slot = t % OR_PAGE;\n            const int64_t lp = (int64_t)layer * num_pages + page;\n            for (int e = 0; e < d; ++e) {\n              const int64_t src = off[n]",
                                 "const int slot = (t + 1) % OR_PAGE;\n            const int64_t lp = (int64_t)layer * num_pages + page;\n            for (int e = 0; e < d; ++e) {\n              const int64_t src = off[n]")],
+    "paged_prefill_top_left": [("const int nkeys = prefix_lens[r] + (int)(t - cu_q[r]) + 1;",
+                                "const int nkeys = (int)(t - cu_q[r]) + 1;")],
+    "paged_prefill_prefix_off_by_one": [("const int nkeys = prefix_lens[r] + (int)(t - cu_q[r]) + 1;",
+                                         "const int nkeys = (prefix_lens[r] > 0 ? prefix_lens[r] - 1 : 0) + (int)(t - cu_q[r]) + 1;")],
+    "paged_prefill_chunk_row_as_q_row": [("attend_row(dtype, d, sigma, q, (t * hq + h) * d, k_pool",
+                                          "attend_row(dtype, d, sigma, q, ((t - cu_q[r]) * hq + h) * d, k_pool")],
+    "paged_prefill_v_token_major": [("k_pool, koff, 1, v_pool, voff, OR_PAGE,\n                 nkeys",
+                                     "k_pool, koff, 1, v_pool, koff, 1,\n                 nkeys")],
     "pack_token_dim_transposed": [("const int64_t dst = off[n] + ((((int64_t)layer * 2 + c) * hkv + h) * len + t) * d + e;",
                                    "const int64_t dst = off[n] + ((((int64_t)layer * 2 + c) * hkv + h) * d + e) * len + t;")],
 }
@@ -62,7 +70,7 @@ def _load(path):
     lib = ctypes.CDLL(path)
     real = oracle._lib()
     for f in ("oracle_prefill", "oracle_prefill_rows", "oracle_decode", "oracle_kv_write",
-              "oracle_pack", "oracle_unpack"):
+              "oracle_pack", "oracle_unpack", "oracle_prefill_paged"):
         getattr(lib, f).argtypes = getattr(real, f).argtypes
         getattr(lib, f).restype = getattr(real, f).restype
     return lib
@@ -176,9 +184,47 @@ def chk_unpack_matches_write():
     return bool(np.array_equal(ku, kw) and np.array_equal(vu, vw))
 
 
+def _paged_pool(rng, prefix, chunk, hq, hkv, d, dtype):
+    total = np.asarray(prefix, np.int32) + np.asarray(chunk, np.int32)
+    pt, num_pages = I.allocate_pages(rng, total, pool_pages=int(np.sum((total + 15) // 16)) + 2)
+    kp, vp = I.empty_pools(num_pages, hkv, d, dtype)
+    _, kf, vf = I.prefill_batch(rng, total, hq, hkv, d, dtype)
+    kp, vp = oracle.kv_write(kf, vf, kp, vp, pt, I.cu_from_lens(total),
+                             np.zeros(len(total), np.int32))
+    q = I.normal(rng, (int(np.sum(chunk)), hq, d), dtype)
+    return q, kp, vp, pt, I.cu_from_lens(chunk), np.asarray(prefix, np.int32)
+
+
+def chk_paged_prefill_brute():
+    rng = np.random.default_rng(31)
+    q, kp, vp, pt, cu, pre = _paged_pool(rng, [20, 3, 0], [5, 18, 7], 4, 2, 8, "fp32")
+    out, _ = oracle.prefill_paged(q, kp, vp, pt, cu, pre, 0.4)
+    return _close(out, brute.prefill_paged(q, kp, vp, pt, cu, pre, 0.4), 1e-11)
+
+
+def chk_chunked_equals_one_shot():
+    rng = np.random.default_rng(32)
+    L, hq, hkv, d = 37, 2, 1, 8
+    q, k, v = I.prefill_batch(rng, np.array([L]), hq, hkv, d, "bf16")
+    ref, _ = oracle.prefill(q, k, v, I.cu_from_lens([L]), 0.3)
+    pt, num_pages = I.allocate_pages(rng, np.array([L]), pool_pages=4)
+    kp, vp = I.empty_pools(num_pages, hkv, d, "bf16")
+    done = 0
+    for n in (9, 1, 20, 7):
+        rows = slice(done, done + n)
+        kp, vp = oracle.kv_write(k[rows], v[rows], kp, vp, pt, I.cu_from_lens([n]),
+                                 np.array([done], np.int32))
+        out, _ = oracle.prefill_paged(q[rows], kp, vp, pt, I.cu_from_lens([n]),
+                                      np.array([done], np.int32), 0.3)
+        if not _close(out, ref[rows], 1e-12):
+            return False
+        done += n
+    return True
+
+
 CHECKS = [chk_prefill_brute, chk_prefill_sdpa, chk_lse, chk_decode_brute,
           chk_last_row_equals_decode, chk_write_pack_transpose, chk_closed_forms,
-          chk_unpack_matches_write]
+          chk_unpack_matches_write, chk_paged_prefill_brute, chk_chunked_equals_one_shot]
 
 
 def _run_checks():

@@ -290,3 +290,92 @@ def test_unpack_inverts_pack_into_another_page_order():
         oa, la = oracle.decode(q, ka[layer], va[layer], pt_a, lens, 0.35)
         ob, lb = oracle.decode(q, kb[layer], vb[layer], pt_b, lens, 0.35)
         assert np.array_equal(oa, ob) and np.array_equal(la, lb)
+
+
+# ---- chunk prefill over the paged cache (prefix-aware, chunk at the end) ----
+def _paged_case(seed, prefix, chunk, hq, hkv, d, dtype, extra_pages=3):
+    """Requests with cached prefixes whose chunks are already written: full
+    sequences of prefix+chunk tokens go through the paged write (start 0), and
+    the chunk rows of Q are drawn separately."""
+    rng = np.random.default_rng(seed)
+    prefix, chunk = np.asarray(prefix, np.int32), np.asarray(chunk, np.int32)
+    total = prefix + chunk
+    pt, num_pages = I.allocate_pages(rng, total, pool_pages=int(np.sum((total + 15) // 16)) + extra_pages)
+    k_pool, v_pool = I.empty_pools(num_pages, hkv, d, dtype)
+    _, kf, vf = I.prefill_batch(rng, total, hq, hkv, d, dtype)
+    k_pool, v_pool = oracle.kv_write(kf, vf, k_pool, v_pool, pt, I.cu_from_lens(total),
+                                     np.zeros(len(total), np.int32))
+    q = I.normal(rng, (int(chunk.sum()), hq, d), dtype)
+    return q, k_pool, v_pool, pt, I.cu_from_lens(chunk), prefix
+
+
+PAGED = [
+    # prefix, chunk, hq, hkv, d
+    ([0], [9], 2, 1, 8),
+    ([16, 5, 0], [1, 7, 20], 4, 2, 16),
+    ([33, 47], [16, 3], 8, 2, 8),
+    ([100], [40], 3, 1, 16),
+]
+
+
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+@pytest.mark.parametrize("prefix,chunk,hq,hkv,d", PAGED)
+def test_prefill_paged_matches_dense_bruteforce(dtype, prefix, chunk, hq, hkv, d):
+    q, kp, vp, pt, cu, pre = _paged_case(21, prefix, chunk, hq, hkv, d, dtype)
+    out, _ = oracle.prefill_paged(q, kp, vp, pt, cu, pre, 0.37)
+    ref = brute.prefill_paged(q, kp, vp, pt, cu, pre, 0.37)
+    assert np.isfinite(out).all() and np.isfinite(ref).all()
+    np.testing.assert_allclose(out, ref, rtol=0, atol=RTOL * 10)
+
+
+@pytest.mark.parametrize("pieces", [[40], [1, 39], [16, 16, 8], [5, 1, 30, 4], [1] * 12 + [28]])
+def test_chunked_prefill_equals_one_shot(pieces):
+    """A prompt processed chunk by chunk (each chunk written to the cache and
+    attended with the earlier chunks as its prefix) gives the one-shot prefill."""
+    rng = np.random.default_rng(23)
+    hq, hkv, d, L = 4, 2, 16, int(sum(pieces))
+    q, k, v = I.prefill_batch(rng, np.array([L]), hq, hkv, d, "bf16")
+    ref, ref_lse = oracle.prefill(q, k, v, I.cu_from_lens([L]), 0.25)
+    pt, num_pages = I.allocate_pages(rng, np.array([L]), pool_pages=(L + 15) // 16 + 4)
+    kp, vp = I.empty_pools(num_pages, hkv, d, "bf16")
+    done = 0
+    for n in pieces:
+        rows = slice(done, done + n)
+        kp, vp = oracle.kv_write(k[rows], v[rows], kp, vp, pt, I.cu_from_lens([n]),
+                                 np.array([done], np.int32))
+        out, lse = oracle.prefill_paged(q[rows], kp, vp, pt, I.cu_from_lens([n]),
+                                        np.array([done], np.int32), 0.25)
+        np.testing.assert_allclose(out, ref[rows], rtol=0, atol=1e-12)
+        np.testing.assert_allclose(lse, ref_lse[rows], rtol=0, atol=1e-12)
+        done += n
+
+
+def test_prefill_paged_chunk_of_one_is_a_decode_step():
+    q, kp, vp, pt, cu, pre = _paged_case(24, [30, 0, 17], [1, 1, 1], 4, 1, 16, "bf16")
+    out, lse = oracle.prefill_paged(q, kp, vp, pt, cu, pre, 0.3)
+    dec, dlse = oracle.decode(q, kp, vp, pt, pre + 1, 0.3)
+    assert np.isfinite(out).all()
+    np.testing.assert_allclose(out, dec, rtol=0, atol=1e-12)
+    np.testing.assert_allclose(lse, dlse, rtol=0, atol=1e-12)
+
+
+def test_prefill_paged_invariant_under_page_permutation():
+    q, kp, vp, pt, cu, pre = _paged_case(25, [20, 3], [13, 30], 4, 2, 8, "bf16")
+    out, _ = oracle.prefill_paged(q, kp, vp, pt, cu, pre, 0.3)
+    rng = np.random.default_rng(5)
+    perm = rng.permutation(kp.shape[0])          # new page id of old page p: perm[p]
+    kp2, vp2 = np.empty_like(kp), np.empty_like(vp)
+    kp2[perm], vp2[perm] = kp, vp
+    pt2 = np.where(pt >= 0, perm[np.maximum(pt, 0)], -1).astype(np.int32)
+    out2, _ = oracle.prefill_paged(q, kp2, vp2, pt2, cu, pre, 0.3)
+    assert np.isfinite(out).all() and np.array_equal(out, out2)
+
+
+def test_prefill_paged_sampled_rows_match_full():
+    q, kp, vp, pt, cu, pre = _paged_case(26, [18, 40], [22, 9], 6, 3, 16, "fp32")
+    out, lse = oracle.prefill_paged(q, kp, vp, pt, cu, pre, 0.2)
+    tok = np.array([0, 5, 21, 22, 30], np.int32)
+    head = np.array([0, 5, 3, 1, 2], np.int32)
+    o2, l2 = oracle.prefill_paged(q, kp, vp, pt, cu, pre, 0.2, tok=tok, head=head)
+    assert np.isfinite(out).all()
+    assert np.array_equal(o2, out[tok, head]) and np.array_equal(l2, lse[tok, head])
