@@ -87,6 +87,33 @@ dopd_status dopd_prefill_attn(const dopd_attn_shape* shape, const void* q, const
                               const int32_t* cu_seqlens_host, int32_t num_reqs, void* stream);
 
 /*
+ * Chunk prefill over the paged cache: the prefill of a request that already
+ * holds cached tokens, i.e. one chunk of a prompt processed in chunks (chunked
+ * prefill, Sec. III-A) or an ultra-short prefill merged into a D-instance's
+ * work next to decode (PD-aggregation, Sec. V-E).  Eq. 1 over the cache,
+ * causal with the chunk aligned to the end of the cache:
+ *   request r has prefix_lens[r] cached tokens and a chunk of
+ *   n_r = cu_seqlens[r+1] - cu_seqlens[r] new tokens whose K/V must already
+ *   be in the pools at positions prefix_lens[r] .. prefix_lens[r] + n_r - 1
+ *   (dopd_kv_write with start_pos = prefix_lens); chunk token i (row
+ *   cu_seqlens[r] + i of q/out [T][Hq][d]) attends to cached positions
+ *   0 .. prefix_lens[r] + i, read through page_table as in dopd_decode_attn.
+ *   cu_seqlens / prefix_lens are device arrays with identical host copies
+ *   (used to size and order the launch); lse (nullable) fp32 [T][Hq].
+ * A chunk of one token is a decode step with context_lens = prefix_lens + 1;
+ * prefix_lens = 0 with the whole prompt written first is dopd_prefill_attn.
+ * bf16: the same MFMA path and rounding as dopd_prefill_attn.  Returns
+ * DOPD_ERR_INVALID_SHAPE if a request's keys need more than page_table_stride
+ * pages.
+ */
+dopd_status dopd_prefill_paged_attn(const dopd_attn_shape* shape, const void* q,
+                                    const void* k_pool, const void* v_pool, int32_t num_pages,
+                                    const int32_t* page_table, int32_t page_table_stride,
+                                    const int32_t* cu_seqlens, const int32_t* cu_seqlens_host,
+                                    const int32_t* prefix_lens, const int32_t* prefix_lens_host,
+                                    int32_t num_reqs, void* out, float* lse, void* stream);
+
+/*
  * Paged KV write: request r appends n_r = cu_new_tokens[r+1] - cu_new_tokens[r]
  * tokens at logical positions start_pos[r] .. start_pos[r] + n_r - 1, taken
  * from rows cu_new_tokens[r] .. of k_new/v_new[total_new_tokens][Hkv][d].

@@ -24,7 +24,7 @@ DOPD_BF16, DOPD_FP32 = 0, 1
 PAGE_SIZE = 16
 
 EXPORTS = (
-    "dopd_prefill_attn", "dopd_kv_write", "dopd_decode_attn", "dopd_decode_workspace_size",
+    "dopd_prefill_attn", "dopd_prefill_paged_attn", "dopd_kv_write", "dopd_decode_attn", "dopd_decode_workspace_size",
     "dopd_kv_pack_for_handoff", "dopd_kv_unpack_from_handoff", "dopd_validate_page_table_host",
     "dopd_status_string",
     "dopd_last_hip_error",
@@ -66,6 +66,7 @@ def lib():
         P, i32, sz = C.c_void_p, C.c_int32, C.c_size_t
         SP = C.POINTER(Shape)
         L.dopd_prefill_attn.argtypes = [SP, P, P, P, P, P, P, P, i32, P]
+        L.dopd_prefill_paged_attn.argtypes = [SP, P, P, P, i32, P, i32, P, P, P, P, i32, P, P, P]
         L.dopd_kv_write.argtypes = [SP, P, P, P, P, i32, P, i32, P, P, i32, i32, P]
         L.dopd_decode_attn.argtypes = [SP, P, P, P, i32, P, i32, P, P, i32, i32, P, P, P, sz, P]
         L.dopd_decode_workspace_size.argtypes = [SP, P, i32, i32]
@@ -76,7 +77,7 @@ def lib():
         L.dopd_status_string.argtypes = [i32]
         L.dopd_status_string.restype = C.c_char_p
         L.dopd_last_hip_error.restype = i32
-        for f in ("dopd_prefill_attn", "dopd_kv_write", "dopd_decode_attn",
+        for f in ("dopd_prefill_attn", "dopd_prefill_paged_attn", "dopd_kv_write", "dopd_decode_attn",
                   "dopd_kv_pack_for_handoff", "dopd_kv_unpack_from_handoff",
                   "dopd_validate_page_table_host"):
             getattr(L, f).restype = i32
@@ -122,6 +123,18 @@ def dopd_prefill_attn(shape, q, k, v, out, lse, cu_seqlens, cu_seqlens_host, num
     _check(lib().dopd_prefill_attn(C.byref(shape), _dptr(q), _dptr(k), _dptr(v), _dptr(out),
                                    _dptr(lse), _dptr(cu_seqlens), _hptr(cu_h), int(num_reqs),
                                    _stream(stream)), "dopd_prefill_attn")
+
+
+def dopd_prefill_paged_attn(shape, q, k_pool, v_pool, num_pages, page_table, page_table_stride,
+                            cu_seqlens, cu_seqlens_host, prefix_lens, prefix_lens_host, num_reqs,
+                            out, lse, stream=None):
+    cu_h = _host_i32(cu_seqlens_host)
+    pre_h = _host_i32(prefix_lens_host)
+    _check(lib().dopd_prefill_paged_attn(C.byref(shape), _dptr(q), _dptr(k_pool), _dptr(v_pool),
+                                         int(num_pages), _dptr(page_table), int(page_table_stride),
+                                         _dptr(cu_seqlens), _hptr(cu_h), _dptr(prefix_lens),
+                                         _hptr(pre_h), int(num_reqs), _dptr(out), _dptr(lse),
+                                         _stream(stream)), "dopd_prefill_paged_attn")
 
 
 def dopd_kv_write(shape, k_new, v_new, k_pool, v_pool, num_pages, page_table,

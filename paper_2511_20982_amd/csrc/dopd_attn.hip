@@ -131,6 +131,74 @@ dopd_status dopd_validate_page_table_host(const int32_t* pt, int32_t stride, int
 }
 
 // ---------------------------------------------------------------- prefill
+extern "C++" {
+namespace {
+
+// Plans and launches the bf16 prefill kernel over chunk lengths cu_host (and,
+// on the paged path, the cached prefixes prefix_host).  Work items are
+// (q tile, request, head); with at most 64 requests the XCD-aware order is
+// used, requests ranked by the keys their last row sees.
+template <bool PAGED>
+dopd_status launch_prefill_bf16(dopd::PrefillArgs a, int d, const int32_t* cu_host,
+                                const int32_t* prefix_host, int32_t nreq, hipStream_t strm) {
+  int max_len = 0;
+  int64_t tiles = 0;
+  for (int32_t r = 0; r < nreq; ++r) {
+    const int len = cu_host[r + 1] - cu_host[r];
+    max_len = std::max(max_len, len);
+    tiles += (len + dopd::kPfBM - 1) / dopd::kPfBM;
+  }
+  a.nreq = nreq;
+  a.max_tiles = (max_len + dopd::kPfBM - 1) / dopd::kPfBM;
+  a.hslots = (a.hq + dopd::kPfHeadsPerWG - 1) / dopd::kPfHeadsPerWG;
+  const int64_t items = tiles * a.hslots;
+  if (items > INT32_MAX / 2) return DOPD_ERR_INVALID_SHAPE;
+  int64_t blocks = items;
+  a.xcd_order = 0;
+  a.n_items = (int)items;
+  a.tiles_total = (int)tiles;
+  a.per_xcd = 0;
+  std::memset(a.ord, 0, sizeof(a.ord));
+  if (nreq <= dopd::kPfMaxOrdered) {
+    // requests by decreasing key count (stable), dealt to XCDs in contiguous slices
+    auto keys = [&](int r) {
+      return (int64_t)(cu_host[r + 1] - cu_host[r]) + (PAGED ? prefix_host[r] : 0);
+    };
+    int order[dopd::kPfMaxOrdered];
+    for (int32_t r = 0; r < nreq; ++r) order[r] = r;
+    std::stable_sort(order, order + nreq, [&](int x, int y) { return keys(x) > keys(y); });
+    for (int32_t r = 0; r < nreq; ++r) a.ord[r] = (uint8_t)order[r];
+    a.xcd_order = 1;
+    a.per_xcd = (int)((items + dopd::kNumXcd - 1) / dopd::kNumXcd);
+    blocks = (int64_t)a.per_xcd * dopd::kNumXcd;
+  }
+  if (blocks == 0) return DOPD_OK;
+  if (d == 64)
+    hipLaunchKernelGGL((dopd::prefill_bf16_kernel<64, PAGED>), dim3((unsigned)blocks),
+                       dim3(dopd::kPfThreads), 0, strm, a);
+  else
+    hipLaunchKernelGGL((dopd::prefill_bf16_kernel<128, PAGED>), dim3((unsigned)blocks),
+                       dim3(dopd::kPfThreads), 0, strm, a);
+  return launch_status();
+}
+
+dopd::PrefillArgs prefill_args(const dopd_attn_shape* s, const void* q, void* out, float* lse,
+                               const int32_t* cu) {
+  dopd::PrefillArgs a;
+  std::memset(&a, 0, sizeof(a));
+  a.q = (const uint16_t*)q;
+  a.out = (uint16_t*)out;
+  a.lse = lse;
+  a.cu = cu;
+  a.hq = s->num_q_heads;
+  a.hkv = s->num_kv_heads;
+  a.scale_log2 = s->softmax_scale * dopd::kLog2e;
+  return a;
+}
+
+}  // namespace
+}  // extern "C++"
+
 dopd_status dopd_prefill_attn(const dopd_attn_shape* s, const void* q, const void* k,
                               const void* v, void* out, float* lse, const int32_t* cu,
                               const int32_t* cu_host, int32_t nreq, void* stream) {
@@ -140,14 +208,8 @@ dopd_status dopd_prefill_attn(const dopd_attn_shape* s, const void* q, const voi
   if (nreq == 0) return DOPD_OK;
   if (!q || !k || !v || !out || !cu || !cu_host) return DOPD_ERR_NULL_POINTER;
   if (cu_host[0] != 0) return DOPD_ERR_INVALID_SHAPE;
-  int max_len = 0;
-  int64_t bf16_items = 0;
-  for (int32_t r = 0; r < nreq; ++r) {
-    const int len = cu_host[r + 1] - cu_host[r];
-    if (len < 0) return DOPD_ERR_INVALID_SHAPE;
-    max_len = std::max(max_len, len);
-    bf16_items += (len + dopd::kPfBM - 1) / dopd::kPfBM;
-  }
+  for (int32_t r = 0; r < nreq; ++r)
+    if (cu_host[r + 1] < cu_host[r]) return DOPD_ERR_INVALID_SHAPE;
   const int64_t T = cu_host[nreq];
   if (T == 0) return DOPD_OK;
   const int hq = s->num_q_heads, hkv = s->num_kv_heads, d = s->head_dim;
@@ -164,44 +226,56 @@ dopd_status dopd_prefill_attn(const dopd_attn_shape* s, const void* q, const voi
                          s->softmax_scale);
     return launch_status();
   }
-  dopd::PrefillArgs a;
-  a.q = (const uint16_t*)q;
+  dopd::PrefillArgs a = prefill_args(s, q, out, lse, cu);
   a.k = (const uint16_t*)k;
   a.v = (const uint16_t*)v;
-  a.out = (uint16_t*)out;
-  a.lse = lse;
-  a.cu = cu;
-  a.nreq = nreq;
-  a.hq = hq;
-  a.hkv = hkv;
-  a.max_tiles = (max_len + dopd::kPfBM - 1) / dopd::kPfBM;
-  a.hslots = (hq + dopd::kPfHeadsPerWG - 1) / dopd::kPfHeadsPerWG;
-  a.scale_log2 = s->softmax_scale * dopd::kLog2e;
-  const int64_t items = bf16_items * a.hslots;
-  if (items > INT32_MAX / 2) return DOPD_ERR_INVALID_SHAPE;
-  int64_t blocks = items;
-  a.xcd_order = 0;
-  a.n_items = (int)items;
-  a.tiles_total = (int)bf16_items;
-  a.per_xcd = 0;
-  std::memset(a.ord, 0, sizeof(a.ord));
-  if (nreq <= dopd::kPfMaxOrdered) {
-    // requests by decreasing length (stable), dealt to XCDs in contiguous slices
-    int order[dopd::kPfMaxOrdered];
-    for (int32_t r = 0; r < nreq; ++r) order[r] = r;
-    std::stable_sort(order, order + nreq, [&](int x, int y) {
-      return cu_host[x + 1] - cu_host[x] > cu_host[y + 1] - cu_host[y];
-    });
-    for (int32_t r = 0; r < nreq; ++r) a.ord[r] = (uint8_t)order[r];
-    a.xcd_order = 1;
-    a.per_xcd = (int)((items + dopd::kNumXcd - 1) / dopd::kNumXcd);
-    blocks = (int64_t)a.per_xcd * dopd::kNumXcd;
+  return launch_prefill_bf16<false>(a, d, cu_host, nullptr, nreq, strm);
+}
+
+dopd_status dopd_prefill_paged_attn(const dopd_attn_shape* s, const void* q, const void* k_pool,
+                                    const void* v_pool, int32_t num_pages,
+                                    const int32_t* page_table, int32_t pt_stride,
+                                    const int32_t* cu, const int32_t* cu_host,
+                                    const int32_t* prefix, const int32_t* prefix_host,
+                                    int32_t nreq, void* out, float* lse, void* stream) {
+  dopd_status st = check_shape(s);
+  if (st != DOPD_OK) return st;
+  if (nreq < 0 || num_pages < 0 || pt_stride < 0) return DOPD_ERR_INVALID_SHAPE;
+  if (nreq == 0) return DOPD_OK;
+  if (!q || !k_pool || !v_pool || !page_table || !cu || !cu_host || !prefix || !prefix_host ||
+      !out)
+    return DOPD_ERR_NULL_POINTER;
+  if (cu_host[0] != 0) return DOPD_ERR_INVALID_SHAPE;
+  for (int32_t r = 0; r < nreq; ++r) {
+    const int64_t n = (int64_t)cu_host[r + 1] - cu_host[r];
+    if (n < 0 || prefix_host[r] < 0) return DOPD_ERR_INVALID_SHAPE;
+    // every page the request's keys touch must have a page-table column
+    if (n > 0 && (prefix_host[r] + n + dopd::kPage - 1) / dopd::kPage > pt_stride)
+      return DOPD_ERR_INVALID_SHAPE;
   }
-  if (d == 64)
-    hipLaunchKernelGGL(dopd::prefill_bf16_kernel<64>, dim3((unsigned)blocks), dim3(dopd::kPfThreads), 0, strm, a);
-  else
-    hipLaunchKernelGGL(dopd::prefill_bf16_kernel<128>, dim3((unsigned)blocks), dim3(dopd::kPfThreads), 0, strm, a);
-  return launch_status();
+  const int64_t T = cu_host[nreq];
+  if (T == 0) return DOPD_OK;
+  const int hq = s->num_q_heads, hkv = s->num_kv_heads, d = s->head_dim;
+  hipStream_t strm = as_stream(stream);
+  if (s->dtype == DOPD_FP32) {
+    dim3 grid((unsigned)T, (unsigned)hq);
+    if (d == 64)
+      hipLaunchKernelGGL(dopd::prefill_paged_f32_kernel<64>, grid, dim3(64), 0, strm,
+                         (const float*)q, (const float*)k_pool, (const float*)v_pool, page_table,
+                         pt_stride, cu, prefix, nreq, hq, hkv, s->softmax_scale, (float*)out, lse);
+    else
+      hipLaunchKernelGGL(dopd::prefill_paged_f32_kernel<128>, grid, dim3(64), 0, strm,
+                         (const float*)q, (const float*)k_pool, (const float*)v_pool, page_table,
+                         pt_stride, cu, prefix, nreq, hq, hkv, s->softmax_scale, (float*)out, lse);
+    return launch_status();
+  }
+  dopd::PrefillArgs a = prefill_args(s, q, out, lse, cu);
+  a.k_pool = (const uint16_t*)k_pool;
+  a.v_pool = (const uint16_t*)v_pool;
+  a.page_table = page_table;
+  a.prefix = prefix;
+  a.pt_stride = pt_stride;
+  return launch_prefill_bf16<true>(a, d, cu_host, prefix_host, nreq, strm);
 }
 
 // ---------------------------------------------------------------- kv write

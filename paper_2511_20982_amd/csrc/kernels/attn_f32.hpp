@@ -95,4 +95,39 @@ __global__ __launch_bounds__(64) void decode_f32_kernel(
   if (lse && lane == 0) lse[(int64_t)r * hq + h] = ls;
 }
 
+// Chunk prefill over the paged cache, fp32: chunk token i of request r (query
+// row cu[r] + i) attends to cached positions 0 .. prefix[r] + i.  Grid: (T, Hq).
+template <int D>
+__global__ __launch_bounds__(64) void prefill_paged_f32_kernel(
+    const float* __restrict__ q, const float* __restrict__ k_pool,
+    const float* __restrict__ v_pool, const int32_t* __restrict__ page_table, int pt_stride,
+    const int32_t* __restrict__ cu, const int32_t* __restrict__ prefix, int nreq, int hq,
+    int hkv, float scale, float* __restrict__ out, float* __restrict__ lse) {
+  const int t = blockIdx.x, h = blockIdx.y, lane = lane_id();
+  int lo = 0, hi = nreq;  // request r with cu[r] <= t < cu[r+1]
+  while (hi - lo > 1) {
+    const int mid = (lo + hi) / 2;
+    if (cu[mid] <= t) lo = mid; else hi = mid;
+  }
+  const int r = lo;
+  const int n = prefix[r] + (t - cu[r]) + 1;
+  const int c = h / (hq / hkv);
+  const int32_t* pt = page_table + (int64_t)r * pt_stride;
+  float qv[D / 64], o[D / 64], ls;
+#pragma unroll
+  for (int x = 0; x < D / 64; ++x) qv[x] = q[((int64_t)t * hq + h) * D + lane + 64 * x];
+  auto key = [&](int j, int x) {
+    const int64_t page = pt[j / kPage];
+    return k_pool[((page * hkv + c) * kPage + j % kPage) * D + lane + 64 * x];
+  };
+  auto val = [&](int j, int x) {
+    const int64_t page = pt[j / kPage];
+    return v_pool[((page * hkv + c) * D + lane + 64 * x) * kPage + j % kPage];
+  };
+  attend_row_f32<D>(qv, n, scale, key, val, o, ls);
+#pragma unroll
+  for (int x = 0; x < D / 64; ++x) out[((int64_t)t * hq + h) * D + lane + 64 * x] = o[x];
+  if (lse && lane == 0) lse[(int64_t)t * hq + h] = ls;
+}
+
 }  // namespace dopd

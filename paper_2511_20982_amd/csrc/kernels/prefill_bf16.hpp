@@ -28,6 +28,8 @@
 // that read the same K/V run together under one L2; otherwise heaviest q
 // tiles first.
 #pragma once
+#include <type_traits>
+
 #include "common.hpp"
 
 namespace dopd {
@@ -49,6 +51,14 @@ struct PrefillArgs {
   // run together on one XCD and share its L2.
   int xcd_order, n_items, per_xcd, tiles_total;
   uint8_t ord[64];     // requests by decreasing length
+  // Chunk prefill over the paged cache (the paged instantiation only): the
+  // chunk rows of request r are q[cu[r] .. cu[r+1]), its keys are the cached
+  // positions 0 .. prefix[r] + chunk length - 1, read through the page table.
+  const uint16_t* k_pool;     // [P][Hkv][16][D]
+  const uint16_t* v_pool;     // [P][Hkv][D][16]
+  const int32_t* page_table;  // [nreq][pt_stride]
+  const int32_t* prefix;      // [nreq]
+  int pt_stride;
 };
 
 constexpr int kPfMaxOrdered = 64;
@@ -125,7 +135,9 @@ __device__ __forceinline__ bool pf_find_item(const PrefillArgs& a, int b, int& t
                      : pf_find_item_lpt(a, b, tile, req, slot);
 }
 
-template <int D>
+// PAGED = false: fresh prompts, K/V token-major beside Q (dopd_prefill_attn).
+// PAGED = true: chunks attending to the paged cache (dopd_prefill_paged_attn).
+template <int D, bool PAGED>
 __global__ __launch_bounds__(kPfThreads, 2) void prefill_bf16_kernel(PrefillArgs a) {
   constexpr int BM = kPfBM, BN = kPfBN;
   constexpr int KS = D / 16;     // k-steps of the QK MFMA
@@ -151,8 +163,10 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_bf16_kernel(PrefillArgs
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int g = a.hq / a.hkv, kvh = h / g;
     const int seq0 = a.cu[r], L = a.cu[r + 1] - seq0;
+    // Cached tokens before the chunk: query row i sits at key position P + i.
+    const int P = PAGED ? __builtin_amdgcn_readfirstlane(a.prefix[r]) : 0;
     const int q0 = tile * BM;
-    const int kv_end = min(L, q0 + BM);
+    const int kv_end = P + min(L, q0 + BM);   // keys of this item: [0, kv_end)
     const int ntiles = (kv_end + BN - 1) / BN;
     const int row_w = q0 + 32 * w;            // first query row of this wave
     const int myq = row_w + (l & 31);         // this lane's query row
@@ -208,8 +222,42 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_bf16_kernel(PrefillArgs
             rsrc, (__attribute__((address_space(3))) void*)(lds + (4 * u + w) * 512), 16, voff,
             64 * u, 0, 0);
     };
-    auto load_k = [&](int buf, int kv0) { stage(kg, kbuf(buf), kv0, lane_k, k_c); };
-    auto load_v = [&](int buf, int kv0) { stage(vg, vbuf(buf), kv0, lane_v, v_c); };
+    // Paged: wave w loads page kv0/16 + w of the tile (clamped to the last
+    // page that holds keys), K rows in the order pi (bits 2 and 3 of the slot
+    // swapped) so that each lane's P values are 8 consecutive keys per P.V
+    // k-step; V^T page blocks keep their dim-major rows: LDS V tile
+    // [D/32 dim groups][8 key chunks][32 dims][8 keys], wave w filling chunks
+    // 2w, 2w+1 (its page).  Slots past the end of the cache hold anything;
+    // they are masked (scores by select, V operand bits by AND).
+    const int32_t* pt_row = PAGED ? a.page_table + (int64_t)r * a.pt_stride : nullptr;
+    const int last_page = (kv_end - 1) / kPage;
+    const int pk_slot = ((l >> 2) & 3) | ((l >> 3) & 4) | ((l >> 1) & 8);  // pi(16w + l/4) % 16
+    const int lane_pk = pk_slot * (2 * D) + 16 * k_c;
+    const int lane_pv = (l & 31) * (2 * kPage) + 16 * (l >> 5);
+    // Page id of this wave's page of tile jt (a vector load; made uniform by
+    // the caller once it has landed).
+    auto page_of = [&](int jt) { return pt_row[min(jt * (BN / kPage) + w, last_page)]; };
+    // Page ids of the next K and V tile loads, and the id loaded a step ahead.
+    int pid_k = 0, pid_v = 0, pid_ahead = 0;
+    auto stage_page = [&](const uint16_t* pool, uint16_t* lds, int page, int lane_off, int u_stride) {
+      const __amdgpu_buffer_rsrc_t rsrc = __builtin_amdgcn_make_buffer_rsrc(
+          (void*)(pool + ((int64_t)page * a.hkv + kvh) * (kPage * D)), (short)0, 2 * kPage * D,
+          0x00020000);
+#pragma unroll
+      for (int u = 0; u < KQW; ++u)
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(
+            rsrc, (__attribute__((address_space(3))) void*)(lds + (4 * u + w) * 512), 16, lane_off,
+            u_stride * u, 0, 0);
+    };
+    // (Paged: the page comes from pid_k / pid_v, not from kv0.)
+    auto load_k = [&](int buf, int kv0) {
+      if constexpr (PAGED) stage_page(a.k_pool, kbuf(buf), pid_k, lane_pk, 64);
+      else stage(kg, kbuf(buf), kv0, lane_k, k_c);
+    };
+    auto load_v = [&](int buf, int kv0) {
+      if constexpr (PAGED) stage_page(a.v_pool, vbuf(buf), pid_v, lane_pv, 32 * 2 * kPage);
+      else stage(vg, vbuf(buf), kv0, lane_v, v_c);
+    };
 
     // A operand of the QK MFMA: K[32 tt + l%32][16 ks + 8 hi + 0..7] = chunk
     // 2ks + hi of row 32tt + l%32: group ks/2, slot (2(ks%2) + hi) ^ ((l/4)%4).
@@ -229,14 +277,18 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_bf16_kernel(PrefillArgs
     // with dim 32et + 16((l/16)%2) + i of keys base .. base + 3.
     const int vr_base = 128 * hi + 32 * ((l & 15) >> 2) + 16 * ((l >> 4) & 1) + 4 * (l & 3);
     auto vread = [&](int buf, int kk, int et) {
-      typedef short s16x4_t __attribute__((ext_vector_type(4)));
-      typedef __attribute__((address_space(3))) s16x4_t* lds_s16x4;
-      const uint16_t* p = vbuf(buf) + et * (BN * 32) + (16 * kk) * 32 + vr_base;
-      const s16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4)(p));
-      const s16x4_t hi4 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4)(p + 8 * 32));
-      const s16x4_t both[2] = {lo, hi4};
       bf16x8 res;
-      __builtin_memcpy(&res, both, 16);
+      if constexpr (PAGED) {  // keys 16kk + 8hi + 0..7 of dim 32et + l%32: one 16-byte chunk
+        res = *reinterpret_cast<const bf16x8*>(vbuf(buf) + ((et * 8 + 2 * kk + hi) * 32 + (l & 31)) * 8);
+      } else {
+        typedef short s16x4_t __attribute__((ext_vector_type(4)));
+        typedef __attribute__((address_space(3))) s16x4_t* lds_s16x4;
+        const uint16_t* p = vbuf(buf) + et * (BN * 32) + (16 * kk) * 32 + vr_base;
+        const s16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4)(p));
+        const s16x4_t hi4 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4)(p + 8 * 32));
+        const s16x4_t both[2] = {lo, hi4};
+        __builtin_memcpy(&res, both, 16);
+      }
       return res;
     };
 
@@ -254,7 +306,7 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_bf16_kernel(PrefillArgs
     // stays far below overflow while it does not fire).
     constexpr float kSumLazy = 20.f;
     // Last key this lane's row may see (causal and end of request).
-    const int last_key = min(myq, kv_end - 1);
+    const int last_key = min(P + myq, kv_end - 1);
 
     f32x16 sa[2], sb[2];  // S^T of two consecutive key tiles (current / next)
     bf16x8 pb[4];         // P^T of the current tile: B operands of the four P.V k-steps
@@ -326,12 +378,36 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_bf16_kernel(PrefillArgs
       }
       __builtin_amdgcn_sched_group_barrier(kMfma, 4, 0);
     };
-    auto pv = [&](int buf) {  // O^T += V^T P^T of the tile
+    // O^T += V^T P^T of the tile; on the paged path a tile that runs past the
+    // cached keys (kv0 + BN > kv_end) clears the V operand bits of those keys
+    // (their slots may hold anything, and 0 * NaN would not vanish).
+    auto pv = [&](int buf, int kv0, auto may_run_past) {
       bf16x8 va[4][ET];
+      if constexpr (PAGED && decltype(may_run_past)::value) {
+        // live keys among this lane's 8 of k-step kk: kv_end - kv0 - 16kk - 8hi
+        // (a uniform test first: only the tile that holds kv_end needs it)
+        const int nv0 = kv0 + BN > kv_end ? kv_end - kv0 - 8 * hi : BN;
 #pragma unroll
-      for (int kk = 0; kk < 4; ++kk)
+        for (int kk = 0; kk < 4; ++kk) {
+          const int nv = nv0 - 16 * kk;
+          uint32_t keep[4];
 #pragma unroll
-        for (int et = 0; et < ET; ++et) va[kk][et] = vread(buf, kk, et);
+          for (int wd = 0; wd < 4; ++wd)
+            keep[wd] = (2 * wd + 1 < nv) ? 0xffffffffu : (2 * wd < nv ? 0x0000ffffu : 0u);
+#pragma unroll
+          for (int et = 0; et < ET; ++et) {
+            u32x4 x = __builtin_bit_cast(u32x4, vread(buf, kk, et));
+#pragma unroll
+            for (int wd = 0; wd < 4; ++wd) x[wd] &= keep[wd];
+            va[kk][et] = __builtin_bit_cast(bf16x8, x);
+          }
+        }
+      } else {
+#pragma unroll
+        for (int kk = 0; kk < 4; ++kk)
+#pragma unroll
+          for (int et = 0; et < ET; ++et) va[kk][et] = vread(buf, kk, et);
+      }
 #pragma unroll
       for (int kk = 0; kk < 4; ++kk)
 #pragma unroll
@@ -352,12 +428,17 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_bf16_kernel(PrefillArgs
 #pragma unroll
         for (int tt = 0; tt < 2; ++tt) s[tt] *= c_in;
       }
-      const int lim = last_key - kv0 - 4 * hi;  // lane holds keys kv0 + 32tt + 8(x/4) + 4hi + x%4
+      // Element (tt, x) of this lane is key kv0 + off + (4 or 8) hi: the
+      // accumulator row 32tt + 8(x/4) + 4hi + x%4, through pi on the paged path.
+      const int lim = last_key - kv0 - (PAGED ? 8 : 4) * hi;
 #pragma unroll
       for (int tt = 0; tt < 2; ++tt)
 #pragma unroll
-        for (int x = 0; x < 16; ++x)
-          if (32 * tt + 8 * (x >> 2) + (x & 3) > lim) s[tt][x] = -INFINITY;
+        for (int x = 0; x < 16; ++x) {
+          const int off = PAGED ? 32 * tt + 16 * (x >> 3) + 4 * ((x >> 2) & 1) + (x & 3)
+                                : 32 * tt + 8 * (x >> 2) + (x & 3);
+          if (off > lim) s[tt][x] = -INFINITY;
+        }
       const float m_tile = row_max(s);  // finite: every row sees key 0 in the first tile
       if (__ballot(m_tile > m_run + kLazy)) rescale_to(m_tile);  // wave-uniform
       l_run += exponent(s);
@@ -396,22 +477,42 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_bf16_kernel(PrefillArgs
     // one tile ahead of V.  A step j: loads K(j + 2) and V(j + 1) into the
     // free buffers, computes S^T(j + 1) with the softmax of tile j, then
     // O^T += V^T P^T of tile j; one barrier (which also waits for the loads).
-    load_k(0, 0);
-    if (ntiles > 1) load_k(1, BN);
-    load_v(0, 0);
+    if constexpr (PAGED) {
+      const int p0 = __builtin_amdgcn_readfirstlane(page_of(0));
+      const int p1 = __builtin_amdgcn_readfirstlane(page_of(1));
+      pid_k = p0;
+      load_k(0, 0);
+      pid_k = p1;
+      if (ntiles > 1) load_k(1, BN);
+      pid_v = p0;
+      load_v(0, 0);
+      // the first step loads K(2) and V(1); the id of tile 3 is read ahead
+      pid_v = p1;
+      pid_k = __builtin_amdgcn_readfirstlane(page_of(2));
+      pid_ahead = page_of(3);
+    } else {
+      load_k(0, 0);
+      if (ntiles > 1) load_k(1, BN);
+      load_v(0, 0);
+    }
     __syncthreads();
     if (wave_active) qk(0, sa);  // every active row sees key 0
     // The steady-state steps form p against the running max without taking
     // the tile's max, so start it at the first tile's max (tile 0 is
     // unmasked there).
-    if (wave_active && pos_scale && q0 > 0) m_run = row_max(sa);
-
     // Tiles every row of the item sees in full (positive scales only).
-    const int nfull = pos_scale ? q0 / BN : 0;
+    const int nfull = pos_scale ? (P + q0) / BN : 0;
+    if (wave_active && nfull > 0) m_run = row_max(sa);
+
     int j = 0;
     auto prefetch = [&](int jj, auto par) {  // K(jj + 2) -> K buffer par, V(jj + 1) -> V buffer par ^ 1
       if (jj + 2 < ntiles) load_k(par(), (jj + 2) * BN);
       if (jj + 1 < ntiles) load_v(par() ^ 1, (jj + 1) * BN);
+      if constexpr (PAGED) {  // next step: K(jj + 3), V(jj + 2); read the id of tile jj + 4
+        pid_v = pid_k;
+        pid_k = __builtin_amdgcn_readfirstlane(pid_ahead);  // landed at the last barrier
+        pid_ahead = page_of(jj + 4);
+      }
     };
     auto even = [] { return 0; };
     auto odd = [] { return 1; };
@@ -419,7 +520,7 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_bf16_kernel(PrefillArgs
       prefetch(j, par);
       if (wave_active) {
         half_qk(sc, sn, par() ^ 1);
-        pv(par());
+        pv(par(), j * BN, std::false_type{});  // steady-state tiles hold cached keys only
       }
       __syncthreads();
     };
@@ -438,11 +539,11 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_bf16_kernel(PrefillArgs
     // Diagonal and ragged tiles: masked softmax, then S^T of the next tile.
     auto step_tail = [&](auto par) {
       prefetch(j, par);
-      if (wave_active && j * BN <= row_w + 31) {  // some key of tile j visible to this wave
+      if (wave_active && j * BN <= P + row_w + 31) {  // some key of tile j visible to this wave
         softmax_masked(sa, j * BN);
-        pv(par());
+        pv(par(), j * BN, std::true_type{});
       }
-      if (wave_active && j + 1 < ntiles && (j + 1) * BN <= row_w + 31) qk(par() ^ 1, sa);
+      if (wave_active && j + 1 < ntiles && (j + 1) * BN <= P + row_w + 31) qk(par() ^ 1, sa);
       __syncthreads();
     };
     for (; j < ntiles; ++j) {

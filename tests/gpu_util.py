@@ -71,6 +71,24 @@ def gpu_prefill(shape, q, k, v, cu, with_lse=True, stream=None):
     return widen(A.to_host(out)), (lse.cpu().numpy().astype(np.float64) if with_lse else None)
 
 
+def gpu_prefill_paged(shape, q, k_pool, v_pool, page_table, cu, prefix, with_lse=True,
+                      pools_dev=None):
+    if pools_dev is None:
+        pools_dev = (A.to_device(k_pool), A.to_device(v_pool))
+    kp, vp = pools_dev
+    qd = A.to_device(q)
+    out, obuf, margin = guarded(qd.shape, qd.dtype)
+    lse = torch.full((q.shape[0], q.shape[1]), float("nan"), device=DEV) if with_lse else None
+    A.dopd_prefill_paged_attn(shape, qd, kp, vp, kp.shape[0], A.to_device(page_table),
+                              page_table.shape[1], A.to_device(cu), cu,
+                              A.to_device(np.asarray(prefix, np.int32)), prefix, len(cu) - 1,
+                              out, lse)
+    torch.cuda.synchronize()
+    assert canary_intact(obuf, margin, out.numel() * out.element_size()), \
+        "paged prefill wrote out of bounds"
+    return widen(A.to_host(out)), (lse.cpu().numpy().astype(np.float64) if with_lse else None)
+
+
 def gpu_kv_write(shape, k_new, v_new, k_pool, v_pool, page_table, cu_new, start_pos):
     kp, vp = A.to_device(k_pool), A.to_device(v_pool)
     A.dopd_kv_write(shape, A.to_device(k_new), A.to_device(v_new), kp, vp, k_pool.shape[0],

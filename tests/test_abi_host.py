@@ -140,3 +140,24 @@ def test_unpack_host_validation(lib):
         A.DOPD_ERR_INVALID_SHAPE                                               # table too narrow
     assert up(C.byref(s), 1, p, p, p, p, None, 2, p, p, 10, p, 64, None) == A.DOPD_ERR_NULL_POINTER
     assert up(C.byref(s), 1, p, p, p, p, A._hptr(lens), 0, p, p, 10, p, 64, None) == A.DOPD_OK
+
+
+def test_prefill_paged_host_validation(lib):
+    s = _shape()
+    p = C.c_void_p(FAKE)
+    cu = np.array([0, 40, 41], np.int32)
+    pre = np.array([600, 0], np.int32)
+    pp = lib.dopd_prefill_paged_attn
+    H = A._hptr
+    # request 0 needs ceil(640/16) = 40 page-table columns
+    assert pp(C.byref(s), p, p, p, 100, p, 39, p, H(cu), p, H(pre), 2, p, None, None) == \
+        A.DOPD_ERR_INVALID_SHAPE                                               # table too narrow
+    bad_pre = np.array([-1, 0], np.int32)
+    assert pp(C.byref(s), p, p, p, 100, p, 64, p, H(cu), p, H(bad_pre), 2, p, None, None) == \
+        A.DOPD_ERR_INVALID_SHAPE                                               # negative prefix
+    bad_cu = np.array([0, 40, 30], np.int32)
+    assert pp(C.byref(s), p, p, p, 100, p, 64, p, H(bad_cu), p, H(pre), 2, p, None, None) == \
+        A.DOPD_ERR_INVALID_SHAPE                                               # decreasing cu
+    assert pp(C.byref(s), p, p, p, 100, p, 64, p, H(cu), p, None, 2, p, None, None) == \
+        A.DOPD_ERR_NULL_POINTER
+    assert pp(C.byref(s), p, p, p, 100, p, 64, p, H(cu), p, H(pre), 0, p, None, None) == A.DOPD_OK

@@ -1,0 +1,129 @@
+"""GPU: chunk prefill over the paged cache (prefix-aware, chunk aligned to the
+end of the cache) against the fp64 oracle, chunked == one-shot, a chunk of
+one token == a decode step, and page-permutation invariance."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2511_20982_amd import inputs as I
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(autouse=True)
+def _gpu(require_gpu):
+    pass
+
+
+from tests import gpu_util as G  # noqa: E402
+
+
+def paged_case(seed, prefix, chunk, hq, hkv, d, dtype):
+    """Pools holding prefix + chunk tokens of each request (NaN elsewhere,
+    tail slots included), and the chunk rows of Q."""
+    rng = np.random.default_rng(seed)
+    prefix, chunk = np.asarray(prefix, np.int32), np.asarray(chunk, np.int32)
+    total = prefix + chunk
+    pt, num_pages = I.allocate_pages(rng, np.maximum(total, 1))
+    kp, vp = I.empty_pools(num_pages, hkv, d, dtype)
+    _, kf, vf = I.prefill_batch(rng, total, hq, hkv, d, dtype)
+    kp, vp = oracle.kv_write(kf, vf, kp, vp, pt, I.cu_from_lens(total),
+                             np.zeros(len(total), np.int32))
+    q = I.normal(rng, (int(chunk.sum()), hq, d), dtype)
+    return q, kp, vp, pt, I.cu_from_lens(chunk), prefix
+
+
+PREFIX = [0, 1, 15, 16, 17, 63, 64, 65, 200, 777, 0, 40, 129]
+CHUNK = [9, 1, 16, 30, 64, 65, 128, 129, 1, 300, 0, 200, 77]
+
+
+@pytest.mark.parametrize("hq,hkv", [(8, 8), (8, 2), (28, 4), (7, 1)])
+@pytest.mark.parametrize("d", [128, 64])
+def test_prefill_paged_bf16_matches_oracle(hq, hkv, d):
+    q, kp, vp, pt, cu, pre = paged_case(80 + hq + d, PREFIX, CHUNK, hq, hkv, d, "bf16")
+    scale = 1.0 / np.sqrt(d)
+    ref, ref_lse = oracle.prefill_paged(q, kp, vp, pt, cu, pre, scale)
+    out, lse = G.gpu_prefill_paged(G.A.make_shape(hq, hkv, d, "bf16"), q, kp, vp, pt, cu, pre)
+    G.assert_attention_close(out, ref, "bf16", f"paged prefill hq={hq} hkv={hkv} d={d}")
+    assert np.max(np.abs(lse - ref_lse)) < 2e-2
+
+
+@pytest.mark.parametrize("d", [64, 128])
+def test_prefill_paged_fp32_matches_oracle(d):
+    q, kp, vp, pt, cu, pre = paged_case(81, [0, 20, 33], [17, 1, 40], 8, 2, d, "fp32")
+    ref, ref_lse = oracle.prefill_paged(q, kp, vp, pt, cu, pre, 1 / np.sqrt(d))
+    out, lse = G.gpu_prefill_paged(G.A.make_shape(8, 2, d, "fp32"), q, kp, vp, pt, cu, pre)
+    G.assert_attention_close(out, ref, "fp32", "paged prefill fp32")
+    assert np.max(np.abs(lse - ref_lse)) < 1e-5
+
+
+def test_prefill_paged_scale_variants():
+    q, kp, vp, pt, cu, pre = paged_case(82, [70, 5], [90, 33], 4, 2, 64, "bf16")
+    for scale in (0.0, 1.0, -0.2):
+        ref, _ = oracle.prefill_paged(q, kp, vp, pt, cu, pre, scale)
+        out, _ = G.gpu_prefill_paged(G.A.make_shape(4, 2, 64, "bf16", scale), q, kp, vp, pt, cu,
+                                     pre, with_lse=False)
+        G.assert_attention_close(out, ref, "bf16", f"paged scale={scale}")
+
+
+def test_prefill_paged_long_prefix_sampled_rows():
+    q, kp, vp, pt, cu, pre = paged_case(83, [3000, 1], [700, 500], 4, 2, 128, "bf16")
+    out, lse = G.gpu_prefill_paged(G.A.make_shape(4, 2, 128), q, kp, vp, pt, cu, pre)
+    tok = np.concatenate([np.arange(0, 700, 23), [699, 700, 701, 1199]]).astype(np.int32)
+    head = (np.arange(len(tok)) % 4).astype(np.int32)
+    ref, ref_lse = oracle.prefill_paged(q, kp, vp, pt, cu, pre, 1 / np.sqrt(128), tok=tok, head=head)
+    G.assert_attention_close(out[tok, head], ref, "bf16", "long prefix rows")
+    assert np.max(np.abs(lse[tok, head] - ref_lse)) < 2e-2
+
+
+@pytest.mark.parametrize("pieces", [[300], [1, 299], [64, 64, 64, 108], [5, 130, 1, 164]])
+def test_chunked_prefill_equals_one_shot_on_gpu(pieces):
+    """The prompt written and attended chunk by chunk on the GPU (dopd_kv_write
+    at start_pos = cached tokens, then dopd_prefill_paged_attn) agrees with the
+    one-shot dopd_prefill_attn and with the oracle."""
+    rng = np.random.default_rng(84)
+    hq, hkv, d, L = 8, 2, 128, int(sum(pieces))
+    q, k, v = I.prefill_batch(rng, np.array([L]), hq, hkv, d, "bf16")
+    sh = G.A.make_shape(hq, hkv, d)
+    ref, _ = oracle.prefill(q, k, v, I.cu_from_lens([L]), 1 / np.sqrt(d))
+    one_shot, _ = G.gpu_prefill(sh, q, k, v, I.cu_from_lens([L]))
+    pt, num_pages = I.allocate_pages(rng, np.array([L]))
+    kp, vp = I.empty_pools(num_pages, hkv, d, "bf16")
+    kpd, vpd = G.A.to_device(kp), G.A.to_device(vp)
+    done, outs = 0, []
+    for n in pieces:
+        rows = slice(done, done + n)
+        G.A.dopd_kv_write(sh, G.A.to_device(k[rows]), G.A.to_device(v[rows]), kpd, vpd, num_pages,
+                          G.A.to_device(pt), pt.shape[1], G.A.to_device(I.cu_from_lens([n])),
+                          G.A.to_device(np.array([done], np.int32)), 1, n)
+        out, _ = G.gpu_prefill_paged(sh, q[rows], None, None, pt, I.cu_from_lens([n]),
+                                     np.array([done], np.int32), pools_dev=(kpd, vpd))
+        outs.append(out)
+        done += n
+    chunked = np.concatenate(outs)
+    G.assert_attention_close(chunked, ref, "bf16", f"chunked {pieces} vs oracle")
+    G.assert_attention_close(chunked, one_shot, "bf16", f"chunked {pieces} vs one-shot")
+
+
+def test_prefill_paged_chunk_of_one_matches_decode():
+    q, kp, vp, pt, cu, pre = paged_case(85, [30, 0, 17, 2047], [1, 1, 1, 1], 28, 4, 128, "bf16")
+    sh = G.A.make_shape(28, 4, 128)
+    out, lse = G.gpu_prefill_paged(sh, q, kp, vp, pt, cu, pre)
+    dec, dlse = G.gpu_decode(sh, q, kp, vp, pt, (pre + 1).astype(np.int32))
+    ref, ref_lse = oracle.decode(q, kp, vp, pt, pre + 1, 1 / np.sqrt(128))
+    G.assert_attention_close(out, ref, "bf16", "chunk of one vs oracle decode")
+    G.assert_attention_close(out, dec, "bf16", "chunk of one vs GPU decode")
+    assert np.max(np.abs(lse - ref_lse)) < 2e-2
+
+
+def test_prefill_paged_invariant_under_page_permutation():
+    q, kp, vp, pt, cu, pre = paged_case(86, [100, 7], [150, 60], 8, 2, 128, "bf16")
+    sh = G.A.make_shape(8, 2, 128)
+    out1, lse1 = G.gpu_prefill_paged(sh, q, kp, vp, pt, cu, pre)
+    perm = np.random.default_rng(7).permutation(kp.shape[0])
+    kp2, vp2 = np.empty_like(kp), np.empty_like(vp)
+    kp2[perm], vp2[perm] = kp, vp
+    pt2 = np.where(pt >= 0, perm[np.maximum(pt, 0)], -1).astype(np.int32)
+    out2, lse2 = G.gpu_prefill_paged(sh, q, kp2, vp2, pt2, cu, pre)
+    assert np.array_equal(out1, out2) and np.array_equal(lse1, lse2)
