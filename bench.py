@@ -46,7 +46,8 @@ KERNEL_SOURCES = ("paper_2511_20982_amd/csrc/dopd_attn.hip",
 # Kernels behind each timed call (the decode call is a split kernel plus, when
 # some context exceeds one split, a merge kernel).
 CALL_KERNELS = {"decode": ("decode_split_kernel", "decode_merge_kernel"),
-                "prefill": ("prefill_bf16_kernel",), "kv_write": ("kv_write_kernel",),
+                "prefill": ("prefill_bf16_kernel",), "prefill_chunked": ("prefill_bf16_kernel",),
+                "kv_write": ("kv_write_kernel",),
                 "pack": ("kv_pack_kernel",), "unpack": ("kv_unpack_kernel",)}
 
 WORKLOADS = {
@@ -58,6 +59,10 @@ WORKLOADS = {
                 "32/32 heads, d128, bf16", 3),
     "decode_gqa": ("decode, GQA 70B-shaped: B256, 64/8 heads, d128, bf16, ctx 80% U[100,500] + "
                    "20% U[4096,16384]", 4),
+    "chunked": ("chunked prefill over the paged cache: the 16 prompts of the varlen prefill "
+                "workload (lognormal(1500,1.0) [32,8192], 32/32 heads, d128, bf16) in chunks of "
+                "--chunk tokens, calls filled to --budget tokens, each chunk attending to its "
+                "cached prefix", 3),
     "handoff": ("P->D handoff on one GPU: pack 8 prefilled requests x 512 tokens from the P pool, "
                 "unpack into a D pool with another page order; 28/4 heads, d128, bf16, "
                 "--pack-layers layers", 5),
@@ -224,6 +229,9 @@ def main():
     ap.add_argument("--pack-layers", type=int, default=1,
                     help="layers packed per handoff in the mixed step (1 = the configured step)")
     ap.add_argument("--split", type=int, default=0, help="decode split tokens (0 = automatic)")
+    ap.add_argument("--chunk", type=int, default=512, help="chunked workload: tokens per chunk")
+    ap.add_argument("--budget", type=int, default=8192,
+                    help="chunked workload: tokens per call (chunks of several prompts)")
     ap.add_argument("--streams", type=int, default=1, choices=(1, 2),
                     help="mixed step: 2 = decode on its own stream beside prefill/write/pack, "
                          "1 = everything in order on one stream")
@@ -393,6 +401,68 @@ def main():
         work = {"pack": ("GB/s", pack_bytes(w.handoff_lens, L, w.hkv, w.d)),
                 "unpack": ("GB/s", pack_bytes(w.handoff_lens, L, w.hkv, w.d))}
         dominant = "unpack"
+    elif args.workload == "chunked":
+        # All K/V go into the paged cache first (one timed write).  Then the
+        # prompts are prefilled in chunks of C tokens, each attending to its
+        # cached prefix: a call takes the next chunk of the prompts in turn until
+        # it holds `budget` tokens (a chunked-prefill batch), calls back to back.
+        C, B = args.chunk, args.budget
+        lens = w.prefill_lens.astype(np.int64)
+        k, v = A.to_device(w.k), A.to_device(w.v)
+        cu = A.to_device(w.cu_seqlens)
+        kp, vp = A.to_device(w.k_pool), A.to_device(w.v_pool)
+        pt_np = w.page_table
+        stride = pt_np.shape[1]
+        n_pre = len(lens)
+        start = torch.zeros(n_pre, dtype=torch.int32, device=dev)
+        T = int(w.cu_seqlens[-1])
+        q_all = A.to_device(w.q)
+        out_all = torch.empty_like(q_all)
+        pos = np.zeros(n_pre, np.int64)
+        chunks = []
+        while (pos < lens).any():
+            sel = []  # (request, start, n)
+            budget = B
+            for r in np.argsort(-(lens - pos), kind="stable"):
+                if budget <= 0:
+                    break
+                n = int(min(C, lens[r] - pos[r], budget))
+                if n > 0:
+                    sel.append((int(r), int(pos[r]), n))
+                    pos[r] += n
+                    budget -= n
+            n_arr = np.array([x[2] for x in sel], np.int32)
+            pre = np.array([x[1] for x in sel], np.int32)
+            rows = np.concatenate([w.cu_seqlens[r] + s0 + np.arange(n) for r, s0, n in sel])
+            rows_d = torch.from_numpy(rows.astype(np.int64)).to(dev)
+            cu_c = I.cu_from_lens(n_arr)
+            pt_c = np.ascontiguousarray(pt_np[[x[0] for x in sel]])
+            chunks.append(dict(q=q_all.index_select(0, rows_d).contiguous(), rows=rows_d,
+                               out=torch.empty((len(rows), w.hq, w.d), dtype=torch.bfloat16,
+                                               device=dev),
+                               cu=A.to_device(cu_c), cu_h=cu_c, pre=A.to_device(pre), pre_h=pre,
+                               pt=A.to_device(pt_c), n=len(sel)))
+        pt = A.to_device(pt_np)
+        tm = {"prefill_chunked": Timer(torch, sA), "kv_write": Timer(torch, sA)}
+
+        def step():
+            with tm["kv_write"]:
+                A.dopd_kv_write(shape, k, v, kp, vp, w.num_pages, pt, stride, cu, start, n_pre, T,
+                                sA)
+            with tm["prefill_chunked"]:
+                for ch in chunks:
+                    A.dopd_prefill_paged_attn(shape, ch["q"], kp, vp, w.num_pages, ch["pt"],
+                                              stride, ch["cu"], ch["cu_h"], ch["pre"], ch["pre_h"],
+                                              ch["n"], ch["out"], None, sA)
+
+        def gather_out():
+            for ch in chunks:
+                out_all.index_copy_(0, ch["rows"], ch["out"])
+            return out_all
+
+        work = {"prefill_chunked": ("TFLOP/s", prefill_flops(w.prefill_lens, w.hq, w.d)),
+                "kv_write": ("GB/s", write_bytes(w.prefill_lens, w.hkv, w.d))}
+        dominant = "prefill_chunked"
     else:  # prefill + write
         q, k, v = A.to_device(w.q), A.to_device(w.k), A.to_device(w.v)
         cu = A.to_device(w.cu_seqlens)
@@ -498,8 +568,11 @@ def main():
             cpu = {"value": round(flops / dt / 1e12, 6), "unit": "TFLOP/s", "cores": threads,
                    "kind": "oracle", "cpu": cpu_info(), "seconds": round(dt, 2),
                    "sample": f"fp64 oracle prefill of {len(rows_tok)} sampled rows (the last 4 "
-                             f"rows of every prompt, 4 heads each; {flops / 1e9:.2f} GFLOP)"}
-            gotf = I.bf16_bits_to_f32(A.to_host(out_p)[rows_tok, heads]).astype(np.float64)
+                             f"rows of every prompt, 4 heads each; {flops / 1e9:.2f} GFLOP)"
+                             + ("; chunked output checked against the one-shot oracle rows"
+                                if args.workload == "chunked" else "")}
+            out_rows = gather_out() if args.workload == "chunked" else out_p
+            gotf = I.bf16_bits_to_f32(A.to_host(out_rows)[rows_tok, heads]).astype(np.float64)
             parity = {"prefill_max_abs_err": float(np.max(np.abs(gotf - ref))),
                       "prefill_rows": int(len(rows_tok))}
 
@@ -519,7 +592,9 @@ def main():
         "data": "synthetic",
         "config": {"workload": desc, "seed": int(w.seed), "split_tokens": args.split,
                    "streams": args.streams if args.workload == "mixed" else 1,
-                   "pack_layers": args.pack_layers if args.workload in ("mixed", "handoff") else None},
+                   "pack_layers": args.pack_layers if args.workload in ("mixed", "handoff") else None,
+                   "chunk": args.chunk if args.workload == "chunked" else None,
+                   "budget": args.budget if args.workload == "chunked" else None},
         "roofline": roofline,
         "kernels": kern,
         "cpu_baseline": cpu,

@@ -137,16 +137,19 @@ dopd_status dopd_kv_write(const dopd_attn_shape* shape, const void* k_new, const
  *   q/out [num_reqs][Hq][d]; lse (nullable) fp32 [num_reqs][Hq].
  *   context_lens_host: identical host copy (>= 1 each), used to size the
  *     launch and the key-range split.
- *   split_tokens: keys per split-K work item, 0 = automatic, else a positive
- *     multiple of 32, at most 4096.  The result does not depend on it beyond
- *     rounding.
+ *   split_tokens: size of the key range each workgroup takes, 0 = automatic
+ *     (one equal share per resident workgroup), else a positive multiple of
+ *     32, at most 4096 (in tokens; a range may span several requests).  The
+ *     result does not depend on it beyond rounding.
  *   workspace: device memory of at least dopd_decode_workspace_size() bytes
  *     for the same arguments, 256-byte aligned, any contents; it holds the
  *     split-K partials.  Calls that overlap in time must not share it.
- * bf16 path: work items (request, KV head, key split) read each page once for
- * all Hq/Hkv query heads of the group (at most 16); requests whose context
- * exceeds one split are finished by a second kernel that merges the split
- * partials exactly (log-sum-exp rescaling), on the same stream.
+ * bf16 path: the keys of all (request, KV head) pairs are cut into equal
+ * shares, one per workgroup, so that long and short contexts balance; each
+ * page is read once for all Hq/Hkv query heads of the group (at most 16); a
+ * (request, KV head) whose keys fall in several shares is finished by a
+ * second kernel that merges the partials exactly (log-sum-exp rescaling), on
+ * the same stream.
  */
 dopd_status dopd_decode_attn(const dopd_attn_shape* shape, const void* q, const void* k_pool,
                              const void* v_pool, int32_t num_pages, const int32_t* page_table,

@@ -45,23 +45,29 @@ dopd_status check_shape(const dopd_attn_shape* s) {
 
 // ---- decode planning --------------------------------------------------------
 constexpr int kMaxGroupBf16 = 16;   // query heads per KV head handled by one decode wave
-constexpr int kAutoSplitMax = 2048;
-constexpr int kAutoSplitMin = 128;
-// Four-wave work items, two resident per CU: 512 slots on 256 CUs; aim for
-// about four rounds so that the ragged items dispatched last fill the tail.
-constexpr int64_t kTargetItems = 2048;
+// Resident four-wave decode workgroups: two per CU on 256 CUs.  The automatic
+// partition gives each of them one equal slice of the pairs (one round).
+constexpr int64_t kDecSlots = 512;
+constexpr int32_t kDecMaxSplitTokens = 4096;  // largest explicit split_tokens
+constexpr int64_t kDecMinPairsPerWg = 4;  // one pair per wave at least
 
-int64_t decode_items(const int32_t* ctx, int32_t n, int split, int hkv) {
-  int64_t items = 0;
-  for (int32_t r = 0; r < n; ++r) items += (int64_t)((ctx[r] + split - 1) / split) * hkv;
-  return items;
+// Work units of the partition: per (r, c), a segment start cost plus its pairs.
+int64_t decode_total_units(const int32_t* ctx, int32_t n, int hkv) {
+  int64_t units = 0;
+  for (int32_t r = 0; r < n; ++r) units += (int64_t)(dopd::kDecSegCost + (ctx[r] + 31) / 32) * hkv;
+  return units;
 }
 
-int choose_split(const int32_t* ctx, int32_t n, int hkv, int32_t requested) {
-  if (requested > 0) return requested;
-  int split = kAutoSplitMax;
-  while (split > kAutoSplitMin && decode_items(ctx, n, split, hkv) < kTargetItems) split /= 2;
-  return split;
+// Workgroups of the partition: split_tokens / 32 units each when given, else
+// one slice per resident slot.
+int64_t decode_nwg(int64_t total_units, int32_t split_tokens) {
+  if (total_units <= 0) return 0;
+  if (split_tokens > 0) {
+    const int64_t per = split_tokens / 32;
+    return (total_units + per - 1) / per;
+  }
+  return std::max<int64_t>(1, std::min(kDecSlots, (total_units + kDecMinPairsPerWg - 1) /
+                                                      kDecMinPairsPerWg));
 }
 
 struct DecodeLayout {
@@ -70,14 +76,39 @@ struct DecodeLayout {
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
-DecodeLayout decode_layout(const dopd_attn_shape* s, const int32_t* ctx, int32_t n, int split) {
+// Partial slots: at most one per (workgroup, (r, c)) boundary, indexed
+// workgroup + (r * Hkv + c).
+DecodeLayout decode_layout(const dopd_attn_shape* s, const int32_t* ctx, int32_t n,
+                           int32_t split_tokens) {
   DecodeLayout L{};
   const int g = s->num_q_heads / s->num_kv_heads;
-  const int64_t slots = decode_items(ctx, n, split, s->num_kv_heads);
+  const int64_t nwg = decode_nwg(decode_total_units(ctx, n, s->num_kv_heads), split_tokens);
+  const int64_t slots = nwg + (int64_t)n * s->num_kv_heads;
   L.part_o_off = 0;
   L.part_ml_off = align256((size_t)slots * g * s->head_dim * sizeof(float));
   L.total = L.part_ml_off + align256((size_t)slots * g * 2 * sizeof(float));
   return L;
+}
+
+// Same slice arithmetic as the kernels: does any (r, c) span two slices?
+bool decode_needs_merge(const int32_t* ctx, int32_t n, int hkv, int64_t total, int64_t nwg) {
+  auto begin = [&](int64_t b) { return b * total / nwg; };
+  auto slice_of = [&](int64_t x) {
+    int64_t b = x * nwg / total;
+    while (b + 1 < nwg && begin(b + 1) <= x) ++b;
+    while (b > 0 && begin(b) > x) --b;
+    return b;
+  };
+  int64_t base = 0;
+  for (int32_t r = 0; r < n; ++r) {
+    const int64_t np = (ctx[r] + 31) / 32, span = dopd::kDecSegCost + np;
+    for (int c = 0; c < hkv; ++c) {
+      const int64_t first = base + c * span + dopd::kDecSegCost;  // unit of the first pair
+      if (slice_of(first) != slice_of(first + np - 1)) return true;
+    }
+    base += span * hkv;
+  }
+  return false;
 }
 
 dopd_status check_decode_host(const dopd_attn_shape* s, const int32_t* ctx_host, int32_t n,
@@ -88,7 +119,7 @@ dopd_status check_decode_host(const dopd_attn_shape* s, const int32_t* ctx_host,
   if (n > 0 && !ctx_host) return DOPD_ERR_NULL_POINTER;
   for (int32_t r = 0; r < n; ++r)
     if (ctx_host[r] < 1) return DOPD_ERR_INVALID_SHAPE;
-  if (split < 0 || (split > 0 && split % 32 != 0) || split > dopd::kDecMaxSplit)
+  if (split < 0 || (split > 0 && split % 32 != 0) || split > kDecMaxSplitTokens)
     return DOPD_ERR_INVALID_SHAPE;
   if (s->dtype == DOPD_BF16 && s->num_q_heads / s->num_kv_heads > kMaxGroupBf16)
     return DOPD_ERR_UNSUPPORTED;
@@ -322,8 +353,7 @@ size_t dopd_decode_workspace_size(const dopd_attn_shape* s, const int32_t* ctx_h
                                   int32_t split_tokens) {
   if (check_decode_host(s, ctx_host, n, split_tokens) != DOPD_OK) return 0;
   if (n == 0 || s->dtype != DOPD_BF16) return 256;
-  const int split = choose_split(ctx_host, n, s->num_kv_heads, split_tokens);
-  return decode_layout(s, ctx_host, n, split).total;
+  return decode_layout(s, ctx_host, n, split_tokens).total;
 }
 
 dopd_status dopd_decode_attn(const dopd_attn_shape* s, const void* q, const void* k_pool,
@@ -353,18 +383,15 @@ dopd_status dopd_decode_attn(const dopd_attn_shape* s, const void* q, const void
                          s->softmax_scale, (float*)out, lse);
     return launch_status();
   }
-  const int split = choose_split(ctx_host, nreq, hkv, split_tokens);
-  const DecodeLayout L = decode_layout(s, ctx_host, nreq, split);
+  const int64_t total = decode_total_units(ctx_host, nreq, hkv);
+  if (total > INT32_MAX / 2) return DOPD_ERR_INVALID_SHAPE;
+  const int64_t nwg = decode_nwg(total, split_tokens);
+  const DecodeLayout L = decode_layout(s, ctx_host, nreq, split_tokens);
   if (!workspace) return DOPD_ERR_NULL_POINTER;
   if (workspace_bytes < L.total) return DOPD_ERR_WORKSPACE_TOO_SMALL;
   if ((reinterpret_cast<uintptr_t>(workspace) & 255) != 0) return DOPD_ERR_INVALID_SHAPE;
-  const int64_t items = decode_items(ctx_host, nreq, split, hkv);
-  if (items > INT32_MAX) return DOPD_ERR_INVALID_SHAPE;
-  int64_t full_items = 0;
-  for (int32_t r = 0; r < nreq; ++r) full_items += (int64_t)(ctx_host[r] / split) * hkv;
   char* ws = static_cast<char*>(workspace);
-  int64_t merge_items = 0;
-  for (int32_t r = 0; r < nreq; ++r) merge_items += ctx_host[r] > split ? hkv : 0;
+  const bool merge = decode_needs_merge(ctx_host, nreq, hkv, total, nwg);
   dopd::DecodeArgs a;
   a.q = (const uint16_t*)q;
   a.k_pool = (const uint16_t*)k_pool;
@@ -379,9 +406,11 @@ dopd_status dopd_decode_attn(const dopd_attn_shape* s, const void* q, const void
   a.nreq = nreq;
   a.hq = hq;
   a.hkv = hkv;
-  a.split = split;
-  a.full_items = (int)full_items;
+  a.total_units = (int)total;
+  a.nwg = (int)nwg;
   a.scale_log2 = s->softmax_scale * dopd::kLog2e;
+  const int64_t items = nwg;
+  const int64_t merge_items = merge ? (int64_t)nreq * hkv : 0;
   if (d == 64)
     hipLaunchKernelGGL(dopd::decode_split_kernel<64>, dim3((unsigned)items), dim3(256), 0, strm, a);
   else

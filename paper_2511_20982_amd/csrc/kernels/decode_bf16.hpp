@@ -1,9 +1,17 @@
 // Paged single-query decode attention, bf16 in / fp32 accumulate, gfx950.
 //
-// Work item = one workgroup of 4 waves = (request r, KV head c, key split s).
-// The split's pages are taken two at a time (32 tokens, a "pair"); wave w
-// handles pairs w, w+4, w+8, ...  For the g = Hq/Hkv query heads of the group
-// (padded to 16 MFMA columns) each wave computes per pair
+// The key range of every (request r, KV head c) is cut into pairs of pages
+// (32 tokens).  Each (r, c) is a span of kDecSegCost + (its pairs) work units
+// (the first kDecSegCost units stand for the fixed cost of starting a
+// segment: loading q, the page ids and the first pair), and the spans of all
+// (r, c), taken r-major then c, form one sequence.  Workgroup b (4 waves)
+// takes the contiguous slice [b * total / nwg, (b + 1) * total / nwg) of it,
+// so every workgroup gets the same amount of work whatever the context
+// lengths (one round over the machine when nwg is the number of resident
+// slots).  A slice crosses (r, c) boundaries: the pairs of one (r, c) inside
+// it are a segment.  Within a segment the waves take its pairs round-robin; for the
+// g = Hq/Hkv query heads of the group (padded to 16 MFMA columns) a wave
+// computes per pair
 //
 //   S^T[32 tok][16 heads] = K[32 tok][d] . Q^T[d][16]      (v_mfma_f32_16x16x32_bf16)
 //   O^T[d][16 heads]     += V^T[d][32 tok] . P^T[32][16]   (v_mfma_f32_16x16x32_bf16)
@@ -18,18 +26,17 @@
 // registers: the loads of the next pair are in flight while the current pair
 // is computed.
 //
-// The four waves' (m, l, O) are merged through LDS.  A request with one split
-// writes its output directly; otherwise each split writes an un-normalised
-// partial to the workspace and a second, small kernel merges the partials of
-// every (r, c) in split order:
+// The four waves' (m, l, O) are merged through LDS.  A segment that is the
+// whole (r, c) writes the output directly; otherwise it writes an
+// un-normalised partial to slot b + (r * Hkv + c) of the workspace (distinct
+// for distinct segments, since along the sequence b and the (r, c) index both
+// only grow), and a second, small kernel merges the partials of every (r, c)
+// in slice order:
 //   M = max_s m_s,  L = sum_s 2^(m_s-M) l_s,  o = sum_s 2^(m_s-M) o~_s / L.
 // That merge is exact in real arithmetic, so the result does not depend on the
-// split size beyond rounding.  The kernel boundary orders the partial writes
+// partition beyond rounding.  The kernel boundary orders the partial writes
 // before the merge reads; no in-kernel fence or counter is needed (a
 // device-scope fence costs a whole-L2 writeback and invalidate on this part).
-//
-// Dispatch order: all full-size splits first, then every request's ragged
-// last split, so the short work items fill the tail of the launch.
 #pragma once
 #include "common.hpp"
 
@@ -45,13 +52,28 @@ struct DecodeArgs {
   float* lse;                 // [B][Hq] or null
   float* part_o;              // [slots][g][D]
   float* part_ml;             // [slots][g][2]
-  int pt_stride, nreq, hq, hkv, split;
-  int full_items;             // number of full-size split items (dispatched first)
+  int pt_stride, nreq, hq, hkv;
+  int total_units;            // sum_r (kDecSegCost + ceil(ctx_r / 32)) * Hkv
+  int nwg;                    // workgroups of the partition
   float scale_log2;           // softmax_scale * log2(e)
 };
 
 constexpr int kDecWaves = 4;
-constexpr int kDecMaxSplit = 4096;  // keys per work item: 128 pairs, 32 per wave
+constexpr int kDecChunkPairs = 32 * kDecWaves;  // pairs whose page ids one wave holds at once
+constexpr int kDecSegCost = 8;                   // work units of a segment start, in pairs
+
+// First work unit of workgroup b's slice.
+__device__ __forceinline__ int dec_slice_begin(const DecodeArgs& a, int b) {
+  return (int)((int64_t)b * a.total_units / a.nwg);
+}
+
+// The workgroup whose slice holds work unit x.
+__device__ __forceinline__ int dec_slice_of(const DecodeArgs& a, int x) {
+  int b = (int)((int64_t)x * a.nwg / a.total_units);
+  while (b + 1 < a.nwg && dec_slice_begin(a, b + 1) <= x) ++b;
+  while (b > 0 && dec_slice_begin(a, b) > x) --b;
+  return b;
+}
 
 template <int D>
 struct DecodePairBuf {
@@ -68,277 +90,275 @@ __global__ __launch_bounds__(256, 2) void decode_split_kernel(DecodeArgs a) {
   __shared__ f32x4 s_o[kDecWaves - 1][NT][64];
 
   const int tid = threadIdx.x, l = lane_id(), w = tid >> 6;
-  const int hq = a.hq, hkv = a.hkv, g = hq / hkv, split = a.split;
+  const int hq = a.hq, hkv = a.hkv, g = hq / hkv;
+  const int b = blockIdx.x;
+  const int lo = dec_slice_begin(a, b), hi_unit = dec_slice_begin(a, b + 1);
+  if (lo >= hi_unit) return;  // uniform
 
-  // ---- work item: full splits first, then ragged last splits
-  int r, local, s;
+  // (r, unit offset inside r's (c, unit) sequence) of the first unit
+  int r, local;
   {
-    const int b = blockIdx.x;
-    if (b < a.full_items) {
-      auto cnt = [&](int rr) { return (a.ctx_lens[rr] / split) * hkv; };
-      if (!find_owner(b, a.nreq, cnt, r, local)) return;
-      s = local / hkv;
-    } else {
-      auto cnt = [&](int rr) { return (a.ctx_lens[rr] % split) ? hkv : 0; };
-      if (!find_owner(b - a.full_items, a.nreq, cnt, r, local)) return;
-      s = a.ctx_lens[r] / split;
-    }
+    auto cnt = [&](int rr) { return (kDecSegCost + (a.ctx_lens[rr] + 31) / 32) * hkv; };
+    if (!find_owner(lo, a.nreq, cnt, r, local)) return;
   }
-  const int c = local % hkv;
-  const int ctx = a.ctx_lens[r];
-  const int nsplit = (ctx + split - 1) / split;
-  const int t_begin = s * split;
-  const int ntok = min(split, ctx - t_begin);
-  const int npairs = (ntok + 31) / 32;
-  const int my_pairs = npairs > w ? (npairs - w + kDecWaves - 1) / kDecWaves : 0;
 
   const int hl = l & 15;  // head within the group (MFMA column)
   const int qg = l >> 4;  // lane group 0..3 (MFMA k-slot group)
-
-  // Q^T operand: lane holds q[r][c*g+hl][SPAN*qg + 8i + j].
-  bf16x8 qop[NQK];
-  {
-    const bool ok = hl < g;
-    const uint16_t* qp = a.q + ((int64_t)r * hq + c * g + (ok ? hl : 0)) * D + SPAN * qg;
-#pragma unroll
-    for (int i = 0; i < NQK; ++i) {
-      u32x4 x = *reinterpret_cast<const u32x4*>(qp + 8 * i);
-      if (!ok) x = u32x4{0, 0, 0, 0};
-      qop[i] = __builtin_bit_cast(bf16x8, x);
-    }
-  }
-
-  // Page ids of this wave's pairs: lane j holds page (j & 1) of its pair j/2.
-  const int32_t* pt = a.page_table + (int64_t)r * a.pt_stride + t_begin / kPage;
-  const int npages = (ntok + kPage - 1) / kPage;
-  int pid = 0;
-  {
-    const int pg = 2 * (w + kDecWaves * (l >> 1)) + (l & 1);
-    if (pg < npages) pid = pt[pg];
-  }
-
-  f32x4 oacc[NT];
-#pragma unroll
-  for (int n = 0; n < NT; ++n) oacc[n] = f32x4{0.f, 0.f, 0.f, 0.f};
-  float m_run = -INFINITY, l_run = 0.f;
-
   const int mrow = l & 15;
   const int tq1 = 8 * (mrow >> 2) + (mrow & 3);  // MFMA #1 rows hold pair tokens 0-3, 8-11, 16-19, 24-27
   const int tq2 = tq1 + 4;                       // MFMA #2 rows hold 4-7, 12-15, 20-23, 28-31
   const int64_t page_elems = (int64_t)hkv * kPage * D;
-  const uint16_t* kbase = a.k_pool + (int64_t)c * kPage * D + SPAN * qg;
-  const uint16_t* vbase = a.v_pool + (int64_t)c * D * kPage + (int64_t)hl * kPage + 8 * (qg & 1);
 
-  auto load_pair = [&](DecodePairBuf<D>& buf, int k) {
-    const int pair = w + kDecWaves * k;
-    const int pageA = __shfl(pid, 2 * k, 64);
-    const int pageB = __shfl(pid, 2 * k + 1, 64);
-    const int valid = min(32, ntok - 32 * pair);
-    // dead tokens read slot 0 of page A (always live) and are masked later
-    const int64_t a1 = tq1 < valid ? (int64_t)(tq1 < kPage ? pageA : pageB) * page_elems + (tq1 & 15) * D
-                                   : (int64_t)pageA * page_elems;
-    const int64_t a2 = tq2 < valid ? (int64_t)(tq2 < kPage ? pageA : pageB) * page_elems + (tq2 & 15) * D
-                                   : (int64_t)pageA * page_elems;
-#pragma unroll
-    for (int i = 0; i < NQK; ++i) {
-      buf.k1[i] = *reinterpret_cast<const u32x4*>(kbase + a1 + 8 * i);
-      buf.k2[i] = *reinterpret_cast<const u32x4*>(kbase + a2 + 8 * i);
+  int pos = lo;
+  while (pos < hi_unit) {  // one (r, c) span per iteration (uniform)
+    const int ctx = a.ctx_lens[r];
+    const int np = (ctx + 31) / 32;                 // pairs of one (r, c)
+    const int span = kDecSegCost + np;              // its work units
+    const int c = local / span, u0 = local % span;
+    const int u1 = min(span, u0 + (hi_unit - pos));
+    const int p0 = max(0, u0 - kDecSegCost), p1 = max(0, u1 - kDecSegCost);  // pairs [p0, p1)
+    pos += u1 - u0;
+    local += u1 - u0;
+    const int rr = r;
+    if (local == span * hkv) {
+      ++r;
+      local = 0;
     }
-    const int pv = (qg < 2 || valid <= kPage) ? pageA : pageB;
-    const uint16_t* p = vbase + (int64_t)pv * page_elems;
-#pragma unroll
-    for (int n = 0; n < NT; ++n) buf.v[n] = *reinterpret_cast<const u32x4*>(p + (int64_t)(16 * n) * kPage);
-  };
+    if (p0 == p1) continue;  // only start-cost units of this (r, c) fall in the slice
+    const int r = rr;  // the segment's request (the loop variable has moved on)
 
-  auto compute_pair = [&](DecodePairBuf<D>& buf, int k) {
-    const int pair = w + kDecWaves * k;
-    const int valid = min(32, ntok - 32 * pair);
-    f32x4 s1 = {0.f, 0.f, 0.f, 0.f}, s2 = {0.f, 0.f, 0.f, 0.f};
+    // Q^T operand: lane holds q[r][c*g+hl][SPAN*qg + 8i + j].
+    bf16x8 qop[NQK];
+    {
+      const bool ok = hl < g;
+      const uint16_t* qp = a.q + ((int64_t)r * hq + c * g + (ok ? hl : 0)) * D + SPAN * qg;
 #pragma unroll
-    for (int i = 0; i < NQK; ++i) {
-      s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, buf.k1[i]), qop[i], s1, 0, 0, 0);
-      s2 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, buf.k2[i]), qop[i], s2, 0, 0, 0);
+      for (int i = 0; i < NQK; ++i) {
+        u32x4 x = *reinterpret_cast<const u32x4*>(qp + 8 * i);
+        if (!ok) x = u32x4{0, 0, 0, 0};
+        qop[i] = __builtin_bit_cast(bf16x8, x);
+      }
     }
-    // lane holds head hl, pair tokens 8qg + 0..3 (s1) and 8qg + 4..7 (s2)
-    float x[8];
+
+    f32x4 oacc[NT];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      x[j] = s1[j] * a.scale_log2;
-      x[4 + j] = s2[j] * a.scale_log2;
-    }
-    if (valid < 32) {  // last pair of a ragged split: mask dead tokens, zero dead V slots
-#pragma unroll
-      for (int j = 0; j < 8; ++j)
-        if (8 * qg + j >= valid) x[j] = -INFINITY;
-      const int nv = valid - 8 * qg;  // live slots among this lane's 8
-#pragma unroll
-      for (int n = 0; n < NT; ++n)
-#pragma unroll
-        for (int wd = 0; wd < 4; ++wd) {
-          const uint32_t keep = (2 * wd + 1 < nv) ? 0xffffffffu : (2 * wd < nv ? 0x0000ffffu : 0u);
-          buf.v[n][wd] &= keep;
+    for (int n = 0; n < NT; ++n) oacc[n] = f32x4{0.f, 0.f, 0.f, 0.f};
+    float m_run = -INFINITY, l_run = 0.f;
+
+    const uint16_t* kbase = a.k_pool + (int64_t)c * kPage * D + SPAN * qg;
+    const uint16_t* vbase = a.v_pool + (int64_t)c * D * kPage + (int64_t)hl * kPage + 8 * (qg & 1);
+
+    // Chunks of up to 128 pairs: lane j of a wave holds the page id of page
+    // (j & 1) of the wave's pair j/2 of the chunk.
+    for (int cb = p0; cb < p1; cb += kDecChunkPairs) {
+      const int t_begin = 32 * cb;
+      const int ntok = min(32 * min(p1 - cb, kDecChunkPairs), ctx - t_begin);
+      const int npairs = (ntok + 31) / 32;
+      const int my_pairs = npairs > w ? (npairs - w + kDecWaves - 1) / kDecWaves : 0;
+      const int32_t* pt = a.page_table + (int64_t)r * a.pt_stride + t_begin / kPage;
+      const int npages = (ntok + kPage - 1) / kPage;
+      int pid = 0;
+      {
+        const int pg = 2 * (w + kDecWaves * (l >> 1)) + (l & 1);
+        if (pg < npages) pid = pt[pg];
+      }
+
+    auto load_pair = [&](DecodePairBuf<D>& buf, int k) {
+      const int pair = w + kDecWaves * k;
+      const int pageA = __shfl(pid, 2 * k, 64);
+      const int pageB = __shfl(pid, 2 * k + 1, 64);
+      const int valid = min(32, ntok - 32 * pair);
+      // dead tokens read slot 0 of page A (always live) and are masked later
+      const int64_t a1 = tq1 < valid ? (int64_t)(tq1 < kPage ? pageA : pageB) * page_elems + (tq1 & 15) * D
+                                     : (int64_t)pageA * page_elems;
+      const int64_t a2 = tq2 < valid ? (int64_t)(tq2 < kPage ? pageA : pageB) * page_elems + (tq2 & 15) * D
+                                     : (int64_t)pageA * page_elems;
+  #pragma unroll
+      for (int i = 0; i < NQK; ++i) {
+        buf.k1[i] = *reinterpret_cast<const u32x4*>(kbase + a1 + 8 * i);
+        buf.k2[i] = *reinterpret_cast<const u32x4*>(kbase + a2 + 8 * i);
+      }
+      const int pv = (qg < 2 || valid <= kPage) ? pageA : pageB;
+      const uint16_t* p = vbase + (int64_t)pv * page_elems;
+  #pragma unroll
+      for (int n = 0; n < NT; ++n) buf.v[n] = *reinterpret_cast<const u32x4*>(p + (int64_t)(16 * n) * kPage);
+    };
+
+    auto compute_pair = [&](DecodePairBuf<D>& buf, int k) {
+      const int pair = w + kDecWaves * k;
+      const int valid = min(32, ntok - 32 * pair);
+      f32x4 s1 = {0.f, 0.f, 0.f, 0.f}, s2 = {0.f, 0.f, 0.f, 0.f};
+  #pragma unroll
+      for (int i = 0; i < NQK; ++i) {
+        s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, buf.k1[i]), qop[i], s1, 0, 0, 0);
+        s2 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, buf.k2[i]), qop[i], s2, 0, 0, 0);
+      }
+      // lane holds head hl, pair tokens 8qg + 0..3 (s1) and 8qg + 4..7 (s2)
+      float x[8];
+  #pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        x[j] = s1[j] * a.scale_log2;
+        x[4 + j] = s2[j] * a.scale_log2;
+      }
+      if (valid < 32) {  // last pair of a ragged split: mask dead tokens, zero dead V slots
+  #pragma unroll
+        for (int j = 0; j < 8; ++j)
+          if (8 * qg + j >= valid) x[j] = -INFINITY;
+        const int nv = valid - 8 * qg;  // live slots among this lane's 8
+  #pragma unroll
+        for (int n = 0; n < NT; ++n)
+  #pragma unroll
+          for (int wd = 0; wd < 4; ++wd) {
+            const uint32_t keep = (2 * wd + 1 < nv) ? 0xffffffffu : (2 * wd < nv ? 0x0000ffffu : 0u);
+            buf.v[n][wd] &= keep;
+          }
+      }
+      float mx = fmaxf(fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3])),
+                       fmaxf(fmaxf(x[4], x[5]), fmaxf(x[6], x[7])));
+      mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+      const float m_new = fmaxf(m_run, mx);  // finite: a pair's first token is live
+      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+      float psum = 0.f;
+      bf16x8 pb;
+  #pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const float p = __builtin_amdgcn_exp2f(x[j] - m_new);
+        psum += p;
+        pb[j] = (__bf16)p;
+      }
+      l_run = l_run * alpha + psum;
+      m_run = m_new;
+  #pragma unroll
+      for (int n = 0; n < NT; ++n) {
+        oacc[n] *= alpha;
+        oacc[n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, buf.v[n]), pb, oacc[n], 0, 0, 0);
+      }
+    };
+
+      if (my_pairs > 0) {
+        // Prefetch loads are issued unconditionally (past the end they re-read
+        // the last pair, an L2 hit) so the compiler can wait for exactly the
+        // buffer being computed while the other one is in flight.
+        const int last = my_pairs - 1;
+        DecodePairBuf<D> b0, b1;
+        load_pair(b0, 0);
+        for (int k = 0; k < my_pairs; k += 2) {
+          load_pair(b1, min(k + 1, last));
+          compute_pair(b0, k);
+          load_pair(b0, min(k + 2, last));
+          if (k + 1 < my_pairs) compute_pair(b1, k + 1);
         }
+      }
     }
-    float mx = fmaxf(fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3])),
-                     fmaxf(fmaxf(x[4], x[5]), fmaxf(x[6], x[7])));
-    mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
-    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-    const float m_new = fmaxf(m_run, mx);  // finite: a pair's first token is live
-    const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
-    float psum = 0.f;
-    bf16x8 pb;
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const float p = __builtin_amdgcn_exp2f(x[j] - m_new);
-      psum += p;
-      pb[j] = (__bf16)p;
-    }
-    l_run = l_run * alpha + psum;
-    m_run = m_new;
-#pragma unroll
-    for (int n = 0; n < NT; ++n) {
-      oacc[n] *= alpha;
-      oacc[n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, buf.v[n]), pb, oacc[n], 0, 0, 0);
-    }
-  };
 
-  if (my_pairs > 0) {
-    // Prefetch loads are issued unconditionally (past the end they re-read the
-    // last pair, an L2 hit) so the compiler can wait for exactly the buffer
-    // being computed while the other one is in flight.
-    const int last = my_pairs - 1;
-    DecodePairBuf<D> b0, b1;
-    load_pair(b0, 0);
-    for (int k = 0; k < my_pairs; k += 2) {
-      load_pair(b1, min(k + 1, last));
-      compute_pair(b0, k);
-      load_pair(b0, min(k + 2, last));
-      if (k + 1 < my_pairs) compute_pair(b1, k + 1);
-    }
-  }
+    // Row sum over the four lane groups (each summed its own tokens).
+    float l_tot = l_run + __shfl_xor(l_run, 16, 64);
+    l_tot += __shfl_xor(l_tot, 32, 64);
 
-  // Row sum over the four lane groups (each summed its own tokens).
-  float l_tot = l_run + __shfl_xor(l_run, 16, 64);
-  l_tot += __shfl_xor(l_tot, 32, 64);
-
-  // ---- merge the four waves in wave 0 (identical lane layouts)
-  if (w > 0) {
-    s_ml[w - 1][0][l] = m_run;
-    s_ml[w - 1][1][l] = l_tot;
+    // ---- merge the four waves in wave 0 (identical lane layouts)
+    if (w > 0) {
+      s_ml[w - 1][0][l] = m_run;
+      s_ml[w - 1][1][l] = l_tot;
 #pragma unroll
-    for (int n = 0; n < NT; ++n) s_o[w - 1][n][l] = oacc[n];
-  }
-  __syncthreads();
-  if (w == 0) {
-    float mw[kDecWaves], lw[kDecWaves];
-    mw[0] = m_run;
-    lw[0] = l_tot;
-    float M = m_run;
-#pragma unroll
-    for (int i = 1; i < kDecWaves; ++i) {
-      mw[i] = s_ml[i - 1][0][l];
-      lw[i] = s_ml[i - 1][1][l];
-      M = fmaxf(M, mw[i]);
+      for (int n = 0; n < NT; ++n) s_o[w - 1][n][l] = oacc[n];
     }
-    float sc[kDecWaves], L = 0.f;
+    __syncthreads();
+    if (w == 0) {
+      float mw[kDecWaves], lw[kDecWaves];
+      mw[0] = m_run;
+      lw[0] = l_tot;
+      float M = m_run;
 #pragma unroll
-    for (int i = 0; i < kDecWaves; ++i) {
-      sc[i] = __builtin_amdgcn_exp2f(mw[i] - M);  // a wave without pairs has m = -inf -> 0
-      L += sc[i] * lw[i];
-    }
+      for (int i = 1; i < kDecWaves; ++i) {
+        mw[i] = s_ml[i - 1][0][l];
+        lw[i] = s_ml[i - 1][1][l];
+        M = fmaxf(M, mw[i]);
+      }
+      float sc[kDecWaves], L = 0.f;
 #pragma unroll
-    for (int n = 0; n < NT; ++n) {
-      f32x4 o = oacc[n] * sc[0];
-#pragma unroll
-      for (int i = 1; i < kDecWaves; ++i) o += s_o[i - 1][n][l] * sc[i];
-      oacc[n] = o;
-    }
-    m_run = M;
-    l_tot = L;
-  }
-
-  const int head = c * g + hl;
-  if (nsplit == 1) {
-    if (w == 0 && hl < g) {
-      const float inv = 1.f / l_tot;
-      uint16_t* op = a.out + ((int64_t)r * hq + head) * D + 4 * qg;
+      for (int i = 0; i < kDecWaves; ++i) {
+        sc[i] = __builtin_amdgcn_exp2f(mw[i] - M);  // a wave without pairs has m = -inf -> 0
+        L += sc[i] * lw[i];
+      }
 #pragma unroll
       for (int n = 0; n < NT; ++n) {
-        u32x2 wv;
-        wv[0] = pack_bf16x2(oacc[n][0] * inv, oacc[n][1] * inv);
-        wv[1] = pack_bf16x2(oacc[n][2] * inv, oacc[n][3] * inv);
-        *reinterpret_cast<u32x2*>(op + 16 * n) = wv;
-      }
-      if (a.lse && qg == 0) a.lse[(int64_t)r * hq + head] = (m_run + __log2f(l_tot)) * kLn2;
-    }
-    return;
-  }
-
-  // ---- split-K: publish this split's partial for the merge kernel.
-  // Partial slot of (r, c, s) = (first split index of r + s) * Hkv + c.
-  int split_base = 0;  // splits of requests 0..r-1
-  for (int r0 = 0; r0 < r; r0 += 64) {
-    const int rr = r0 + l;
-    const int v = rr < r ? (a.ctx_lens[rr] + split - 1) / split : 0;
-    split_base += __shfl(wave_inclusive_scan(v), 63, 64);
-  }
-  const int64_t slot = (int64_t)(split_base + s) * hkv + c;
-  if (w == 0 && hl < g) {
-    float* po = a.part_o + (slot * g + hl) * D + 4 * qg;
+        f32x4 o = oacc[n] * sc[0];
 #pragma unroll
-    for (int n = 0; n < NT; ++n) *reinterpret_cast<f32x4*>(po + 16 * n) = oacc[n];
-    if (qg == 0) *reinterpret_cast<float2*>(a.part_ml + (slot * g + hl) * 2) = float2{m_run, l_tot};
+        for (int i = 1; i < kDecWaves; ++i) o += s_o[i - 1][n][l] * sc[i];
+        oacc[n] = o;
+      }
+      const int head = c * g + hl;
+      if (hl < g) {
+        if (p0 == 0 && p1 == np) {  // the whole (r, c): final output
+          const float inv = 1.f / L;
+          uint16_t* op = a.out + ((int64_t)r * hq + head) * D + 4 * qg;
+#pragma unroll
+          for (int n = 0; n < NT; ++n) {
+            u32x2 wv;
+            wv[0] = pack_bf16x2(oacc[n][0] * inv, oacc[n][1] * inv);
+            wv[1] = pack_bf16x2(oacc[n][2] * inv, oacc[n][3] * inv);
+            *reinterpret_cast<u32x2*>(op + 16 * n) = wv;
+          }
+          if (a.lse && qg == 0) a.lse[(int64_t)r * hq + head] = (M + __log2f(L)) * kLn2;
+        } else {  // a partial for the merge kernel
+          const int64_t slot = (int64_t)b + r * hkv + c;
+          float* po = a.part_o + (slot * g + hl) * D + 4 * qg;
+#pragma unroll
+          for (int n = 0; n < NT; ++n) *reinterpret_cast<f32x4*>(po + 16 * n) = oacc[n];
+          if (qg == 0) *reinterpret_cast<float2*>(a.part_ml + (slot * g + hl) * 2) = float2{M, L};
+        }
+      }
+    }
+    __syncthreads();  // the LDS merge buffers are reused by the next segment
   }
 }
 
-// Merges the split partials of every (r, c) with more than one split.
+// Merges the partials of every (r, c) whose pairs span more than one slice.
 // Workgroup = one (r, c); thread = one 4-dim chunk of one query head.
 template <int D>
 __global__ __launch_bounds__(256) void decode_merge_kernel(DecodeArgs a) {
   const int tid = threadIdx.x, l = lane_id();
-  const int hq = a.hq, hkv = a.hkv, g = hq / hkv, split = a.split;
-  int r, c;
-  {
-    int local;
-    auto cnt = [&](int rr) { return a.ctx_lens[rr] > split ? hkv : 0; };
-    if (!find_owner(blockIdx.x, a.nreq, cnt, r, local)) return;
-    c = local;
-  }
-  const int nsplit = (a.ctx_lens[r] + split - 1) / split;
-  int split_base = 0;
+  const int hq = a.hq, hkv = a.hkv, g = hq / hkv;
+  const int r = blockIdx.x / hkv, c = blockIdx.x % hkv;
+  const int np = (a.ctx_lens[r] + 31) / 32;
+  int base = 0;  // first work unit of request r
   for (int r0 = 0; r0 < r; r0 += 64) {
     const int rr = r0 + l;
-    const int v = rr < r ? (a.ctx_lens[rr] + split - 1) / split : 0;
-    split_base += __shfl(wave_inclusive_scan(v), 63, 64);
+    const int v = rr < r ? (kDecSegCost + (a.ctx_lens[rr] + 31) / 32) * hkv : 0;
+    base += __shfl(wave_inclusive_scan(v), 63, 64);
   }
-  const int64_t slot0 = (int64_t)split_base * hkv + c;
+  const int first = base + c * (kDecSegCost + np) + kDecSegCost;  // unit of the first pair
+  const int b0 = dec_slice_of(a, first), b1 = dec_slice_of(a, first + np - 1);
+  if (b0 == b1) return;  // one segment: written directly
+  const int64_t rc = (int64_t)r * hkv + c;
   const int chunks = g * (D / 4);
   for (int ch = tid; ch < chunks; ch += 256) {
     const int hh = ch / (D / 4), e0 = 4 * (ch % (D / 4));
     float M = -INFINITY, L = 0.f;
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-    auto fold = [&](float2 ml, f32x4 ov) {  // online log-sum-exp merge, split order
+    auto fold = [&](float2 ml, f32x4 ov) {  // online log-sum-exp merge, slice order
       const float Mn = fmaxf(M, ml.x);
       const float s_old = __builtin_amdgcn_exp2f(M - Mn), s_new = __builtin_amdgcn_exp2f(ml.x - Mn);
       L = L * s_old + ml.y * s_new;
       acc = acc * s_old + ov * s_new;
       M = Mn;
     };
-    int sp = 0;
-    for (; sp + 4 <= nsplit; sp += 4) {  // four independent loads in flight
+    int b = b0;
+    for (; b + 4 <= b1 + 1; b += 4) {  // four independent loads in flight
       float2 ml[4];
       f32x4 ov[4];
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
-        const int64_t sl = slot0 + (int64_t)(sp + u) * hkv;
+        const int64_t sl = b + u + rc;
         ml[u] = *reinterpret_cast<const float2*>(a.part_ml + (sl * g + hh) * 2);
         ov[u] = *reinterpret_cast<const f32x4*>(a.part_o + (sl * g + hh) * D + e0);
       }
 #pragma unroll
       for (int u = 0; u < 4; ++u) fold(ml[u], ov[u]);
     }
-    for (; sp < nsplit; ++sp) {
-      const int64_t sl = slot0 + (int64_t)sp * hkv;
+    for (; b <= b1; ++b) {
+      const int64_t sl = b + rc;
       fold(*reinterpret_cast<const float2*>(a.part_ml + (sl * g + hh) * 2),
            *reinterpret_cast<const f32x4*>(a.part_o + (sl * g + hh) * D + e0));
     }
