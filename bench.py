@@ -46,7 +46,8 @@ KERNEL_SOURCES = ("paper_2511_20982_amd/csrc/dopd_attn.hip",
 # Kernels behind each timed call (the decode call is a split kernel plus, when
 # some context exceeds one split, a merge kernel).
 CALL_KERNELS = {"decode": ("decode_split_kernel", "decode_merge_kernel"),
-                "prefill": ("prefill_bf16_kernel",), "prefill_chunked": ("prefill_bf16_kernel",),
+                "prefill": ("prefill_bf16_kernel<128, false>", "prefill_bf16_kernel<64, false>"),
+                "prefill_chunked": ("prefill_bf16_kernel<128, true>", "prefill_bf16_kernel<64, true>"),
                 "kv_write": ("kv_write_kernel",),
                 "pack": ("kv_pack_kernel",), "unpack": ("kv_unpack_kernel",)}
 
