@@ -38,8 +38,16 @@ def _lib():
         lib.oracle_kv_write.argtypes = [i32, i32, i32, P, P, P, P, P, i32, P, P, i32]
         lib.oracle_pack.argtypes = [i32, i32, i32, i32, P, P, i32, P, i32, P, P, P, i32, P]
         lib.oracle_unpack.argtypes = [i32, i32, i32, i32, P, P, P, P, i32, P, P, i32, P, i32]
+        lib.oracle_e4m3_value.argtypes = [C.c_uint8]
+        lib.oracle_e4m3_value.restype = C.c_double
+        lib.oracle_e4m3_encode.argtypes = [C.c_float]
+        lib.oracle_e4m3_encode.restype = C.c_uint8
+        lib.oracle_e4m3_quantize.argtypes = [i32, C.c_int64, i32, i32, P, P, P]
+        lib.oracle_decode_e4m3.argtypes = [i32, i32, i32, i32, C.c_float, P, P, P, P, P, P, i32,
+                                           P, i32, P, P]
         for f in (lib.oracle_prefill, lib.oracle_prefill_rows, lib.oracle_decode,
-                  lib.oracle_kv_write, lib.oracle_pack, lib.oracle_unpack):
+                  lib.oracle_kv_write, lib.oracle_pack, lib.oracle_unpack,
+                  lib.oracle_prefill_paged, lib.oracle_e4m3_quantize, lib.oracle_decode_e4m3):
             f.restype = i32
         _LIB = lib
     return _LIB
@@ -182,3 +190,58 @@ def unpack(buf, in_offsets, req_ids, seq_lens, k_pool, v_pool, num_layers, page_
     _lib().oracle_unpack(kp.itemsize, hkv, d, num_layers, _p(buf), _p(off), _p(req), _p(lens),
                          len(req), _p(kp), _p(vp), num_pages, _p(pt), pt.shape[1])
     return kp, vp
+
+
+# ---- FP8 (OCP E4M3) KV pages ------------------------------------------------
+def e4m3_value(codes):
+    """float64 value of each E4M3 code (oracle.c: oracle_e4m3_value)."""
+    table = np.array([_lib().oracle_e4m3_value(c) for c in range(256)], np.float64)
+    return table[np.asarray(codes, np.uint8)]
+
+
+def e4m3_encode(y):
+    """Nearest E4M3 code (ties to even, saturating at 448) of each float32 y."""
+    y = _c(y, np.float32)
+    out = np.zeros(y.shape, np.uint8)
+    one = np.ones(1, np.float32)
+    rc = _lib().oracle_e4m3_quantize(FP32, y.size, 1, 1, _p(y), _p(one), _p(out))
+    if rc:
+        raise ValueError(f"oracle_e4m3_quantize rc={rc}")
+    return out
+
+
+def e4m3_quantize(x, scale):
+    """Codes of x[T][Hkv][d] (bf16 bits or float32) with one scale per head:
+    E4M3_rne(sat(x * fp32(1/scale[h]))), the product in fp32."""
+    x = _c(x)
+    sc = _c(scale, np.float32)
+    t, hkv, d = x.shape
+    if sc.shape != (hkv,):
+        raise ValueError("one scale per KV head")
+    out = np.zeros(x.shape, np.uint8)
+    rc = _lib().oracle_e4m3_quantize(_dt(x), t, hkv, d, _p(x), _p(sc), _p(out))
+    if rc:
+        raise ValueError(f"oracle_e4m3_quantize rc={rc}")
+    return out
+
+
+def decode_e4m3(q, k_pool, v_pool, k_scale, v_scale, page_table, context_lens, scale):
+    """Paged decode over E4M3 pools (uint8 codes, bf16/fp32 q) with per-KV-head
+    scales -> (out[B][Hq][d], lse[B][Hq])."""
+    q = _c(q)
+    k_pool, v_pool = _c(k_pool, np.uint8), _c(v_pool, np.uint8)
+    ks, vs = _c(k_scale, np.float32), _c(v_scale, np.float32)
+    pt = _c(page_table, np.int32)
+    ctx = _c(context_lens, np.int32)
+    b, hq, d = q.shape
+    hkv = k_pool.shape[-3]
+    if ks.shape != (hkv,) or vs.shape != (hkv,):
+        raise ValueError("one scale per KV head")
+    out = np.zeros((b, hq, d), np.float64)
+    lse = np.zeros((b, hq), np.float64)
+    rc = _lib().oracle_decode_e4m3(_dt(q), hq, hkv, d, float(scale), _p(q), _p(k_pool),
+                                   _p(v_pool), _p(ks), _p(vs), _p(pt), pt.shape[1], _p(ctx), b,
+                                   _p(out), _p(lse))
+    if rc:
+        raise ValueError(f"oracle_decode_e4m3 rc={rc}")
+    return out, lse

@@ -23,6 +23,17 @@
  *
  * Inputs are bf16 bit patterns (uint16) or fp32, widened exactly to double.
  * sigma is the float scale widened to double.  Outputs are double.
+ *
+ * FP8 KV pages (a storage format the paper's FP8 models imply, Sec. VI-A;
+ * the paper gives no scaling rule): OCP 8-bit floating point E4M3 -- 1 sign,
+ * 4 exponent (bias 7) and 3 mantissa bits, no infinities, S.1111.111 is NaN,
+ * largest finite value 448.  One scale per KV head and pool (K and V
+ * separately): the stored code of element x of head h is
+ *   code = E4M3_rne(sat(float(x) * float(1 / scale[h])))
+ * where 1/scale and the product are fp32 operations rounded to nearest even,
+ * sat() clamps to [-448, 448] (NaN stays NaN) and E4M3_rne rounds to the
+ * nearest code, ties to the even code.  The cached value is value(code) *
+ * scale[h], exactly, in double.
  */
 #include <math.h>
 #include <stdint.h>
@@ -31,9 +42,62 @@
 
 #define OR_BF16 0
 #define OR_FP32 1
+#define OR_E4M3 2
 #define OR_PAGE 16
 
+/* Value of an E4M3 code: (-1)^s 2^(E-7) (1 + M/8) for E >= 1, (-1)^s 2^-6 M/8
+ * for E = 0. */
+double oracle_e4m3_value(uint8_t c) {
+  const int s = c >> 7, e = (c >> 3) & 15, m = c & 7;
+  if (e == 15 && m == 7) return NAN;
+  const double v = e == 0 ? ldexp((double)m, -9) : ldexp((double)(8 + m), e - 10);
+  return s ? -v : v;
+}
+
+/* Nearest E4M3 code of y (ties to even), saturating at +-448. */
+uint8_t oracle_e4m3_encode(float y) {
+  const uint8_t s = signbit(y) ? 0x80 : 0;
+  if (isnan(y)) return s | 0x7F;
+  const double a = fabs((double)y);
+  if (a >= 448.0) return s | 0x7E;
+  if (a < ldexp(1.0, -6)) /* subnormal step 2^-9; 8 steps is the code of 2^-6 */
+    return s | (uint8_t)nearbyint(a * 512.0);
+  int ex;
+  frexp(a, &ex); /* a in [2^(ex-1), 2^ex) */
+  int E = ex - 1; /* -6 .. 8 */
+  int m = (int)nearbyint(ldexp(a, 3 - E)); /* 8 .. 16 */
+  if (m == 16) {
+    m = 8;
+    E += 1;
+  }
+  return s | (uint8_t)((E + 7) << 3) | (uint8_t)(m - 8);
+}
+
+/* Codes of x[n][hkv][d] (bf16 bits or fp32) with one scale per head. */
+int oracle_e4m3_quantize(int dtype, int64_t n, int hkv, int d, const void *x,
+                         const float *scale, uint8_t *out) {
+  for (int h = 0; h < hkv; ++h)
+    if (!(scale[h] > 0.0f)) return 1;
+  for (int64_t t = 0; t < n; ++t)
+    for (int h = 0; h < hkv; ++h) {
+      const float inv = 1.0f / scale[h];
+      for (int e = 0; e < d; ++e) {
+        const int64_t i = (t * hkv + h) * d + e;
+        float xf;
+        if (dtype == OR_BF16) {
+          uint32_t u = (uint32_t)((const uint16_t *)x)[i] << 16;
+          memcpy(&xf, &u, 4);
+        } else {
+          xf = ((const float *)x)[i];
+        }
+        out[i] = oracle_e4m3_encode(xf * inv);
+      }
+    }
+  return 0;
+}
+
 static inline double ld(const void *base, int dtype, int64_t i) {
+  if (dtype == OR_E4M3) return oracle_e4m3_value(((const uint8_t *)base)[i]);
   if (dtype == OR_BF16) {
     uint32_t u = (uint32_t)((const uint16_t *)base)[i] << 16;
     float f;
@@ -46,15 +110,16 @@ static inline double ld(const void *base, int dtype, int64_t i) {
 /* One query row against n keys given by explicit element offsets.
  * koff[j] / voff[j] are the element offsets of key/value j; element e of
  * key j is at koff[j] + e*kstride_e, of value j at voff[j] + e*vstride_e. */
-static void attend_row(int dtype, int d, double sigma, const void *q, int64_t qoff,
-                       const void *kb, const int64_t *koff, int64_t kse,
-                       const void *vb, const int64_t *voff, int64_t vse, int n,
-                       double *sc, double *out, double *lse) {
+static void attend_row_kv(int qdt, int kvdt, double kscale, double vscale, int d,
+                          double sigma, const void *q, int64_t qoff, const void *kb,
+                          const int64_t *koff, int64_t kse, const void *vb,
+                          const int64_t *voff, int64_t vse, int n, double *sc, double *out,
+                          double *lse) {
   double m = -INFINITY;
   for (int j = 0; j < n; ++j) {
     double s = 0.0;
     for (int e = 0; e < d; ++e)
-      s += ld(q, dtype, qoff + e) * ld(kb, dtype, koff[j] + e * kse);
+      s += ld(q, qdt, qoff + e) * (ld(kb, kvdt, koff[j] + e * kse) * kscale);
     sc[j] = sigma * s;
     if (sc[j] > m) m = sc[j];
   }
@@ -65,10 +130,19 @@ static void attend_row(int dtype, int d, double sigma, const void *q, int64_t qo
   }
   for (int e = 0; e < d; ++e) {
     double acc = 0.0;
-    for (int j = 0; j < n; ++j) acc += sc[j] * ld(vb, dtype, voff[j] + e * vse);
+    for (int j = 0; j < n; ++j) acc += sc[j] * (ld(vb, kvdt, voff[j] + e * vse) * vscale);
     out[e] = acc / l;
   }
   if (lse) *lse = m + log(l);
+}
+
+/* Q, K and V of one element type, unscaled. */
+static void attend_row(int dtype, int d, double sigma, const void *q, int64_t qoff,
+                       const void *kb, const int64_t *koff, int64_t kse,
+                       const void *vb, const int64_t *voff, int64_t vse, int n,
+                       double *sc, double *out, double *lse) {
+  attend_row_kv(dtype, dtype, 1.0, 1.0, d, sigma, q, qoff, kb, koff, kse, vb, voff, vse, n, sc,
+                out, lse);
 }
 
 /* Varlen causal prefill over contiguous token-major Q[T][Hq][d], K/V[T][Hkv][d].
@@ -148,9 +222,10 @@ int oracle_prefill_rows(int dtype, int hq, int hkv, int d, float scale, const vo
 
 /* Single-query decode over the paged cache.
  * q[B][Hq][d]; context_lens[B] counts the current token; out[B][Hq][d]; lse[B][Hq]. */
-int oracle_decode(int dtype, int hq, int hkv, int d, float scale, const void *q,
-                  const void *k_pool, const void *v_pool, const int32_t *page_table,
-                  int pt_stride, const int32_t *ctx, int nreq, double *out, double *lse) {
+static int decode_impl(int qdt, int kvdt, const float *k_scale, const float *v_scale, int hq,
+                       int hkv, int d, float scale, const void *q, const void *k_pool,
+                       const void *v_pool, const int32_t *page_table, int pt_stride,
+                       const int32_t *ctx, int nreq, double *out, double *lse) {
   if (hkv <= 0 || hq % hkv) return 1;
   const int g = hq / hkv;
   const double sigma = (double)scale;
@@ -172,14 +247,33 @@ int oracle_decode(int dtype, int hq, int hkv, int d, float scale, const void *q,
         koff[j] = ((page * hkv + c) * OR_PAGE + slot) * d;   /* element e at +e   */
         voff[j] = (page * hkv + c) * (int64_t)d * OR_PAGE + slot; /* element e at +16e */
       }
-      attend_row(dtype, d, sigma, q, p * d, k_pool, koff, 1, v_pool, voff, OR_PAGE, ctx[r], sc,
-                 out + p * d, lse ? lse + p : NULL);
+      attend_row_kv(qdt, kvdt, k_scale ? (double)k_scale[c] : 1.0,
+                    v_scale ? (double)v_scale[c] : 1.0, d, sigma, q, p * d, k_pool, koff, 1,
+                    v_pool, voff, OR_PAGE, ctx[r], sc, out + p * d, lse ? lse + p : NULL);
     }
     free(sc);
     free(koff);
     free(voff);
   }
   return 0;
+}
+
+int oracle_decode(int dtype, int hq, int hkv, int d, float scale, const void *q,
+                  const void *k_pool, const void *v_pool, const int32_t *page_table,
+                  int pt_stride, const int32_t *ctx, int nreq, double *out, double *lse) {
+  return decode_impl(dtype, dtype, NULL, NULL, hq, hkv, d, scale, q, k_pool, v_pool, page_table,
+                     pt_stride, ctx, nreq, out, lse);
+}
+
+/* Decode over E4M3 pools (codes, same page layouts) with per-KV-head scales:
+ * key j of head c is value(code) * k_scale[c], value j is value(code) *
+ * v_scale[c].  q (bf16 or fp32 by qdtype) [B][Hq][d]. */
+int oracle_decode_e4m3(int qdtype, int hq, int hkv, int d, float scale, const void *q,
+                       const uint8_t *k_pool, const uint8_t *v_pool, const float *k_scale,
+                       const float *v_scale, const int32_t *page_table, int pt_stride,
+                       const int32_t *ctx, int nreq, double *out, double *lse) {
+  return decode_impl(qdtype, OR_E4M3, k_scale, v_scale, hq, hkv, d, scale, q, k_pool, v_pool,
+                     page_table, pt_stride, ctx, nreq, out, lse);
 }
 
 /* Prefill of a chunk over the paged cache (a prompt processed in chunks, or a

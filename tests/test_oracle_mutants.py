@@ -48,6 +48,14 @@ MUTANTS = {
                                           "attend_row(dtype, d, sigma, q, ((t - cu_q[r]) * hq + h) * d, k_pool")],
     "paged_prefill_v_token_major": [("k_pool, koff, 1, v_pool, voff, OR_PAGE,\n                 nkeys",
                                      "k_pool, koff, 1, v_pool, koff, 1,\n                 nkeys")],
+    "e4m3_exponent_bias_8": [("ldexp((double)(8 + m), e - 10)", "ldexp((double)(8 + m), e - 11)")],
+    "e4m3_encode_ties_away": [("int m = (int)nearbyint(ldexp(a, 3 - E));", "int m = (int)round(ldexp(a, 3 - E));")],
+    "e4m3_overflow_to_nan": [("if (a >= 448.0) return s | 0x7E;", "if (a >= 464.0) return s | 0x7F;")],
+    "e4m3_subnormal_step": [("return s | (uint8_t)nearbyint(a * 512.0);", "return s | (uint8_t)nearbyint(a * 256.0);")],
+    "quantize_multiplies_by_scale": [("out[i] = oracle_e4m3_encode(xf * inv);", "out[i] = oracle_e4m3_encode(xf * scale[h]);")],
+    "quantize_first_head_scale": [("const float inv = 1.0f / scale[h];", "const float inv = 1.0f / scale[0];")],
+    "decode_e4m3_k_scale_of_head0": [("k_scale ? (double)k_scale[c] : 1.0", "k_scale ? (double)k_scale[0] : 1.0")],
+    "decode_e4m3_v_scale_as_k_scale": [("v_scale ? (double)v_scale[c] : 1.0", "v_scale ? (double)k_scale[c] : 1.0")],
     "pack_token_dim_transposed": [("const int64_t dst = off[n] + ((((int64_t)layer * 2 + c) * hkv + h) * len + t) * d + e;",
                                    "const int64_t dst = off[n] + ((((int64_t)layer * 2 + c) * hkv + h) * d + e) * len + t;")],
 }
@@ -70,7 +78,8 @@ def _load(path):
     lib = ctypes.CDLL(path)
     real = oracle._lib()
     for f in ("oracle_prefill", "oracle_prefill_rows", "oracle_decode", "oracle_kv_write",
-              "oracle_pack", "oracle_unpack", "oracle_prefill_paged"):
+              "oracle_pack", "oracle_unpack", "oracle_prefill_paged", "oracle_e4m3_value",
+              "oracle_e4m3_encode", "oracle_e4m3_quantize", "oracle_decode_e4m3"):
         getattr(lib, f).argtypes = getattr(real, f).argtypes
         getattr(lib, f).restype = getattr(real, f).restype
     return lib
@@ -222,7 +231,53 @@ def chk_chunked_equals_one_shot():
     return True
 
 
-CHECKS = [chk_prefill_brute, chk_prefill_sdpa, chk_lse, chk_decode_brute,
+def chk_e4m3_table():
+    v = oracle.e4m3_value(np.arange(256))
+    t = torch.arange(256, dtype=torch.uint8).view(torch.float8_e4m3fn).to(torch.float64).numpy()
+    fin = ~np.isnan(t)
+    return bool(np.array_equal(np.isnan(v), ~fin) and np.array_equal(v[fin], t[fin]))
+
+
+def chk_e4m3_encode():
+    v = torch.arange(127, dtype=torch.uint8).view(torch.float8_e4m3fn).to(torch.float64).numpy()
+    mids = ((v[:-1] + v[1:]) / 2).astype(np.float32)
+    lo = np.arange(126)
+    ok = np.array_equal(oracle.e4m3_encode(mids), np.where(lo % 2 == 0, lo, lo + 1))
+    big = np.array([448, 470, 1e9, -1e9], np.float32)
+    ok &= list(oracle.e4m3_encode(big)) == [0x7E, 0x7E, 0x7E, 0xFE]
+    y = np.random.default_rng(31).standard_normal(2000).astype(np.float32) * 20
+    t = torch.from_numpy(y).to(torch.float8_e4m3fn).view(torch.uint8).numpy()
+    return bool(ok and np.array_equal(oracle.e4m3_encode(y), t))
+
+
+def chk_e4m3_quantize():
+    rng = np.random.default_rng(32)
+    x = I.normal(rng, (5, 3, 8), "fp32")
+    scale = np.array([0.5, 0.01, 0.07], np.float32)
+    y = x * (np.float32(1) / scale)[None, :, None]
+    t = torch.from_numpy(np.clip(y, -448, 448).astype(np.float32)).to(
+        torch.float8_e4m3fn).view(torch.uint8).numpy()
+    return bool(np.array_equal(oracle.e4m3_quantize(x, scale), t))
+
+
+def chk_decode_e4m3_brute():
+    w = I.decode_workload("t", 33, [1, 17, 40], 4, 2, 16, "bf16")
+    rng = np.random.default_rng(33)
+    kp = rng.integers(0, 0x7F, w.k_pool.shape).astype(np.uint8) | (
+        rng.integers(0, 2, w.k_pool.shape).astype(np.uint8) << 7)
+    vp = rng.integers(0, 0x7F, w.v_pool.shape).astype(np.uint8)
+    ks = np.array([0.01, 0.03], np.float32)
+    vs = np.array([0.02, 0.005], np.float32)
+    out, _ = oracle.decode_e4m3(w.q_dec, kp, vp, ks, vs, w.page_table, w.context_lens, w.scale)
+    tab = torch.arange(256, dtype=torch.uint8).view(torch.float8_e4m3fn).to(torch.float64).numpy()
+    kd = tab[kp] * ks.astype(np.float64)[None, :, None, None]
+    vd = tab[vp] * vs.astype(np.float64)[None, :, None, None]
+    ref = brute.decode(w.q_dec, kd, vd, w.page_table, w.context_lens, w.scale)
+    return _close(out, ref, 1e-12)
+
+
+CHECKS = [chk_e4m3_table, chk_e4m3_encode, chk_e4m3_quantize, chk_decode_e4m3_brute,
+          chk_prefill_brute, chk_prefill_sdpa, chk_lse, chk_decode_brute,
           chk_last_row_equals_decode, chk_write_pack_transpose, chk_closed_forms,
           chk_unpack_matches_write, chk_paged_prefill_brute, chk_chunked_equals_one_shot]
 
