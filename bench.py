@@ -71,10 +71,13 @@ WORKLOADS = {
 
 
 # ------------------------------------------------------------------ algorithmic work
-def decode_bytes(ctx, hq, hkv, d, s=2):
+def decode_bytes(ctx, hq, hkv, d, s=2, kv_s=None):
+    """K and V once (kv_s bytes per element), q and out (s bytes), page ids, lengths."""
     ctx = np.asarray(ctx, np.int64)
     b = len(ctx)
-    return int((2 * hkv * d * ctx * s).sum() + b * hq * d * 2 * s + (4 * ((ctx + 15) // 16)).sum() + 4 * b)
+    kv_s = s if kv_s is None else kv_s
+    return int((2 * hkv * d * ctx * kv_s).sum() + b * hq * d * 2 * s +
+               (4 * ((ctx + 15) // 16)).sum() + 4 * b)
 
 
 def prefill_flops(lens, hq, d):
@@ -236,6 +239,9 @@ def main():
     ap.add_argument("--streams", type=int, default=1, choices=(1, 2),
                     help="mixed step: 2 = decode on its own stream beside prefill/write/pack, "
                          "1 = everything in order on one stream")
+    ap.add_argument("--kv", choices=("bf16", "fp8"), default="bf16",
+                    help="decode workloads: KV cache element type (fp8 = E4M3 pages with "
+                         "per-KV-head scales, written by the fp8 writer before timing)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calib-mib", type=int, default=0,
                     help="after timing, run one device copy of this size (counter calibration)")
@@ -249,6 +255,9 @@ def main():
         summarize(args)
         return
 
+    if args.kv == "fp8" and args.workload not in ("decode_mha", "decode_gqa"):
+        print("--kv fp8 applies to the decode_mha and decode_gqa workloads", file=sys.stderr)
+        sys.exit(2)
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py runs on one GPU only: the hot path is measured on a single MI355X; "
               "--gpus must be 1", file=sys.stderr)
@@ -354,13 +363,45 @@ def main():
         n_dec = len(w.context_lens)
         ws = A.decode_workspace(shape, w.context_lens, n_dec, args.split)
         tm = {"decode": Timer(torch, sA)}
+        if args.kv == "fp8":
+            # The cache as a prefill would leave it: token-major K/V of every
+            # cached token (gathered from the bf16 pools), one scale per KV head
+            # from its absolute maximum, written by the fp8 writer (untimed).
+            shape8 = A.make_shape(w.hq, w.hkv, w.d, "fp8", w.scale)
+            cl = w.context_lens.astype(np.int64)
+            r_idx = np.repeat(np.arange(n_dec), cl)
+            j = np.arange(int(cl.sum())) - np.repeat(np.cumsum(cl) - cl, cl)
+            pg = torch.from_numpy(w.page_table[r_idx, j // 16].astype(np.int64)).to(dev)
+            sl = torch.from_numpy((j % 16).astype(np.int64)).to(dev)
+            ktok = kp[pg, :, sl, :].contiguous()          # [T][Hkv][d]
+            vtok = vp[pg, :, :, sl].contiguous()          # [T][Hkv][d]
+            ks = (ktok.abs().amax(dim=(0, 2)).float() / 448.0).contiguous()
+            vs = (vtok.abs().amax(dim=(0, 2)).float() / 448.0).contiguous()
+            kp8 = torch.full((w.num_pages, w.hkv, 16, w.d), 0x7F, dtype=torch.uint8, device=dev)
+            vp8 = torch.full((w.num_pages, w.hkv, w.d, 16), 0x7F, dtype=torch.uint8, device=dev)
+            cu_t = A.to_device(I.cu_from_lens(w.context_lens))
+            A.dopd_kv_write_fp8(shape8, ktok, vtok, ks, vs, kp8, vp8, w.num_pages, pt,
+                                w.page_table.shape[1], cu_t,
+                                torch.zeros(n_dec, dtype=torch.int32, device=dev), n_dec,
+                                int(cl.sum()), sA)
+            torch.cuda.synchronize()
+            del ktok, vtok, kp, vp
 
-        def step():
-            with tm["decode"]:
-                A.dopd_decode_attn(shape, q_dec, kp, vp, w.num_pages, pt, w.page_table.shape[1],
-                                   ctx, w.context_lens, n_dec, args.split, out_d, None, ws, stream=sA)
+            def step():
+                with tm["decode"]:
+                    A.dopd_decode_attn_fp8(shape8, q_dec, kp8, vp8, ks, vs, w.num_pages, pt,
+                                           w.page_table.shape[1], ctx, w.context_lens, n_dec,
+                                           args.split, out_d, None, ws, stream=sA)
 
-        work = {"decode": ("GB/s", decode_bytes(w.context_lens, w.hq, w.hkv, w.d))}
+            work = {"decode": ("GB/s", decode_bytes(w.context_lens, w.hq, w.hkv, w.d, kv_s=1))}
+        else:
+            def step():
+                with tm["decode"]:
+                    A.dopd_decode_attn(shape, q_dec, kp, vp, w.num_pages, pt,
+                                       w.page_table.shape[1], ctx, w.context_lens, n_dec,
+                                       args.split, out_d, None, ws, stream=sA)
+
+            work = {"decode": ("GB/s", decode_bytes(w.context_lens, w.hq, w.hkv, w.d))}
         dominant = "decode"
     elif args.workload == "handoff":
         L = args.pack_layers
@@ -523,7 +564,8 @@ def main():
                 "bound": "mfma" if dk["unit"] == "TFLOP/s" else "hbm",
                 "achieved": dk["rate"], "peak": BF16_PEAK_TFLOPS if dk["unit"] == "TFLOP/s" else HBM_PEAK_GBS,
                 "unit": dk["unit"], "frac": dk["frac"],
-                "traffic": load_traffic(args.workload, dominant)}
+                "traffic": load_traffic(args.workload + ("_fp8" if args.kv == "fp8" else ""),
+                                        dominant)}
 
     # ---- CPU baseline: the fp64 oracle on host cores, plus a parity spot check
     cpu = None
@@ -532,7 +574,29 @@ def main():
         import oracle
         threads = int(os.environ.get("OMP_NUM_THREADS", "0")) or len(os.sched_getaffinity(0))
         os.environ.setdefault("OMP_NUM_THREADS", str(threads))
-        if dominant == "decode":
+        if dominant == "decode" and args.kv == "fp8":
+            # The oracle quantises the bf16 cache itself (same scales, its own
+            # encoder) and decodes the whole batch over its codes.
+            ks_h, vs_h = ks.cpu().numpy(), vs.cpu().numpy()
+            P, hkv, d = w.num_pages, w.hkv, w.d
+            kq = oracle.e4m3_quantize(w.k_pool.transpose(0, 2, 1, 3).reshape(-1, hkv, d), ks_h)
+            vq = oracle.e4m3_quantize(w.v_pool.transpose(0, 3, 1, 2).reshape(-1, hkv, d), vs_h)
+            kq = kq.reshape(P, 16, hkv, d).transpose(0, 2, 1, 3).copy()
+            vq = vq.reshape(P, 16, hkv, d).transpose(0, 2, 3, 1).copy()
+            t1 = time.time()
+            ref, _ = oracle.decode_e4m3(w.q_dec, kq, vq, ks_h, vs_h, w.page_table,
+                                        w.context_lens, w.scale)
+            dt = time.time() - t1
+            amount = work["decode"][1]
+            cpu = {"value": round(amount / dt / 1e9, 4), "unit": "GB/s", "cores": threads,
+                   "kind": "oracle", "cpu": cpu_info(), "seconds": round(dt, 2),
+                   "sample": f"fp64 oracle decode over E4M3 pages of the whole batch "
+                             f"({len(w.context_lens)} requests, {amount / 1e9:.3f} GB algorithmic)"}
+            gotf = I.bf16_bits_to_f32(A.to_host(out_d)).astype(np.float64)
+            parity = {"decode_max_abs_err": float(np.max(np.abs(gotf - ref))),
+                      "decode_rows": int(ref.shape[0] * ref.shape[1]),
+                      "kv": "fp8 pages from the GPU writer; oracle quantised the same bf16 cache"}
+        elif dominant == "decode":
             # The whole decode batch of the step (about a second of host work).
             t1 = time.time()
             ref, _ = oracle.decode(w.q_dec, w.k_pool, w.v_pool, w.page_table, w.context_lens,
@@ -591,7 +655,9 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic",
-        "config": {"workload": desc, "seed": int(w.seed), "split_tokens": args.split,
+        "config": {"workload": desc + (", KV cache E4M3 with per-KV-head scales"
+                                       if args.kv == "fp8" else ""),
+                   "seed": int(w.seed), "split_tokens": args.split, "kv": args.kv,
                    "streams": args.streams if args.workload == "mixed" else 1,
                    "pack_layers": args.pack_layers if args.workload in ("mixed", "handoff") else None,
                    "chunk": args.chunk if args.workload == "chunked" else None,

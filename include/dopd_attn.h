@@ -24,6 +24,16 @@
  *   call only enqueues work on that stream; nothing synchronises.
  * - Element types: DOPD_BF16 (bf16 storage, fp32 accumulation, outputs
  *   rounded to nearest even) or DOPD_FP32 (fp32 throughout).
+ *   DOPD_FP8_E4M3 describes a paged cache of OCP E4M3 codes (one byte per
+ *   element; 1 sign, 4 exponent bits with bias 7, 3 mantissa bits, no
+ *   infinities, largest finite value 448) with one fp32 scale per KV head
+ *   for K and one for V: a cached element is code_value * scale[head].  Q,
+ *   out and fresh K/V stay bf16.  The paper's models store FP8 (Sec. VI-A);
+ *   it gives no scaling rule, so the per-head scale is this library's.  It
+ *   halves the bytes decode and handoff move.  Entry points that take it:
+ *   dopd_kv_write_fp8, dopd_decode_attn_fp8, dopd_decode_workspace_size and
+ *   the handoff pack/unpack (byte copies); the others return
+ *   DOPD_ERR_UNSUPPORTED for it.
  * - Fresh tokens are token-major: Q/out [T][Hq][d], K/V [T][Hkv][d].
  * - GQA: query head h uses KV head h / (Hq / Hkv); Hq % Hkv must be 0.
  * - Paged cache (one pool per layer, page_size = 16 tokens):
@@ -58,14 +68,14 @@ enum {
   DOPD_ERR_HIP = 5
 };
 
-enum { DOPD_BF16 = 0, DOPD_FP32 = 1 };
+enum { DOPD_BF16 = 0, DOPD_FP32 = 1, DOPD_FP8_E4M3 = 2 };
 
 typedef struct {
   int32_t num_q_heads;   /* Hq                                   */
   int32_t num_kv_heads;  /* Hkv, divides Hq                      */
   int32_t head_dim;      /* d: 64 or 128                         */
   int32_t page_size;     /* tokens per cache page: 16            */
-  int32_t dtype;         /* DOPD_BF16 or DOPD_FP32               */
+  int32_t dtype;         /* DOPD_BF16, DOPD_FP32, DOPD_FP8_E4M3  */
   float softmax_scale;   /* multiplies Q.K before the softmax    */
 } dopd_attn_shape;
 
@@ -130,6 +140,24 @@ dopd_status dopd_kv_write(const dopd_attn_shape* shape, const void* k_new, const
                           int32_t num_reqs, int32_t total_new_tokens, void* stream);
 
 /*
+ * Paged KV write into E4M3 pools (shape->dtype = DOPD_FP8_E4M3): the same
+ * placement as dopd_kv_write, from bf16 k_new/v_new [total_new_tokens][Hkv][d],
+ * with element x of KV head h stored as the code
+ *     E4M3_rne(sat(x * fp32(1 / scale[h])))
+ * where 1/scale[h] and the product are fp32 operations rounded to nearest
+ * even, sat() clamps to [-448, 448] (NaN stays NaN) and E4M3_rne rounds to
+ * the nearest code, ties to the even code.  k_scale/v_scale: device fp32
+ * [Hkv], positive and finite (not checked on the device).  k_pool/v_pool:
+ * one byte per element, same page layouts.  Other slots are untouched.
+ */
+dopd_status dopd_kv_write_fp8(const dopd_attn_shape* shape, const void* k_new, const void* v_new,
+                              const float* k_scale, const float* v_scale, void* k_pool,
+                              void* v_pool, int32_t num_pages, const int32_t* page_table,
+                              int32_t page_table_stride, const int32_t* cu_new_tokens,
+                              const int32_t* start_pos, int32_t num_reqs,
+                              int32_t total_new_tokens, void* stream);
+
+/*
  * Paged single-query decode attention: for request r with context_lens[r]
  * cached tokens (counting the current one, whose K/V must already be in the
  * cache) and every query head h,
@@ -158,7 +186,24 @@ dopd_status dopd_decode_attn(const dopd_attn_shape* shape, const void* q, const 
                              int32_t split_tokens, void* out, float* lse, void* workspace,
                              size_t workspace_bytes, void* stream);
 
-/* Workspace bytes dopd_decode_attn needs for these arguments (0 on bad input). */
+/*
+ * Decode over E4M3 pools (shape->dtype = DOPD_FP8_E4M3): dopd_decode_attn's
+ * operation with K_j = code * k_scale[c] and V_j = code * v_scale[c] for KV
+ * head c; q and out bf16, lse as there.  The codes are widened to bf16
+ * (exactly) for the same MFMA path; the K scale multiplies the softmax scale
+ * and the V scale the output, in fp32.  Same partition, workspace
+ * (dopd_decode_workspace_size with the same shape) and split_tokens rules;
+ * half the bytes of the bf16 cache per token.
+ */
+dopd_status dopd_decode_attn_fp8(const dopd_attn_shape* shape, const void* q,
+                                 const void* k_pool, const void* v_pool, const float* k_scale,
+                                 const float* v_scale, int32_t num_pages,
+                                 const int32_t* page_table, int32_t page_table_stride,
+                                 const int32_t* context_lens, const int32_t* context_lens_host,
+                                 int32_t num_reqs, int32_t split_tokens, void* out, float* lse,
+                                 void* workspace, size_t workspace_bytes, void* stream);
+
+/* Workspace bytes dopd_decode_attn(_fp8) needs for these arguments (0 on bad input). */
 size_t dopd_decode_workspace_size(const dopd_attn_shape* shape,
                                   const int32_t* context_lens_host, int32_t num_reqs,
                                   int32_t split_tokens);

@@ -78,6 +78,7 @@ int oracle_e4m3_quantize(int dtype, int64_t n, int hkv, int d, const void *x,
                          const float *scale, uint8_t *out) {
   for (int h = 0; h < hkv; ++h)
     if (!(scale[h] > 0.0f)) return 1;
+#pragma omp parallel for schedule(static)
   for (int64_t t = 0; t < n; ++t)
     for (int h = 0; h < hkv; ++h) {
       const float inv = 1.0f / scale[h];

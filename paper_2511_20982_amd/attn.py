@@ -20,11 +20,12 @@ LIB_PATH = os.path.join(HERE, "libdopd_attn.so")
 
 DOPD_OK, DOPD_ERR_NULL_POINTER, DOPD_ERR_INVALID_SHAPE = 0, 1, 2
 DOPD_ERR_UNSUPPORTED, DOPD_ERR_WORKSPACE_TOO_SMALL, DOPD_ERR_HIP = 3, 4, 5
-DOPD_BF16, DOPD_FP32 = 0, 1
+DOPD_BF16, DOPD_FP32, DOPD_FP8_E4M3 = 0, 1, 2
 PAGE_SIZE = 16
 
 EXPORTS = (
-    "dopd_prefill_attn", "dopd_prefill_paged_attn", "dopd_kv_write", "dopd_decode_attn", "dopd_decode_workspace_size",
+    "dopd_prefill_attn", "dopd_prefill_paged_attn", "dopd_kv_write", "dopd_kv_write_fp8",
+    "dopd_decode_attn", "dopd_decode_attn_fp8", "dopd_decode_workspace_size",
     "dopd_kv_pack_for_handoff", "dopd_kv_unpack_from_handoff", "dopd_validate_page_table_host",
     "dopd_status_string",
     "dopd_last_hip_error",
@@ -48,8 +49,9 @@ class Shape(C.Structure):
 
 def make_shape(hq: int, hkv: int, d: int, dtype: str = "bf16", scale: float | None = None,
                page_size: int = PAGE_SIZE) -> Shape:
-    """Shape descriptor; the softmax scale defaults to 1/sqrt(d)."""
-    dt = {"bf16": DOPD_BF16, "fp32": DOPD_FP32}[dtype]
+    """Shape descriptor; the softmax scale defaults to 1/sqrt(d).  dtype "fp8"
+    means E4M3 KV pages (bf16 q/out/fresh K/V)."""
+    dt = {"bf16": DOPD_BF16, "fp32": DOPD_FP32, "fp8": DOPD_FP8_E4M3}[dtype]
     return Shape(hq, hkv, d, page_size, dt, 1.0 / math.sqrt(d) if scale is None else scale)
 
 
@@ -69,6 +71,9 @@ def lib():
         L.dopd_prefill_paged_attn.argtypes = [SP, P, P, P, i32, P, i32, P, P, P, P, i32, P, P, P]
         L.dopd_kv_write.argtypes = [SP, P, P, P, P, i32, P, i32, P, P, i32, i32, P]
         L.dopd_decode_attn.argtypes = [SP, P, P, P, i32, P, i32, P, P, i32, i32, P, P, P, sz, P]
+        L.dopd_kv_write_fp8.argtypes = [SP, P, P, P, P, P, P, i32, P, i32, P, P, i32, i32, P]
+        L.dopd_decode_attn_fp8.argtypes = [SP, P, P, P, P, P, i32, P, i32, P, P, i32, i32, P, P,
+                                           P, sz, P]
         L.dopd_decode_workspace_size.argtypes = [SP, P, i32, i32]
         L.dopd_decode_workspace_size.restype = sz
         L.dopd_kv_pack_for_handoff.argtypes = [SP, i32, P, P, i32, P, i32, P, P, P, P, i32, P, P]
@@ -77,7 +82,8 @@ def lib():
         L.dopd_status_string.argtypes = [i32]
         L.dopd_status_string.restype = C.c_char_p
         L.dopd_last_hip_error.restype = i32
-        for f in ("dopd_prefill_attn", "dopd_prefill_paged_attn", "dopd_kv_write", "dopd_decode_attn",
+        for f in ("dopd_prefill_attn", "dopd_prefill_paged_attn", "dopd_kv_write",
+                  "dopd_kv_write_fp8", "dopd_decode_attn", "dopd_decode_attn_fp8",
                   "dopd_kv_pack_for_handoff", "dopd_kv_unpack_from_handoff",
                   "dopd_validate_page_table_host"):
             getattr(L, f).restype = i32
@@ -147,6 +153,16 @@ def dopd_kv_write(shape, k_new, v_new, k_pool, v_pool, num_pages, page_table,
            "dopd_kv_write")
 
 
+def dopd_kv_write_fp8(shape, k_new, v_new, k_scale, v_scale, k_pool, v_pool, num_pages,
+                      page_table, page_table_stride, cu_new_tokens, start_pos, num_reqs,
+                      total_new_tokens, stream=None):
+    _check(lib().dopd_kv_write_fp8(C.byref(shape), _dptr(k_new), _dptr(v_new), _dptr(k_scale),
+                                   _dptr(v_scale), _dptr(k_pool), _dptr(v_pool), int(num_pages),
+                                   _dptr(page_table), int(page_table_stride),
+                                   _dptr(cu_new_tokens), _dptr(start_pos), int(num_reqs),
+                                   int(total_new_tokens), _stream(stream)), "dopd_kv_write_fp8")
+
+
 def dopd_decode_workspace_size(shape, context_lens_host, num_reqs, split_tokens=0) -> int:
     ctx = _host_i32(context_lens_host)
     return int(lib().dopd_decode_workspace_size(C.byref(shape), _hptr(ctx), int(num_reqs),
@@ -164,6 +180,21 @@ def dopd_decode_attn(shape, q, k_pool, v_pool, num_pages, page_table, page_table
                                   _dptr(context_lens), _hptr(ctx), int(num_reqs),
                                   int(split_tokens), _dptr(out), _dptr(lse), _dptr(workspace),
                                   int(workspace_bytes), _stream(stream)), "dopd_decode_attn")
+
+
+def dopd_decode_attn_fp8(shape, q, k_pool, v_pool, k_scale, v_scale, num_pages, page_table,
+                         page_table_stride, context_lens, context_lens_host, num_reqs,
+                         split_tokens, out, lse, workspace, workspace_bytes=None, stream=None):
+    ctx = _host_i32(context_lens_host)
+    if workspace_bytes is None:
+        workspace_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check(lib().dopd_decode_attn_fp8(C.byref(shape), _dptr(q), _dptr(k_pool), _dptr(v_pool),
+                                      _dptr(k_scale), _dptr(v_scale), int(num_pages),
+                                      _dptr(page_table), int(page_table_stride),
+                                      _dptr(context_lens), _hptr(ctx), int(num_reqs),
+                                      int(split_tokens), _dptr(out), _dptr(lse),
+                                      _dptr(workspace), int(workspace_bytes), _stream(stream)),
+           "dopd_decode_attn_fp8")
 
 
 def dopd_kv_pack_for_handoff(shape, num_layers, k_pool, v_pool, num_pages, page_table,

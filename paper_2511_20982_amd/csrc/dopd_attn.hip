@@ -38,8 +38,16 @@ dopd_status check_shape(const dopd_attn_shape* s) {
     return DOPD_ERR_INVALID_SHAPE;
   if (s->head_dim != 64 && s->head_dim != 128) return DOPD_ERR_UNSUPPORTED;
   if (s->page_size != dopd::kPage) return DOPD_ERR_UNSUPPORTED;
-  if (s->dtype != DOPD_BF16 && s->dtype != DOPD_FP32) return DOPD_ERR_UNSUPPORTED;
+  if (s->dtype != DOPD_BF16 && s->dtype != DOPD_FP32 && s->dtype != DOPD_FP8_E4M3)
+    return DOPD_ERR_UNSUPPORTED;
   return DOPD_OK;
+}
+
+// Entry points whose pools hold bf16 or fp32 only.
+dopd_status check_shape_no_fp8(const dopd_attn_shape* s) {
+  const dopd_status st = check_shape(s);
+  if (st != DOPD_OK) return st;
+  return s->dtype == DOPD_FP8_E4M3 ? DOPD_ERR_UNSUPPORTED : DOPD_OK;
 }
 
 
@@ -121,9 +129,63 @@ dopd_status check_decode_host(const dopd_attn_shape* s, const int32_t* ctx_host,
     if (ctx_host[r] < 1) return DOPD_ERR_INVALID_SHAPE;
   if (split < 0 || (split > 0 && split % 32 != 0) || split > kDecMaxSplitTokens)
     return DOPD_ERR_INVALID_SHAPE;
-  if (s->dtype == DOPD_BF16 && s->num_q_heads / s->num_kv_heads > kMaxGroupBf16)
+  if (s->dtype != DOPD_FP32 && s->num_q_heads / s->num_kv_heads > kMaxGroupBf16)
     return DOPD_ERR_UNSUPPORTED;
   return DOPD_OK;
+}
+
+// The bf16-operand decode (bf16 or E4M3 pools) after the host checks: plan
+// the partition, check the workspace, launch the split kernel and, when some
+// (request, KV head) spans two slices, the merge kernel.
+template <bool KV8>
+dopd_status launch_decode_bf16(const dopd_attn_shape* s, const void* q, const void* k_pool,
+                               const void* v_pool, const float* k_scale, const float* v_scale,
+                               const int32_t* pt, int32_t pt_stride, const int32_t* ctx,
+                               const int32_t* ctx_host, int32_t nreq, int32_t split_tokens,
+                               void* out, float* lse, void* workspace, size_t workspace_bytes,
+                               hipStream_t strm) {
+  const int hkv = s->num_kv_heads, hq = s->num_q_heads, d = s->head_dim;
+  const int64_t total = decode_total_units(ctx_host, nreq, hkv);
+  if (total > INT32_MAX / 2) return DOPD_ERR_INVALID_SHAPE;
+  const int64_t nwg = decode_nwg(total, split_tokens);
+  const DecodeLayout L = decode_layout(s, ctx_host, nreq, split_tokens);
+  if (!workspace) return DOPD_ERR_NULL_POINTER;
+  if (workspace_bytes < L.total) return DOPD_ERR_WORKSPACE_TOO_SMALL;
+  if ((reinterpret_cast<uintptr_t>(workspace) & 255) != 0) return DOPD_ERR_INVALID_SHAPE;
+  char* ws = static_cast<char*>(workspace);
+  const bool merge = decode_needs_merge(ctx_host, nreq, hkv, total, nwg);
+  dopd::DecodeArgs a;
+  a.q = (const uint16_t*)q;
+  a.k_pool = k_pool;
+  a.v_pool = v_pool;
+  a.k_scale = k_scale;
+  a.v_scale = v_scale;
+  a.page_table = pt;
+  a.ctx_lens = ctx;
+  a.out = (uint16_t*)out;
+  a.lse = lse;
+  a.part_o = reinterpret_cast<float*>(ws + L.part_o_off);
+  a.part_ml = reinterpret_cast<float*>(ws + L.part_ml_off);
+  a.pt_stride = pt_stride;
+  a.nreq = nreq;
+  a.hq = hq;
+  a.hkv = hkv;
+  a.total_units = (int)total;
+  a.nwg = (int)nwg;
+  a.scale_log2 = s->softmax_scale * dopd::kLog2e;
+  const int64_t items = nwg;
+  const int64_t merge_items = merge ? (int64_t)nreq * hkv : 0;
+  if (d == 64)
+    hipLaunchKernelGGL((dopd::decode_split_kernel<64, KV8>), dim3((unsigned)items), dim3(256), 0, strm, a);
+  else
+    hipLaunchKernelGGL((dopd::decode_split_kernel<128, KV8>), dim3((unsigned)items), dim3(256), 0, strm, a);
+  const dopd_status st = launch_status();
+  if (st != DOPD_OK || merge_items == 0) return st;
+  if (d == 64)
+    hipLaunchKernelGGL(dopd::decode_merge_kernel<64>, dim3((unsigned)merge_items), dim3(256), 0, strm, a);
+  else
+    hipLaunchKernelGGL(dopd::decode_merge_kernel<128>, dim3((unsigned)merge_items), dim3(256), 0, strm, a);
+  return launch_status();
 }
 
 }  // namespace
@@ -135,7 +197,7 @@ const char* dopd_status_string(dopd_status status) {
     case DOPD_OK: return "ok";
     case DOPD_ERR_NULL_POINTER: return "null pointer argument";
     case DOPD_ERR_INVALID_SHAPE: return "invalid shape, count or length";
-    case DOPD_ERR_UNSUPPORTED: return "unsupported dtype, head_dim, page_size or head ratio";
+    case DOPD_ERR_UNSUPPORTED: return "unsupported dtype, head_dim, page_size or head ratio for this entry point";
     case DOPD_ERR_WORKSPACE_TOO_SMALL: return "workspace too small";
     case DOPD_ERR_HIP: return "HIP launch error";
     default: return "unknown status";
@@ -233,7 +295,7 @@ dopd::PrefillArgs prefill_args(const dopd_attn_shape* s, const void* q, void* ou
 dopd_status dopd_prefill_attn(const dopd_attn_shape* s, const void* q, const void* k,
                               const void* v, void* out, float* lse, const int32_t* cu,
                               const int32_t* cu_host, int32_t nreq, void* stream) {
-  dopd_status st = check_shape(s);
+  dopd_status st = check_shape_no_fp8(s);
   if (st != DOPD_OK) return st;
   if (nreq < 0) return DOPD_ERR_INVALID_SHAPE;
   if (nreq == 0) return DOPD_OK;
@@ -269,7 +331,7 @@ dopd_status dopd_prefill_paged_attn(const dopd_attn_shape* s, const void* q, con
                                     const int32_t* cu, const int32_t* cu_host,
                                     const int32_t* prefix, const int32_t* prefix_host,
                                     int32_t nreq, void* out, float* lse, void* stream) {
-  dopd_status st = check_shape(s);
+  dopd_status st = check_shape_no_fp8(s);
   if (st != DOPD_OK) return st;
   if (nreq < 0 || num_pages < 0 || pt_stride < 0) return DOPD_ERR_INVALID_SHAPE;
   if (nreq == 0) return DOPD_OK;
@@ -314,7 +376,7 @@ dopd_status dopd_kv_write(const dopd_attn_shape* s, const void* k_new, const voi
                           void* k_pool, void* v_pool, int32_t num_pages, const int32_t* pt,
                           int32_t pt_stride, const int32_t* cu_new, const int32_t* start_pos,
                           int32_t nreq, int32_t total_new, void* stream) {
-  dopd_status st = check_shape(s);
+  dopd_status st = check_shape_no_fp8(s);
   if (st != DOPD_OK) return st;
   if (nreq < 0 || total_new < 0 || num_pages < 0 || pt_stride < 0) return DOPD_ERR_INVALID_SHAPE;
   if (nreq == 0 || total_new == 0) return DOPD_OK;
@@ -348,11 +410,42 @@ dopd_status dopd_kv_write(const dopd_attn_shape* s, const void* k_new, const voi
   return launch_status();
 }
 
+dopd_status dopd_kv_write_fp8(const dopd_attn_shape* s, const void* k_new, const void* v_new,
+                              const float* k_scale, const float* v_scale, void* k_pool,
+                              void* v_pool, int32_t num_pages, const int32_t* pt,
+                              int32_t pt_stride, const int32_t* cu_new, const int32_t* start_pos,
+                              int32_t nreq, int32_t total_new, void* stream) {
+  dopd_status st = check_shape(s);
+  if (st != DOPD_OK) return st;
+  if (s->dtype != DOPD_FP8_E4M3) return DOPD_ERR_UNSUPPORTED;
+  if (nreq < 0 || total_new < 0 || num_pages < 0 || pt_stride < 0) return DOPD_ERR_INVALID_SHAPE;
+  if (nreq == 0 || total_new == 0) return DOPD_OK;
+  if (!k_new || !v_new || !k_scale || !v_scale || !k_pool || !v_pool || !pt || !cu_new ||
+      !start_pos)
+    return DOPD_ERR_NULL_POINTER;
+  const int64_t blocks = (int64_t)total_new / dopd::kPage + 2 * (int64_t)nreq + 1;
+  if (blocks > INT32_MAX || s->num_kv_heads > 65535) return DOPD_ERR_INVALID_SHAPE;
+  hipStream_t strm = as_stream(stream);
+  const int hkv = s->num_kv_heads;
+  const dim3 grid((unsigned)blocks, (unsigned)hkv), block(dopd::kKvwThreads);
+  auto* kn = (const uint16_t*)k_new;
+  auto* vn = (const uint16_t*)v_new;
+  auto* kp = (uint8_t*)k_pool;
+  auto* vp = (uint8_t*)v_pool;
+  if (s->head_dim == 64)
+    hipLaunchKernelGGL(dopd::kv_write_e4m3_kernel<64>, grid, block, 0, strm, kn, vn, k_scale,
+                       v_scale, kp, vp, pt, pt_stride, cu_new, start_pos, nreq, hkv);
+  else
+    hipLaunchKernelGGL(dopd::kv_write_e4m3_kernel<128>, grid, block, 0, strm, kn, vn, k_scale,
+                       v_scale, kp, vp, pt, pt_stride, cu_new, start_pos, nreq, hkv);
+  return launch_status();
+}
+
 // ---------------------------------------------------------------- decode
 size_t dopd_decode_workspace_size(const dopd_attn_shape* s, const int32_t* ctx_host, int32_t n,
                                   int32_t split_tokens) {
   if (check_decode_host(s, ctx_host, n, split_tokens) != DOPD_OK) return 0;
-  if (n == 0 || s->dtype != DOPD_BF16) return 256;
+  if (n == 0 || s->dtype == DOPD_FP32) return 256;
   return decode_layout(s, ctx_host, n, split_tokens).total;
 }
 
@@ -363,6 +456,7 @@ dopd_status dopd_decode_attn(const dopd_attn_shape* s, const void* q, const void
                              void* workspace, size_t workspace_bytes, void* stream) {
   dopd_status st = check_decode_host(s, ctx_host, nreq, split_tokens);
   if (st != DOPD_OK) return st;
+  if (s->dtype == DOPD_FP8_E4M3) return DOPD_ERR_UNSUPPORTED;  // dopd_decode_attn_fp8
   if (num_pages < 0 || pt_stride < 0) return DOPD_ERR_INVALID_SHAPE;
   if (nreq == 0) return DOPD_OK;
   if (!q || !k_pool || !v_pool || !pt || !ctx || !out) return DOPD_ERR_NULL_POINTER;
@@ -383,45 +477,30 @@ dopd_status dopd_decode_attn(const dopd_attn_shape* s, const void* q, const void
                          s->softmax_scale, (float*)out, lse);
     return launch_status();
   }
-  const int64_t total = decode_total_units(ctx_host, nreq, hkv);
-  if (total > INT32_MAX / 2) return DOPD_ERR_INVALID_SHAPE;
-  const int64_t nwg = decode_nwg(total, split_tokens);
-  const DecodeLayout L = decode_layout(s, ctx_host, nreq, split_tokens);
-  if (!workspace) return DOPD_ERR_NULL_POINTER;
-  if (workspace_bytes < L.total) return DOPD_ERR_WORKSPACE_TOO_SMALL;
-  if ((reinterpret_cast<uintptr_t>(workspace) & 255) != 0) return DOPD_ERR_INVALID_SHAPE;
-  char* ws = static_cast<char*>(workspace);
-  const bool merge = decode_needs_merge(ctx_host, nreq, hkv, total, nwg);
-  dopd::DecodeArgs a;
-  a.q = (const uint16_t*)q;
-  a.k_pool = (const uint16_t*)k_pool;
-  a.v_pool = (const uint16_t*)v_pool;
-  a.page_table = pt;
-  a.ctx_lens = ctx;
-  a.out = (uint16_t*)out;
-  a.lse = lse;
-  a.part_o = reinterpret_cast<float*>(ws + L.part_o_off);
-  a.part_ml = reinterpret_cast<float*>(ws + L.part_ml_off);
-  a.pt_stride = pt_stride;
-  a.nreq = nreq;
-  a.hq = hq;
-  a.hkv = hkv;
-  a.total_units = (int)total;
-  a.nwg = (int)nwg;
-  a.scale_log2 = s->softmax_scale * dopd::kLog2e;
-  const int64_t items = nwg;
-  const int64_t merge_items = merge ? (int64_t)nreq * hkv : 0;
-  if (d == 64)
-    hipLaunchKernelGGL(dopd::decode_split_kernel<64>, dim3((unsigned)items), dim3(256), 0, strm, a);
-  else
-    hipLaunchKernelGGL(dopd::decode_split_kernel<128>, dim3((unsigned)items), dim3(256), 0, strm, a);
-  st = launch_status();
-  if (st != DOPD_OK || merge_items == 0) return st;
-  if (d == 64)
-    hipLaunchKernelGGL(dopd::decode_merge_kernel<64>, dim3((unsigned)merge_items), dim3(256), 0, strm, a);
-  else
-    hipLaunchKernelGGL(dopd::decode_merge_kernel<128>, dim3((unsigned)merge_items), dim3(256), 0, strm, a);
-  return launch_status();
+  return launch_decode_bf16<false>(s, q, k_pool, v_pool, nullptr, nullptr, pt, pt_stride, ctx,
+                                   ctx_host, nreq, split_tokens, out, lse, workspace,
+                                   workspace_bytes, strm);
+}
+
+dopd_status dopd_decode_attn_fp8(const dopd_attn_shape* s, const void* q, const void* k_pool,
+                                 const void* v_pool, const float* k_scale, const float* v_scale,
+                                 int32_t num_pages, const int32_t* pt, int32_t pt_stride,
+                                 const int32_t* ctx, const int32_t* ctx_host, int32_t nreq,
+                                 int32_t split_tokens, void* out, float* lse, void* workspace,
+                                 size_t workspace_bytes, void* stream) {
+  dopd_status st = check_decode_host(s, ctx_host, nreq, split_tokens);
+  if (st != DOPD_OK) return st;
+  if (s->dtype != DOPD_FP8_E4M3) return DOPD_ERR_UNSUPPORTED;
+  if (num_pages < 0 || pt_stride < 0) return DOPD_ERR_INVALID_SHAPE;
+  if (nreq == 0) return DOPD_OK;
+  if (!q || !k_pool || !v_pool || !k_scale || !v_scale || !pt || !ctx || !out)
+    return DOPD_ERR_NULL_POINTER;
+  for (int32_t r = 0; r < nreq; ++r)
+    if ((int64_t)(ctx_host[r] + dopd::kPage - 1) / dopd::kPage > pt_stride)
+      return DOPD_ERR_INVALID_SHAPE;
+  return launch_decode_bf16<true>(s, q, k_pool, v_pool, k_scale, v_scale, pt, pt_stride, ctx,
+                                  ctx_host, nreq, split_tokens, out, lse, workspace,
+                                  workspace_bytes, as_stream(stream));
 }
 
 // ---------------------------------------------------------------- handoff pack
@@ -451,7 +530,11 @@ dopd_status dopd_kv_pack_for_handoff(const dopd_attn_shape* s, int32_t num_layer
   dim3 grid((unsigned)((max_len + dopd::kPage - 1) / dopd::kPage), (unsigned)num_handoff,
             (unsigned)zdim);
   hipStream_t strm = as_stream(stream);
-  if (s->dtype == DOPD_BF16)
+  if (s->dtype == DOPD_FP8_E4M3)
+    hipLaunchKernelGGL(dopd::kv_pack_kernel<uint8_t>, grid, dim3(256), 0, strm,
+                       (const uint8_t*)k_pool, (const uint8_t*)v_pool, num_pages, pt, pt_stride,
+                       req_ids, seq_lens, out_offsets, s->num_kv_heads, s->head_dim, (uint8_t*)out);
+  else if (s->dtype == DOPD_BF16)
     hipLaunchKernelGGL(dopd::kv_pack_kernel<uint16_t>, grid, dim3(256), 0, strm,
                        (const uint16_t*)k_pool, (const uint16_t*)v_pool, num_pages, pt, pt_stride,
                        req_ids, seq_lens, out_offsets, s->num_kv_heads, s->head_dim, (uint16_t*)out);
@@ -490,7 +573,16 @@ dopd_status dopd_kv_unpack_from_handoff(const dopd_attn_shape* s, int32_t num_la
             (unsigned)zdim);
   hipStream_t strm = as_stream(stream);
   const int hkv = s->num_kv_heads;
-  if (s->dtype == DOPD_BF16) {
+  if (s->dtype == DOPD_FP8_E4M3) {
+    auto* src = (const uint8_t*)in;
+    auto* kp = (uint8_t*)k_pool; auto* vp = (uint8_t*)v_pool;
+    if (s->head_dim == 64)
+      hipLaunchKernelGGL((dopd::kv_unpack_kernel<uint8_t, 64>), grid, dim3(256), 0, strm, src,
+                         in_offsets, req_ids, seq_lens, kp, vp, num_pages, pt, pt_stride, hkv);
+    else
+      hipLaunchKernelGGL((dopd::kv_unpack_kernel<uint8_t, 128>), grid, dim3(256), 0, strm, src,
+                         in_offsets, req_ids, seq_lens, kp, vp, num_pages, pt, pt_stride, hkv);
+  } else if (s->dtype == DOPD_BF16) {
     auto* src = (const uint16_t*)in;
     auto* kp = (uint16_t*)k_pool; auto* vp = (uint16_t*)v_pool;
     if (s->head_dim == 64)

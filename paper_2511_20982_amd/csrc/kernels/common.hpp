@@ -6,6 +6,7 @@
 namespace dopd {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef short s16x4 __attribute__((ext_vector_type(4)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
@@ -28,6 +29,29 @@ __device__ __forceinline__ uint32_t f32_to_bf16_bits(float f) {
 
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
   return f32_to_bf16_bits(lo) | (f32_to_bf16_bits(hi) << 16);
+}
+
+// ---- OCP E4M3 (1 sign, 4 exponent bits with bias 7, 3 mantissa bits; no
+// infinities; largest finite 448) KV-page codes.
+// Saturates to [-448, 448] before the conversion (a NaN stays NaN), so the
+// hardware conversion only ever rounds (to nearest even) inside the range.
+__device__ __forceinline__ float e4m3_saturate(float y) {
+  return y > 448.f ? 448.f : (y < -448.f ? -448.f : y);
+}
+
+// Four fp32 values -> four E4M3 codes, byte i holding value i.
+__device__ __forceinline__ uint32_t e4m3x4_from_f32(float a, float b, float c, float d) {
+  int w = __builtin_amdgcn_cvt_pk_fp8_f32(e4m3_saturate(a), e4m3_saturate(b), 0, false);
+  w = __builtin_amdgcn_cvt_pk_fp8_f32(e4m3_saturate(c), e4m3_saturate(d), w, true);
+  return (uint32_t)w;
+}
+
+// Four E4M3 codes (byte i = element i) -> four bf16 as two packed pairs.
+// Exact: every E4M3 value is a bf16 value.
+__device__ __forceinline__ u32x2 bf16x4_from_e4m3x4(uint32_t w) {
+  const bf16x2 lo = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8((int)w, 1.0f, false);
+  const bf16x2 hi = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8((int)w, 1.0f, true);
+  return u32x2{__builtin_bit_cast(uint32_t, lo), __builtin_bit_cast(uint32_t, hi)};
 }
 
 __device__ __forceinline__ int lane_id() { return __lane_id(); }

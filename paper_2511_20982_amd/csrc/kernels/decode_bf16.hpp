@@ -37,15 +37,26 @@
 // partition beyond rounding.  The kernel boundary orders the partial writes
 // before the merge reads; no in-kernel fence or counter is needed (a
 // device-scope fence costs a whole-L2 writeback and invalidate on this part).
+//
+// KV8 = true reads pages of E4M3 codes (one byte per element, same layouts)
+// with one scale per KV head: the MFMA operands are the codes widened to
+// bf16 (exact), the K scale is folded into the softmax scale and the V scale
+// into the output.  Each K lane reads a 32-byte run and each V lane 8 bytes;
+// the loaded bytes are converted just before their MFMAs, so the buffers in
+// flight stay raw.
 #pragma once
+#include <type_traits>
+
 #include "common.hpp"
 
 namespace dopd {
 
 struct DecodeArgs {
   const uint16_t* q;          // [B][Hq][D]
-  const uint16_t* k_pool;     // [P][Hkv][16][D]
-  const uint16_t* v_pool;     // [P][Hkv][D][16]
+  const void* k_pool;         // [P][Hkv][16][D] bf16 or E4M3
+  const void* v_pool;         // [P][Hkv][D][16] bf16 or E4M3
+  const float* k_scale;       // [Hkv], E4M3 pools only
+  const float* v_scale;       // [Hkv], E4M3 pools only
   const int32_t* page_table;  // [B][pt_stride]
   const int32_t* ctx_lens;    // [B]
   uint16_t* out;              // [B][Hq][D]
@@ -75,14 +86,32 @@ __device__ __forceinline__ int dec_slice_of(const DecodeArgs& a, int x) {
   return b;
 }
 
-template <int D>
+template <int D, bool KV8>
 struct DecodePairBuf {
   u32x4 k1[D / 32], k2[D / 32];  // K rows of the two QK MFMAs
   u32x4 v[D / 16];               // V^T rows, one per 16-dim tile
 };
-
 template <int D>
+struct DecodePairBuf<D, true> {  // raw E4M3 codes
+  u32x4 k1[D / 64], k2[D / 64];
+  u32x2 v[D / 16];
+};
+
+// bf16 MFMA operand i of a lane's K run (dims 8i .. 8i+7 of the run).
+template <bool KV8, class KArr>
+__device__ __forceinline__ bf16x8 dec_k_operand(const KArr& k, int i) {
+  if constexpr (KV8) {
+    const u32x4 w = k[i >> 1];
+    const u32x2 lo = bf16x4_from_e4m3x4(w[2 * (i & 1)]), hi = bf16x4_from_e4m3x4(w[2 * (i & 1) + 1]);
+    return __builtin_bit_cast(bf16x8, u32x4{lo[0], lo[1], hi[0], hi[1]});
+  } else {
+    return __builtin_bit_cast(bf16x8, k[i]);
+  }
+}
+
+template <int D, bool KV8>
 __global__ __launch_bounds__(256, 2) void decode_split_kernel(DecodeArgs a) {
+  using KT = std::conditional_t<KV8, uint8_t, uint16_t>;
   constexpr int NQK = D / 32;  // QK MFMAs (k = 32) per 16-token row block
   constexpr int NT = D / 16;   // O^T tiles of 16 dims
   constexpr int SPAN = D / 4;  // contiguous dims of a K row read by one lane
@@ -144,9 +173,12 @@ __global__ __launch_bounds__(256, 2) void decode_split_kernel(DecodeArgs a) {
 #pragma unroll
     for (int n = 0; n < NT; ++n) oacc[n] = f32x4{0.f, 0.f, 0.f, 0.f};
     float m_run = -INFINITY, l_run = 0.f;
+    // E4M3 pools: k = code * k_scale[c] scales every score, v = code * v_scale[c] the output.
+    const float sl2 = KV8 ? a.scale_log2 * a.k_scale[c] : a.scale_log2;
 
-    const uint16_t* kbase = a.k_pool + (int64_t)c * kPage * D + SPAN * qg;
-    const uint16_t* vbase = a.v_pool + (int64_t)c * D * kPage + (int64_t)hl * kPage + 8 * (qg & 1);
+    const KT* kbase = static_cast<const KT*>(a.k_pool) + (int64_t)c * kPage * D + SPAN * qg;
+    const KT* vbase = static_cast<const KT*>(a.v_pool) + (int64_t)c * D * kPage + (int64_t)hl * kPage +
+                      8 * (qg & 1);
 
     // Chunks of up to 128 pairs: lane j of a wave holds the page id of page
     // (j & 1) of the wave's pair j/2 of the chunk.
@@ -163,7 +195,7 @@ __global__ __launch_bounds__(256, 2) void decode_split_kernel(DecodeArgs a) {
         if (pg < npages) pid = pt[pg];
       }
 
-    auto load_pair = [&](DecodePairBuf<D>& buf, int k) {
+    auto load_pair = [&](DecodePairBuf<D, KV8>& buf, int k) {
       const int pair = w + kDecWaves * k;
       const int pageA = __shfl(pid, 2 * k, 64);
       const int pageB = __shfl(pid, 2 * k + 1, 64);
@@ -173,32 +205,38 @@ __global__ __launch_bounds__(256, 2) void decode_split_kernel(DecodeArgs a) {
                                      : (int64_t)pageA * page_elems;
       const int64_t a2 = tq2 < valid ? (int64_t)(tq2 < kPage ? pageA : pageB) * page_elems + (tq2 & 15) * D
                                      : (int64_t)pageA * page_elems;
+      constexpr int KEL = 16 / sizeof(KT);  // elements per 16-byte load
   #pragma unroll
-      for (int i = 0; i < NQK; ++i) {
-        buf.k1[i] = *reinterpret_cast<const u32x4*>(kbase + a1 + 8 * i);
-        buf.k2[i] = *reinterpret_cast<const u32x4*>(kbase + a2 + 8 * i);
+      for (int i = 0; i < SPAN / KEL; ++i) {
+        buf.k1[i] = *reinterpret_cast<const u32x4*>(kbase + a1 + KEL * i);
+        buf.k2[i] = *reinterpret_cast<const u32x4*>(kbase + a2 + KEL * i);
       }
       const int pv = (qg < 2 || valid <= kPage) ? pageA : pageB;
-      const uint16_t* p = vbase + (int64_t)pv * page_elems;
+      const KT* p = vbase + (int64_t)pv * page_elems;
   #pragma unroll
-      for (int n = 0; n < NT; ++n) buf.v[n] = *reinterpret_cast<const u32x4*>(p + (int64_t)(16 * n) * kPage);
+      for (int n = 0; n < NT; ++n) {
+        if constexpr (KV8)
+          buf.v[n] = *reinterpret_cast<const u32x2*>(p + (int64_t)(16 * n) * kPage);
+        else
+          buf.v[n] = *reinterpret_cast<const u32x4*>(p + (int64_t)(16 * n) * kPage);
+      }
     };
 
-    auto compute_pair = [&](DecodePairBuf<D>& buf, int k) {
+    auto compute_pair = [&](DecodePairBuf<D, KV8>& buf, int k) {
       const int pair = w + kDecWaves * k;
       const int valid = min(32, ntok - 32 * pair);
       f32x4 s1 = {0.f, 0.f, 0.f, 0.f}, s2 = {0.f, 0.f, 0.f, 0.f};
   #pragma unroll
       for (int i = 0; i < NQK; ++i) {
-        s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, buf.k1[i]), qop[i], s1, 0, 0, 0);
-        s2 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, buf.k2[i]), qop[i], s2, 0, 0, 0);
+        s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(dec_k_operand<KV8>(buf.k1, i), qop[i], s1, 0, 0, 0);
+        s2 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(dec_k_operand<KV8>(buf.k2, i), qop[i], s2, 0, 0, 0);
       }
       // lane holds head hl, pair tokens 8qg + 0..3 (s1) and 8qg + 4..7 (s2)
       float x[8];
   #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        x[j] = s1[j] * a.scale_log2;
-        x[4 + j] = s2[j] * a.scale_log2;
+        x[j] = s1[j] * sl2;
+        x[4 + j] = s2[j] * sl2;
       }
       if (valid < 32) {  // last pair of a ragged split: mask dead tokens, zero dead V slots
   #pragma unroll
@@ -206,12 +244,22 @@ __global__ __launch_bounds__(256, 2) void decode_split_kernel(DecodeArgs a) {
           if (8 * qg + j >= valid) x[j] = -INFINITY;
         const int nv = valid - 8 * qg;  // live slots among this lane's 8
   #pragma unroll
-        for (int n = 0; n < NT; ++n)
+        for (int n = 0; n < NT; ++n) {
+          if constexpr (KV8) {
   #pragma unroll
-          for (int wd = 0; wd < 4; ++wd) {
-            const uint32_t keep = (2 * wd + 1 < nv) ? 0xffffffffu : (2 * wd < nv ? 0x0000ffffu : 0u);
-            buf.v[n][wd] &= keep;
+            for (int wd = 0; wd < 2; ++wd) {  // one byte per slot
+              const int live = min(4, max(0, nv - 4 * wd));
+              const uint32_t keep = live >= 4 ? 0xffffffffu : ((1u << (8 * live)) - 1u);
+              buf.v[n][wd] &= keep;
+            }
+          } else {
+  #pragma unroll
+            for (int wd = 0; wd < 4; ++wd) {
+              const uint32_t keep = (2 * wd + 1 < nv) ? 0xffffffffu : (2 * wd < nv ? 0x0000ffffu : 0u);
+              buf.v[n][wd] &= keep;
+            }
           }
+        }
       }
       float mx = fmaxf(fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3])),
                        fmaxf(fmaxf(x[4], x[5]), fmaxf(x[6], x[7])));
@@ -232,7 +280,14 @@ __global__ __launch_bounds__(256, 2) void decode_split_kernel(DecodeArgs a) {
   #pragma unroll
       for (int n = 0; n < NT; ++n) {
         oacc[n] *= alpha;
-        oacc[n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, buf.v[n]), pb, oacc[n], 0, 0, 0);
+        bf16x8 vop;
+        if constexpr (KV8) {
+          const u32x2 lo = bf16x4_from_e4m3x4(buf.v[n][0]), hi = bf16x4_from_e4m3x4(buf.v[n][1]);
+          vop = __builtin_bit_cast(bf16x8, u32x4{lo[0], lo[1], hi[0], hi[1]});
+        } else {
+          vop = __builtin_bit_cast(bf16x8, buf.v[n]);
+        }
+        oacc[n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vop, pb, oacc[n], 0, 0, 0);
       }
     };
 
@@ -241,7 +296,7 @@ __global__ __launch_bounds__(256, 2) void decode_split_kernel(DecodeArgs a) {
         // the last pair, an L2 hit) so the compiler can wait for exactly the
         // buffer being computed while the other one is in flight.
         const int last = my_pairs - 1;
-        DecodePairBuf<D> b0, b1;
+        DecodePairBuf<D, KV8> b0, b1;
         load_pair(b0, 0);
         for (int k = 0; k < my_pairs; k += 2) {
           load_pair(b1, min(k + 1, last));
@@ -281,12 +336,13 @@ __global__ __launch_bounds__(256, 2) void decode_split_kernel(DecodeArgs a) {
         sc[i] = __builtin_amdgcn_exp2f(mw[i] - M);  // a wave without pairs has m = -inf -> 0
         L += sc[i] * lw[i];
       }
+      const float vsc = KV8 ? a.v_scale[c] : 1.f;
 #pragma unroll
       for (int n = 0; n < NT; ++n) {
         f32x4 o = oacc[n] * sc[0];
 #pragma unroll
         for (int i = 1; i < kDecWaves; ++i) o += s_o[i - 1][n][l] * sc[i];
-        oacc[n] = o;
+        oacc[n] = KV8 ? o * vsc : o;
       }
       const int head = c * g + hl;
       if (hl < g) {

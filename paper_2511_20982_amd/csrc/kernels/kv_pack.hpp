@@ -7,7 +7,7 @@
 
 namespace dopd {
 
-template <typename T>
+template <typename T>  // uint8_t (E4M3 codes), uint16_t (bf16) or uint32_t (fp32) elements
 __global__ __launch_bounds__(256) void kv_pack_kernel(
     const T* __restrict__ k_pool, const T* __restrict__ v_pool, int num_pages,
     const int32_t* __restrict__ page_table, int pt_stride, const int32_t* __restrict__ req_ids,
@@ -53,7 +53,12 @@ __global__ __launch_bounds__(256) void kv_pack_kernel(
       u32x4 x;
 #pragma unroll
       for (int w = 0; w < 4; ++w) {
-        if constexpr (sizeof(T) == 2)
+        if constexpr (sizeof(T) == 1)
+          x[w] = (uint32_t)sv[(e0 + 4 * w) * kPage + t] |
+                 ((uint32_t)sv[(e0 + 4 * w + 1) * kPage + t] << 8) |
+                 ((uint32_t)sv[(e0 + 4 * w + 2) * kPage + t] << 16) |
+                 ((uint32_t)sv[(e0 + 4 * w + 3) * kPage + t] << 24);
+        else if constexpr (sizeof(T) == 2)
           x[w] = (uint32_t)sv[(e0 + 2 * w) * kPage + t] |
                  ((uint32_t)sv[(e0 + 2 * w + 1) * kPage + t] << 16);
         else

@@ -59,7 +59,11 @@ __global__ __launch_bounds__(256) void kv_unpack_kernel(
       u32x4 x;
 #pragma unroll
       for (int w = 0; w < 4; ++w) {
-        if constexpr (sizeof(T) == 2) {
+        if constexpr (sizeof(T) == 1) {
+          const int s = run * kEl + 4 * w;
+          x[w] = (uint32_t)s_v[s * TP + e] | ((uint32_t)s_v[(s + 1) * TP + e] << 8) |
+                 ((uint32_t)s_v[(s + 2) * TP + e] << 16) | ((uint32_t)s_v[(s + 3) * TP + e] << 24);
+        } else if constexpr (sizeof(T) == 2) {
           const int s = run * kEl + 2 * w;
           x[w] = (uint32_t)s_v[s * TP + e] | ((uint32_t)s_v[(s + 1) * TP + e] << 16);
         } else {

@@ -28,17 +28,17 @@ def guarded(shape, dtype: torch.dtype, margin: int = 4096):
     """Tensor of `shape` inside a buffer whose margins hold a canary pattern."""
     n = int(np.prod(shape))
     esz = torch.tensor([], dtype=dtype).element_size()
-    words = (n * esz + 2 * margin) // 2
+    words = (n * esz + 1) // 2 + margin  # margin bytes on either side
     buf = torch.full((words,), CANARY, dtype=torch.int16, device=DEV)
-    body = buf[margin // 2: margin // 2 + n * esz // 2].view(dtype).view(*shape)
+    body = buf.view(torch.uint8)[margin: margin + n * esz].view(dtype).view(*shape)
     return body, buf, margin
 
 
 def canary_intact(buf, margin, nbytes) -> bool:
-    h = buf.cpu().numpy().view(np.uint16)
-    lo = h[: margin // 2]
-    hi = h[margin // 2 + nbytes // 2:]
-    return bool(np.all(lo == CANARY) and np.all(hi == CANARY))
+    h = buf.cpu().numpy().view(np.uint8)
+    lo = h[:margin]
+    hi = h[margin + nbytes: margin + nbytes + margin - 1]
+    return bool(np.all(lo == 0x5A) and np.all(hi == 0x5A))
 
 
 def assert_attention_close(gpu: np.ndarray, ref: np.ndarray, dtype: str, what: str = ""):
@@ -119,7 +119,8 @@ def gpu_decode(shape, q, k_pool, v_pool, page_table, ctx, split=0, with_lse=True
 
 def gpu_pack(shape, k_pool, v_pool, num_layers, page_table, req_ids, seq_lens, offsets):
     total = int(offsets[-1])
-    dt = torch.bfloat16 if k_pool.dtype == np.uint16 else torch.float32
+    dt = {np.dtype(np.uint16): torch.bfloat16, np.dtype(np.float32): torch.float32,
+          np.dtype(np.uint8): torch.uint8}[k_pool.dtype]
     out, obuf, margin = guarded((total,), dt)
     kp, vp = A.to_device(k_pool), A.to_device(v_pool)
     num_pages = k_pool.shape[-4]
@@ -129,3 +130,56 @@ def gpu_pack(shape, k_pool, v_pool, num_layers, page_table, req_ids, seq_lens, o
     torch.cuda.synchronize()
     assert canary_intact(obuf, margin, out.numel() * out.element_size()), "pack wrote out of bounds"
     return A.to_host(out)
+
+
+# ------------------------------------------------------------------ E4M3 KV pages
+def quantize_pools(k_pool, v_pool, k_scale, v_scale):
+    """bf16 pools -> E4M3 code pools (uint8, same layouts), by the oracle's
+    quantiser: the inputs of the fp8 decode tests."""
+    import oracle
+    p, hkv, _, d = k_pool.shape
+    kq = oracle.e4m3_quantize(k_pool.transpose(0, 2, 1, 3).reshape(-1, hkv, d), k_scale)
+    vq = oracle.e4m3_quantize(v_pool.transpose(0, 3, 1, 2).reshape(-1, hkv, d), v_scale)
+    kq = kq.reshape(p, 16, hkv, d).transpose(0, 2, 1, 3).copy()
+    vq = vq.reshape(p, 16, hkv, d).transpose(0, 2, 3, 1).copy()
+    return kq, vq
+
+
+def gpu_kv_write_fp8(shape, k_new, v_new, k_scale, v_scale, k_pool, v_pool, page_table, cu_new,
+                     start_pos):
+    kp, vp = A.to_device(k_pool), A.to_device(v_pool)
+    A.dopd_kv_write_fp8(shape, A.to_device(k_new), A.to_device(v_new), A.to_device(k_scale),
+                        A.to_device(v_scale), kp, vp, k_pool.shape[0], A.to_device(page_table),
+                        page_table.shape[1], A.to_device(cu_new), A.to_device(start_pos),
+                        len(cu_new) - 1, int(cu_new[-1]))
+    torch.cuda.synchronize()
+    return A.to_host(kp), A.to_host(vp)
+
+
+def gpu_decode_fp8(shape, q, k_pool, v_pool, k_scale, v_scale, page_table, ctx, split=0,
+                   with_lse=True, pools_dev=None):
+    if pools_dev is None:
+        pools_dev = (A.to_device(k_pool), A.to_device(v_pool))
+    kp, vp = pools_dev
+    qd = A.to_device(q)
+    out, obuf, margin = guarded(qd.shape, qd.dtype)
+    lse = torch.full((q.shape[0], q.shape[1]), float("nan"), device=DEV) if with_lse else None
+    ws = A.decode_workspace(shape, ctx, len(ctx), split)
+    A.dopd_decode_attn_fp8(shape, qd, kp, vp, A.to_device(np.asarray(k_scale, np.float32)),
+                           A.to_device(np.asarray(v_scale, np.float32)), kp.shape[0],
+                           A.to_device(page_table), page_table.shape[1], A.to_device(ctx), ctx,
+                           len(ctx), split, out, lse, ws)
+    torch.cuda.synchronize()
+    assert canary_intact(obuf, margin, out.numel() * out.element_size()), \
+        "fp8 decode wrote out of bounds"
+    return widen(A.to_host(out)), (lse.cpu().numpy().astype(np.float64) if with_lse else None)
+
+
+def gpu_unpack(shape, buf, offs, req, lens, k_pool, v_pool, layers, pt):
+    kp, vp = A.to_device(k_pool), A.to_device(v_pool)
+    num_pages = k_pool.shape[-4]
+    A.dopd_kv_unpack_from_handoff(shape, layers, A.to_device(buf), A.to_device(offs),
+                                  A.to_device(req), A.to_device(lens), lens, len(req), kp, vp,
+                                  num_pages, A.to_device(pt), pt.shape[1])
+    torch.cuda.synchronize()
+    return A.to_host(kp), A.to_host(vp)

@@ -161,3 +161,41 @@ def test_prefill_paged_host_validation(lib):
     assert pp(C.byref(s), p, p, p, 100, p, 64, p, H(cu), p, None, 2, p, None, None) == \
         A.DOPD_ERR_NULL_POINTER
     assert pp(C.byref(s), p, p, p, 100, p, 64, p, H(cu), p, H(pre), 0, p, None, None) == A.DOPD_OK
+
+
+def _decode_fp8(lib, shape, ctx, scales=FAKE, ws=FAKE, ws_bytes=1 << 30):
+    ctx = np.asarray(ctx, np.int32)
+    p = C.c_void_p(FAKE)
+    sc = C.c_void_p(scales) if scales else None
+    return lib.dopd_decode_attn_fp8(C.byref(shape), p, p, p, sc, sc, 10, p, 1024, p,
+                                    A._hptr(ctx), len(ctx), 0, p, None,
+                                    C.c_void_p(ws) if ws else None, ws_bytes, None)
+
+
+def test_fp8_host_validation(lib):
+    f8, b16 = _shape(dtype="fp8"), _shape()
+    p = C.c_void_p(FAKE)
+    # E4M3 pools only through the entry points that take scales, and the byte copies.
+    assert _decode(lib, f8, [5]) == A.DOPD_ERR_UNSUPPORTED
+    assert _prefill(lib, f8, [0, 4]) == A.DOPD_ERR_UNSUPPORTED
+    assert lib.dopd_kv_write(C.byref(f8), p, p, p, p, 10, p, 4, p, p, 1, 5, None) == \
+        A.DOPD_ERR_UNSUPPORTED
+    assert _decode_fp8(lib, b16, [5]) == A.DOPD_ERR_UNSUPPORTED
+    assert _decode_fp8(lib, f8, [5, 0]) == A.DOPD_ERR_INVALID_SHAPE
+    assert _decode_fp8(lib, f8, [5], scales=0) == A.DOPD_ERR_NULL_POINTER
+    assert _decode_fp8(lib, f8, [5], ws=0) == A.DOPD_ERR_NULL_POINTER
+    assert _decode_fp8(lib, f8, [3000, 17], ws_bytes=256) == A.DOPD_ERR_WORKSPACE_TOO_SMALL
+    assert _decode_fp8(lib, _shape(hq=34, hkv=2, dtype="fp8"), [5]) == A.DOPD_ERR_UNSUPPORTED
+    # Same partition, same workspace as the bf16 cache.
+    ctx = [3000, 17, 900]
+    assert A.dopd_decode_workspace_size(f8, ctx, 3) == A.dopd_decode_workspace_size(b16, ctx, 3)
+    w8 = lib.dopd_kv_write_fp8
+    assert w8(C.byref(b16), p, p, p, p, p, p, 10, p, 4, p, p, 1, 5, None) == A.DOPD_ERR_UNSUPPORTED
+    assert w8(C.byref(f8), p, p, None, p, p, p, 10, p, 4, p, p, 1, 5, None) == \
+        A.DOPD_ERR_NULL_POINTER
+    assert w8(C.byref(f8), p, p, p, p, p, p, 10, p, 4, p, p, -1, 5, None) == \
+        A.DOPD_ERR_INVALID_SHAPE
+    assert w8(C.byref(f8), p, p, p, p, p, p, 10, p, 4, p, p, 1, 0, None) == A.DOPD_OK
+    lens = np.array([40, 600], np.int32)
+    assert lib.dopd_kv_pack_for_handoff(C.byref(f8), 1, p, p, 10, p, 8, p, p, A._hptr(lens), p, 2,
+                                        p, None) == A.DOPD_ERR_INVALID_SHAPE   # 600 > 8 pages

@@ -107,17 +107,6 @@ def test_write_then_pack_round_trip_is_a_transpose():
         assert np.array_equal(out[off[r]:off[r + 1]], expect.reshape(-1))
 
 
-def gpu_unpack(shape, buf, offs, req, lens, k_pool, v_pool, layers, pt):
-    import torch
-    kp, vp = G.A.to_device(k_pool), G.A.to_device(v_pool)
-    num_pages = k_pool.shape[-4]
-    G.A.dopd_kv_unpack_from_handoff(shape, layers, G.A.to_device(buf), G.A.to_device(offs),
-                                    G.A.to_device(req), G.A.to_device(lens), lens, len(req), kp, vp,
-                                    num_pages, G.A.to_device(pt), pt.shape[1])
-    torch.cuda.synchronize()
-    return G.A.to_host(kp), G.A.to_host(vp)
-
-
 @pytest.mark.parametrize("dtype,d,layers", [("bf16", 128, 2), ("bf16", 64, 1), ("fp32", 64, 3),
                                             ("fp32", 128, 1)])
 def test_unpack_bit_exact(dtype, d, layers):
@@ -132,7 +121,7 @@ def test_unpack_bit_exact(dtype, d, layers):
     offs = I.handoff_offsets(seq, layers, hkv, d)
     buf = I.normal(rng, (int(offs[-1]),), dtype)
     ref_k, ref_v = oracle.unpack(buf, offs, req, seq, kp, vp, layers, pt)
-    gk, gv = gpu_unpack(G.A.make_shape(8, hkv, d, dtype), buf, offs, req, seq, kp, vp, layers, pt)
+    gk, gv = G.gpu_unpack(G.A.make_shape(8, hkv, d, dtype), buf, offs, req, seq, kp, vp, layers, pt)
     assert np.array_equal(gk.view(np.uint8), ref_k.view(np.uint8))
     assert np.array_equal(gv.view(np.uint8), ref_v.view(np.uint8))
 
@@ -147,7 +136,7 @@ def test_unpack_unaligned_offsets():
     buf = I.normal(rng, (int(offs[-1]),), "bf16")
     req = np.arange(2, dtype=np.int32)
     ref_k, ref_v = oracle.unpack(buf, offs, req, lens, kp, vp, 1, pt)
-    gk, gv = gpu_unpack(G.A.make_shape(2, hkv, d), buf, offs, req, lens, kp, vp, 1, pt)
+    gk, gv = G.gpu_unpack(G.A.make_shape(2, hkv, d), buf, offs, req, lens, kp, vp, 1, pt)
     assert np.array_equal(gk, ref_k) and np.array_equal(gv, ref_v)
 
 
@@ -166,7 +155,7 @@ def test_handoff_round_trip_decode_bit_identical():
     offs = I.handoff_offsets(lens, 1, hkv, d)
     sh = G.A.make_shape(hq, hkv, d)
     buf = G.gpu_pack(sh, ka, va, 1, pt_a, req, lens, offs)
-    gk, gv = gpu_unpack(sh, buf, offs, req, lens, kb, vb, 1, pt_b)
+    gk, gv = G.gpu_unpack(sh, buf, offs, req, lens, kb, vb, 1, pt_b)
     ref_k, ref_v = oracle.unpack(buf, offs, req, lens, kb, vb, 1, pt_b)
     assert np.array_equal(gk, ref_k) and np.array_equal(gv, ref_v)
     q = I.normal(rng, (4, hq, d), "bf16")
