@@ -85,10 +85,12 @@ def prefill_flops(lens, hq, d):
     return int((4 * d * hq * lens * (lens + 1) // 2).sum())
 
 
-def write_bytes(lens, hkv, d, s=2):
+def write_bytes(lens, hkv, d, s=2, out_s=None):
+    """K and V read (s bytes per element) and written (out_s bytes), page ids, lengths."""
     lens = np.asarray(lens, np.int64)
     t = int(lens.sum())
-    return int(2 * (2 * t * hkv * d * s) + 4 * ((lens + 15) // 16).sum() + 8 * len(lens))
+    out_s = s if out_s is None else out_s
+    return int(2 * t * hkv * d * (s + out_s) + 4 * ((lens + 15) // 16).sum() + 8 * len(lens))
 
 
 def pack_bytes(lens, layers, hkv, d, s=2):
@@ -240,8 +242,9 @@ def main():
                     help="mixed step: 2 = decode on its own stream beside prefill/write/pack, "
                          "1 = everything in order on one stream")
     ap.add_argument("--kv", choices=("bf16", "fp8"), default="bf16",
-                    help="decode workloads: KV cache element type (fp8 = E4M3 pages with "
-                         "per-KV-head scales, written by the fp8 writer before timing)")
+                    help="KV cache element type (fp8 = E4M3 pages with per-KV-head scales): "
+                         "decode workloads read it (written by the fp8 writer before timing), "
+                         "the prefill workload writes it")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calib-mib", type=int, default=0,
                     help="after timing, run one device copy of this size (counter calibration)")
@@ -255,8 +258,9 @@ def main():
         summarize(args)
         return
 
-    if args.kv == "fp8" and args.workload not in ("decode_mha", "decode_gqa"):
-        print("--kv fp8 applies to the decode_mha and decode_gqa workloads", file=sys.stderr)
+    if args.kv == "fp8" and args.workload not in ("decode_mha", "decode_gqa", "prefill"):
+        print("--kv fp8 applies to the decode_mha, decode_gqa and prefill workloads",
+              file=sys.stderr)
         sys.exit(2)
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py runs on one GPU only: the hot path is measured on a single MI355X; "
@@ -515,16 +519,33 @@ def main():
         start = torch.zeros(n_pre, dtype=torch.int32, device=dev)
         T = int(w.cu_seqlens[-1])
         tm = {"prefill": Timer(torch, sA), "kv_write": Timer(torch, sA)}
+        if args.kv == "fp8":
+            # The prompts' K/V go to an E4M3 cache (scales from each head's
+            # absolute maximum over the batch).
+            shape8 = A.make_shape(w.hq, w.hkv, w.d, "fp8", w.scale)
+            ks = (k.abs().amax(dim=(0, 2)).float() / 448.0).contiguous()
+            vs = (v.abs().amax(dim=(0, 2)).float() / 448.0).contiguous()
+            kp = torch.full((w.num_pages, w.hkv, 16, w.d), 0x7F, dtype=torch.uint8, device=dev)
+            vp = torch.full((w.num_pages, w.hkv, w.d, 16), 0x7F, dtype=torch.uint8, device=dev)
+
+            def write():
+                A.dopd_kv_write_fp8(shape8, k, v, ks, vs, kp, vp, w.num_pages, pt,
+                                    w.page_table.shape[1], cu, start, n_pre, T, sA)
+            wbytes = write_bytes(w.prefill_lens, w.hkv, w.d, out_s=1)
+        else:
+            def write():
+                A.dopd_kv_write(shape, k, v, kp, vp, w.num_pages, pt, w.page_table.shape[1], cu,
+                                start, n_pre, T, sA)
+            wbytes = write_bytes(w.prefill_lens, w.hkv, w.d)
 
         def step():
             with tm["prefill"]:
                 A.dopd_prefill_attn(shape, q, k, v, out_p, None, cu, w.cu_seqlens, n_pre, sA)
             with tm["kv_write"]:
-                A.dopd_kv_write(shape, k, v, kp, vp, w.num_pages, pt, w.page_table.shape[1], cu,
-                                start, n_pre, T, sA)
+                write()
 
         work = {"prefill": ("TFLOP/s", prefill_flops(w.prefill_lens, w.hq, w.d)),
-                "kv_write": ("GB/s", write_bytes(w.prefill_lens, w.hkv, w.d))}
+                "kv_write": ("GB/s", wbytes)}
         dominant = "prefill"
 
     for _ in range(args.warmup):
