@@ -4,18 +4,20 @@
 Default workload: one mixed prefill/decode step with handoff (28 query heads,
 4 KV heads, d 128, bf16):
 
-  stream A: varlen causal prefill over 8 x 512 fresh tokens -> paged KV write
-            of those 4096 tokens -> handoff pack of the 8 requests (1 layer)
-  stream B: split-K paged decode of 192 requests, context lognormal(2048, 0.7)
-            clipped to [64, 16384], concurrently with stream A
+  varlen causal prefill over 8 x 512 fresh tokens -> paged KV write of those
+  4096 tokens -> split-K paged decode of 192 requests, context
+  lognormal(2048, 0.7) clipped to [64, 16384] -> handoff pack of the 8
+  prefilled requests (1 layer), in order on one stream (``--streams 2`` puts
+  the decode on a second stream beside the others)
 
 A "step" is one such launch set; K timed steps run back to back after W
 warm-up steps.  Every kernel is bracketed by HIP events on the stream it runs
 on.  The headline value is decode attention HBM throughput (algorithmic bytes /
 decode kernel time); prefill TFLOP/s and the write/pack bandwidths are
 reported beside it.  ``--workload`` selects the single-kernel workloads
-(decode MHA 7B-shaped, varlen prefill + write, GQA decode 70B-shaped) for the
-per-workload tables.
+(decode MHA 7B-shaped, varlen prefill + write, GQA decode 70B-shaped, chunked
+prefill over the paged cache, the P->D handoff) for the per-workload tables;
+``--kv fp8`` runs the decode workloads over E4M3 KV pages.
 
 Prints ONE JSON line.
 """
@@ -182,7 +184,7 @@ def summarize(args):
             c["hbm_bytes_per_call"] = int(1024 * (c["fetch_kib"] * ff + c["write_kib"] * fw))
         tr = {"workload": args.label, "source_hash": source_hash(), "copy_factors": factors,
               "calls": calls, "command": args.command}
-        with open(os.path.join(PROFILES, f"traffic_{args.label}.json"), "w") as f:
+        with open(os.path.join(args.traffic_dir, f"traffic_{args.label}.json"), "w") as f:
             json.dump(tr, f, indent=1)
         out.append("\nHBM bytes per call (scaled): " +
                    ", ".join(f"{k}: {v['hbm_bytes_per_call'] / 1e6:.1f} MB" for k, v in calls.items()))
@@ -253,6 +255,8 @@ def main():
     ap.add_argument("--label", default="mixed")
     ap.add_argument("--command", default="")
     ap.add_argument("--summary-out", default=None)
+    ap.add_argument("--traffic-dir", default=PROFILES,
+                    help="where --summarize writes traffic_<label>.json")
     args = ap.parse_args()
     if args.summarize:
         summarize(args)
