@@ -387,6 +387,7 @@ def main():
             vs = (vtok.abs().amax(dim=(0, 2)).float() / 448.0).contiguous()
             kp8 = torch.full((w.num_pages, w.hkv, 16, w.d), 0x7F, dtype=torch.uint8, device=dev)
             vp8 = torch.full((w.num_pages, w.hkv, w.d, 16), 0x7F, dtype=torch.uint8, device=dev)
+            ws = A.decode_workspace(shape8, w.context_lens, n_dec, args.split)
             cu_t = A.to_device(I.cu_from_lens(w.context_lens))
             A.dopd_kv_write_fp8(shape8, ktok, vtok, ks, vs, kp8, vp8, w.num_pages, pt,
                                 w.page_table.shape[1], cu_t,
