@@ -4,11 +4,11 @@
 Default workload: one mixed prefill/decode step with handoff (28 query heads,
 4 KV heads, d 128, bf16):
 
-  varlen causal prefill over 8 x 512 fresh tokens -> paged KV write of those
-  4096 tokens -> split-K paged decode of 192 requests, context
-  lognormal(2048, 0.7) clipped to [64, 16384] -> handoff pack of the 8
-  prefilled requests (1 layer), in order on one stream (``--streams 2`` puts
-  the decode on a second stream beside the others)
+  split-K paged decode of 192 requests, context lognormal(2048, 0.7) clipped
+  to [64, 16384] -> varlen causal prefill over 8 x 512 fresh tokens -> paged
+  KV write of those 4096 tokens -> handoff pack of the 8 prefilled requests
+  (1 layer), in order on one stream (``--order prefill-first`` runs the
+  decode after the write; ``--streams 2`` puts it on a second stream)
 
 A "step" is one such launch set; K timed steps run back to back after W
 warm-up steps.  Every kernel is bracketed by HIP events on the stream it runs
@@ -240,6 +240,9 @@ def main():
     ap.add_argument("--chunk", type=int, default=512, help="chunked workload: tokens per chunk")
     ap.add_argument("--budget", type=int, default=8192,
                     help="chunked workload: tokens per call (chunks of several prompts)")
+    ap.add_argument("--order", choices=("decode-first", "prefill-first"), default="decode-first",
+                    help="mixed step on one stream: the decode batch before the prefill, write "
+                         "and pack (its tokens are the TPOT-bound ones), or after the write")
     ap.add_argument("--streams", type=int, default=1, choices=(1, 2),
                     help="mixed step: 2 = decode on its own stream beside prefill/write/pack, "
                          "1 = everything in order on one stream")
@@ -328,26 +331,30 @@ def main():
         if args.streams == 1:
             tm["decode"] = Timer(torch, sA)
 
+        dec_first = args.streams == 1 and args.order == "decode-first"
+
+        def decode_call():
+            with tm["decode"]:
+                A.dopd_decode_attn(shape, q_dec, kp[0], vp[0], w.num_pages, pt, stride, ctx,
+                                   w.context_lens, n_dec, args.split, out_d, None, ws,
+                                   stream=sD)
+
         def step():
             # Two streams: the prefill is enqueued first, so its large workgroups
             # are dispatched before the decode work items fill the machine.
             if args.streams == 2:
                 sB.wait_stream(sA)
+            if dec_first:
+                decode_call()
             with tm["prefill"]:
                 A.dopd_prefill_attn(shape, q, k, v, out_p, None, cu, w.cu_seqlens, n_pre, sA)
             if args.streams == 2:
-                with tm["decode"]:
-                    A.dopd_decode_attn(shape, q_dec, kp[0], vp[0], w.num_pages, pt, stride, ctx,
-                                       w.context_lens, n_dec, args.split, out_d, None, ws,
-                                       stream=sD)
+                decode_call()
             with tm["kv_write"]:
                 A.dopd_kv_write(shape, k, v, kp[0], vp[0], w.num_pages, pre_pt, stride, cu, start,
                                 n_pre, T, sA)
-            if args.streams == 1:
-                with tm["decode"]:
-                    A.dopd_decode_attn(shape, q_dec, kp[0], vp[0], w.num_pages, pt, stride, ctx,
-                                       w.context_lens, n_dec, args.split, out_d, None, ws,
-                                       stream=sD)
+            if args.streams == 1 and not dec_first:
+                decode_call()
             with tm["pack"]:
                 A.dopd_kv_pack_for_handoff(shape, L, kp, vp, w.num_pages, pt, stride, hreq, hlen,
                                            w.handoff_lens, offs, n_pre, out_h, sA)
@@ -685,6 +692,7 @@ def main():
                                        if args.kv == "fp8" else ""),
                    "seed": int(w.seed), "split_tokens": args.split, "kv": args.kv,
                    "streams": args.streams if args.workload == "mixed" else 1,
+                   "order": args.order if args.workload == "mixed" and args.streams == 1 else None,
                    "pack_layers": args.pack_layers if args.workload in ("mixed", "handoff") else None,
                    "chunk": args.chunk if args.workload == "chunked" else None,
                    "budget": args.budget if args.workload == "chunked" else None},
