@@ -127,3 +127,17 @@ def test_prefill_paged_invariant_under_page_permutation():
     pt2 = np.where(pt >= 0, perm[np.maximum(pt, 0)], -1).astype(np.int32)
     out2, lse2 = G.gpu_prefill_paged(sh, q, kp2, vp2, pt2, cu, pre)
     assert np.array_equal(out1, out2) and np.array_equal(lse1, lse2)
+
+
+def test_prefill_paged_many_requests():
+    # 80 chunks (more than the length-ordered work list holds), random
+    # prefixes and chunk lengths, some empty chunks.
+    rng = np.random.default_rng(88)
+    prefix = rng.integers(0, 500, 80)
+    chunk = rng.integers(0, 200, 80)
+    chunk[[0, 41]] = 0
+    q, kp, vp, pt, cu, pre = paged_case(89, prefix, chunk, 8, 2, 128, "bf16")
+    ref, ref_lse = oracle.prefill_paged(q, kp, vp, pt, cu, pre, 1 / np.sqrt(128))
+    out, lse = G.gpu_prefill_paged(G.A.make_shape(8, 2, 128, "bf16"), q, kp, vp, pt, cu, pre)
+    G.assert_attention_close(out, ref, "bf16", "paged prefill 80 requests")
+    assert np.max(np.abs(lse - ref_lse)) < 2e-2
