@@ -2,7 +2,6 @@
 oracle satisfies exactly (page permutation, split size, determinism)."""
 import numpy as np
 import pytest
-import torch
 
 import oracle
 from paper_2511_20982_amd import inputs as I

@@ -3,7 +3,6 @@ end of the cache) against the fp64 oracle, chunked == one-shot, a chunk of
 one token == a decode step, and page-permutation invariance."""
 import numpy as np
 import pytest
-import torch
 
 import oracle
 from paper_2511_20982_amd import inputs as I

@@ -2,7 +2,6 @@
 and checks that the pins catch every one of them.  The real oracle must pass
 the same checks.  This measures the strength of the pins, not the GPU path."""
 import ctypes
-import math
 import os
 import subprocess
 

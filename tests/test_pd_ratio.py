@@ -11,7 +11,6 @@ reproduces bilinear functions, and the batcher emits every request exactly
 once within its length and waiting bounds.
 """
 import itertools
-import math
 
 import numpy as np
 import pytest
