@@ -503,6 +503,9 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_bf16_kernel(PrefillArgs
     // Tiles every row of the item sees in full (positive scales only).
     const int nfull = pos_scale ? (P + q0) / BN : 0;
     if (wave_active && nfull > 0) m_run = row_max(sa);
+    // The first step's prefetch writes K tile 2 into K buffer 0: every wave
+    // must have read tile 0 from it first.
+    __syncthreads();
 
     int j = 0;
     auto prefetch = [&](int jj, auto par) {  // K(jj + 2) -> K buffer par, V(jj + 1) -> V buffer par ^ 1
