@@ -378,36 +378,13 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_bf16_kernel(PrefillArgs
       }
       __builtin_amdgcn_sched_group_barrier(kMfma, 4, 0);
     };
-    // O^T += V^T P^T of the tile; on the paged path a tile that runs past the
-    // cached keys (kv0 + BN > kv_end) clears the V operand bits of those keys
-    // (their slots may hold anything, and 0 * NaN would not vanish).
-    auto pv = [&](int buf, int kv0, auto may_run_past) {
+    // O^T += V^T P^T of the tile.
+    auto pv = [&](int buf) {
       bf16x8 va[4][ET];
-      if constexpr (PAGED && decltype(may_run_past)::value) {
-        // live keys among this lane's 8 of k-step kk: kv_end - kv0 - 16kk - 8hi
-        // (a uniform test first: only the tile that holds kv_end needs it)
-        const int nv0 = kv0 + BN > kv_end ? kv_end - kv0 - 8 * hi : BN;
 #pragma unroll
-        for (int kk = 0; kk < 4; ++kk) {
-          const int nv = nv0 - 16 * kk;
-          uint32_t keep[4];
+      for (int kk = 0; kk < 4; ++kk)
 #pragma unroll
-          for (int wd = 0; wd < 4; ++wd)
-            keep[wd] = (2 * wd + 1 < nv) ? 0xffffffffu : (2 * wd < nv ? 0x0000ffffu : 0u);
-#pragma unroll
-          for (int et = 0; et < ET; ++et) {
-            u32x4 x = __builtin_bit_cast(u32x4, vread(buf, kk, et));
-#pragma unroll
-            for (int wd = 0; wd < 4; ++wd) x[wd] &= keep[wd];
-            va[kk][et] = __builtin_bit_cast(bf16x8, x);
-          }
-        }
-      } else {
-#pragma unroll
-        for (int kk = 0; kk < 4; ++kk)
-#pragma unroll
-          for (int et = 0; et < ET; ++et) va[kk][et] = vread(buf, kk, et);
-      }
+        for (int et = 0; et < ET; ++et) va[kk][et] = vread(buf, kk, et);
 #pragma unroll
       for (int kk = 0; kk < 4; ++kk)
 #pragma unroll
@@ -473,6 +450,33 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_bf16_kernel(PrefillArgs
       l_run += psum;
     };
 
+    // Paged: the keys of the last tile past the end of the cache come from
+    // slots that may hold anything, NaN included (pages past the last one are
+    // read as copies of it).  Their P is 0, but 0 * NaN is not, so once the
+    // tile's V pages have landed each wave clears those keys in its own page
+    // of the V tile; the barrier that closes the step publishes the zeros.
+    auto clear_dead_v = [&](int buf, int jt) {
+      if constexpr (PAGED) {
+        const int nlive = kv_end - jt * BN;  // live keys of tile jt (uniform, >= 1)
+        if (nlive >= 16 * w + 16) return;    // this wave's page is all live
+        __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0): this wave's V page has landed
+        const int kc = 2 * w + hi;           // key chunk of this lane: keys 8kc .. 8kc + 7
+        const int nv = nlive - 8 * kc;       // live keys among them
+        uint32_t keep[4];
+#pragma unroll
+        for (int wd = 0; wd < 4; ++wd)
+          keep[wd] = (2 * wd + 1 < nv) ? 0xffffffffu : (2 * wd < nv ? 0x0000ffffu : 0u);
+#pragma unroll
+        for (int et = 0; et < ET; ++et) {
+          u32x4* p = reinterpret_cast<u32x4*>(vbuf(buf) + ((et * 8 + kc) * 32 + (l & 31)) * 8);
+          u32x4 x = *p;
+#pragma unroll
+          for (int wd = 0; wd < 4; ++wd) x[wd] &= keep[wd];
+          *p = x;
+        }
+      }
+    };
+
     // K tile s sits in K buffer s % 2 and V tile s in V buffer s % 2; K runs
     // one tile ahead of V.  A step j: loads K(j + 2) and V(j + 1) into the
     // free buffers, computes S^T(j + 1) with the softmax of tile j, then
@@ -486,6 +490,7 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_bf16_kernel(PrefillArgs
       if (ntiles > 1) load_k(1, BN);
       pid_v = p0;
       load_v(0, 0);
+      clear_dead_v(0, 0);
       // the first step loads K(2) and V(1); the id of tile 3 is read ahead
       pid_v = p1;
       pid_k = __builtin_amdgcn_readfirstlane(page_of(2));
@@ -523,8 +528,9 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_bf16_kernel(PrefillArgs
       prefetch(j, par);
       if (wave_active) {
         half_qk(sc, sn, par() ^ 1);
-        pv(par(), j * BN, std::false_type{});  // steady-state tiles hold cached keys only
+        pv(par());
       }
+      if (j + 1 < ntiles) clear_dead_v(par() ^ 1, j + 1);
       __syncthreads();
     };
     for (; j + 1 < nfull; j += 2) {
@@ -544,9 +550,10 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_bf16_kernel(PrefillArgs
       prefetch(j, par);
       if (wave_active && j * BN <= P + row_w + 31) {  // some key of tile j visible to this wave
         softmax_masked(sa, j * BN);
-        pv(par(), j * BN, std::true_type{});
+        pv(par());
       }
       if (wave_active && j + 1 < ntiles && (j + 1) * BN <= P + row_w + 31) qk(par() ^ 1, sa);
+      if (j + 1 < ntiles) clear_dead_v(par() ^ 1, j + 1);
       __syncthreads();
     };
     for (; j < ntiles; ++j) {
