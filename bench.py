@@ -110,6 +110,18 @@ def source_hash() -> str:
     return h.hexdigest()[:16]
 
 
+def repeat_timed(fn, min_seconds):
+    """Calls fn until at least min_seconds have passed (once at least); returns
+    (first result, passes, seconds)."""
+    t0 = time.time()
+    res = fn()
+    n = 1
+    while time.time() - t0 < min_seconds:
+        fn()
+        n += 1
+    return res, n, time.time() - t0
+
+
 def load_traffic(workload, call):
     """HBM bytes per call from committed counter summaries, if the kernels are unchanged."""
     path = os.path.join(PROFILES, f"traffic_{workload}.json")
@@ -258,6 +270,8 @@ def main():
     ap.add_argument("--label", default="mixed")
     ap.add_argument("--command", default="")
     ap.add_argument("--summary-out", default=None)
+    ap.add_argument("--cpu-seconds", type=float, default=10.0,
+                    help="host time the oracle baseline is timed over (passes repeat)")
     ap.add_argument("--traffic-dir", default=PROFILES,
                     help="where --summarize writes traffic_<label>.json")
     args = ap.parse_args()
@@ -616,40 +630,40 @@ def main():
             vq = oracle.e4m3_quantize(w.v_pool.transpose(0, 3, 1, 2).reshape(-1, hkv, d), vs_h)
             kq = kq.reshape(P, 16, hkv, d).transpose(0, 2, 1, 3).copy()
             vq = vq.reshape(P, 16, hkv, d).transpose(0, 2, 3, 1).copy()
-            t1 = time.time()
-            ref, _ = oracle.decode_e4m3(w.q_dec, kq, vq, ks_h, vs_h, w.page_table,
-                                        w.context_lens, w.scale)
-            dt = time.time() - t1
+            (ref, _), n, dt = repeat_timed(
+                lambda: oracle.decode_e4m3(w.q_dec, kq, vq, ks_h, vs_h, w.page_table,
+                                           w.context_lens, w.scale), args.cpu_seconds)
             amount = work["decode"][1]
-            cpu = {"value": round(amount / dt / 1e9, 4), "unit": "GB/s", "cores": threads,
+            cpu = {"value": round(n * amount / dt / 1e9, 4), "unit": "GB/s", "cores": threads,
                    "kind": "oracle", "cpu": cpu_info(), "seconds": round(dt, 2),
                    "sample": f"fp64 oracle decode over E4M3 pages of the whole batch "
-                             f"({len(w.context_lens)} requests, {amount / 1e9:.3f} GB algorithmic)"}
+                             f"({len(w.context_lens)} requests, {amount / 1e9:.3f} GB algorithmic), "
+                             f"{n} passes"}
             gotf = I.bf16_bits_to_f32(A.to_host(out_d)).astype(np.float64)
             parity = {"decode_max_abs_err": float(np.max(np.abs(gotf - ref))),
                       "decode_rows": int(ref.shape[0] * ref.shape[1]),
                       "kv": "fp8 pages from the GPU writer; oracle quantised the same bf16 cache"}
         elif dominant == "decode":
             # The whole decode batch of the step (about a second of host work).
-            t1 = time.time()
-            ref, _ = oracle.decode(w.q_dec, w.k_pool, w.v_pool, w.page_table, w.context_lens,
-                                   w.scale)
-            dt = time.time() - t1
+            (ref, _), n, dt = repeat_timed(
+                lambda: oracle.decode(w.q_dec, w.k_pool, w.v_pool, w.page_table,
+                                      w.context_lens, w.scale), args.cpu_seconds)
             amount = decode_bytes(w.context_lens, w.hq, w.hkv, w.d)
-            cpu = {"value": round(amount / dt / 1e9, 4), "unit": "GB/s", "cores": threads,
+            cpu = {"value": round(n * amount / dt / 1e9, 4), "unit": "GB/s", "cores": threads,
                    "kind": "oracle", "cpu": cpu_info(), "seconds": round(dt, 2),
                    "sample": f"fp64 oracle decode of the whole batch ({len(w.context_lens)} "
-                             f"requests, {amount / 1e9:.3f} GB algorithmic)"}
+                             f"requests, {amount / 1e9:.3f} GB algorithmic), {n} passes"}
             gotf = I.bf16_bits_to_f32(A.to_host(out_d)).astype(np.float64)
             parity = {"decode_max_abs_err": float(np.max(np.abs(gotf - ref))),
                       "decode_rows": int(ref.shape[0] * ref.shape[1])}
             if "prefill" in kern:
-                t1 = time.time()
-                ref_p, _ = oracle.prefill(w.q, w.k, w.v, w.cu_seqlens, w.scale)
-                dtp = time.time() - t1
-                cpu["prefill_tflops"] = round(work["prefill"][1] / dtp / 1e12, 6)
+                (ref_p, _), n_p, dtp = repeat_timed(
+                    lambda: oracle.prefill(w.q, w.k, w.v, w.cu_seqlens, w.scale),
+                    args.cpu_seconds)
+                cpu["prefill_tflops"] = round(n_p * work["prefill"][1] / dtp / 1e12, 6)
                 cpu["prefill_seconds"] = round(dtp, 2)
-                cpu["sample"] += f"; fp64 oracle prefill of the whole prefill batch ({dtp:.1f} s)"
+                cpu["sample"] += (f"; fp64 oracle prefill of the whole prefill batch, {n_p} passes "
+                                  f"({dtp:.1f} s)")
                 gotp = I.bf16_bits_to_f32(A.to_host(out_p)).astype(np.float64)
                 parity["prefill_max_abs_err"] = float(np.max(np.abs(gotp - ref_p)))
         else:
@@ -657,16 +671,17 @@ def main():
             rows_tok = np.concatenate([w.cu_seqlens[1:] - 1 - i for i in range(4)])
             rows_tok = np.repeat(rows_tok, 4)
             heads = (np.arange(len(rows_tok)) * 7) % w.hq
-            t1 = time.time()
-            ref, _ = oracle.prefill_rows(w.q, w.k, w.v, w.cu_seqlens, w.scale, rows_tok, heads)
-            dt = time.time() - t1
+            (ref, _), n, dt = repeat_timed(
+                lambda: oracle.prefill_rows(w.q, w.k, w.v, w.cu_seqlens, w.scale, rows_tok, heads),
+                args.cpu_seconds)
             req_of = np.searchsorted(w.cu_seqlens, rows_tok, side="right") - 1
             pos = rows_tok - w.cu_seqlens[req_of]
             flops = int((4 * w.d * (pos + 1)).sum())
-            cpu = {"value": round(flops / dt / 1e12, 6), "unit": "TFLOP/s", "cores": threads,
+            cpu = {"value": round(n * flops / dt / 1e12, 6), "unit": "TFLOP/s", "cores": threads,
                    "kind": "oracle", "cpu": cpu_info(), "seconds": round(dt, 2),
                    "sample": f"fp64 oracle prefill of {len(rows_tok)} sampled rows (the last 4 "
-                             f"rows of every prompt, 4 heads each; {flops / 1e9:.2f} GFLOP)"
+                             f"rows of every prompt, 4 heads each; {flops / 1e9:.2f} GFLOP), "
+                             f"{n} passes"
                              + ("; chunked output checked against the one-shot oracle rows"
                                 if args.workload == "chunked" else "")}
             out_rows = gather_out() if args.workload == "chunked" else out_p

@@ -86,3 +86,11 @@ def test_summarize_scales_counters_by_the_calibration_kernel(tmp_path):
     assert t["source_hash"] == B.source_hash()
     text = out.read_text()
     assert "decode_split_kernel" in text and "200.00" in text
+
+
+def test_repeat_timed_covers_the_requested_time():
+    calls = []
+    res, n, dt = B.repeat_timed(lambda: calls.append(1) or len(calls), 0.05)
+    assert res == 1 and n == len(calls) and n >= 2 and dt >= 0.05
+    res, n, _ = B.repeat_timed(lambda: 7, 0.0)
+    assert res == 7 and n == 1
