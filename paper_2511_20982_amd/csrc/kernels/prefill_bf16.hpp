@@ -560,11 +560,16 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_bf16_kernel(PrefillArgs
       if (j & 1) step_tail(odd);
       else step_tail(even);
     }
-    if (!wave_active || myq >= L) return;
+    if (!wave_active) return;
     float l_tot = l_run + __shfl_xor(l_run, 32, 64);
     const float inv = 1.f / l_tot;
-    // lane holds O^T[e = 32et + 8(x/4) + 4hi + x%4][myq]
-    uint16_t* op = a.out + ((int64_t)(seq0 + myq) * a.hq + h) * D + 4 * hi;
+    // The wave's 32 x D output block goes through LDS (no load is in flight
+    // and every wave is past its last tile read: the loop's last barrier), so
+    // that 16 lanes store one 256-byte row instead of 32 rows taking 8-byte
+    // pieces.  Wave w uses one of the four tile buffers; rows padded by 16
+    // bytes.  Lane holds O^T[e = 32et + 8(x/4) + 4hi + x%4][myq].
+    constexpr int RS = D + 8;
+    uint16_t* so = w == 0 ? sK0 : w == 1 ? sK1 : w == 2 ? sV0 : sV1;
 #pragma unroll
     for (int et = 0; et < ET; ++et)
 #pragma unroll
@@ -572,9 +577,23 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_bf16_kernel(PrefillArgs
         u32x2 x;
         x[0] = pack_bf16x2(oacc[et][4 * gq] * inv, oacc[et][4 * gq + 1] * inv);
         x[1] = pack_bf16x2(oacc[et][4 * gq + 2] * inv, oacc[et][4 * gq + 3] * inv);
-        *reinterpret_cast<u32x2*>(op + 32 * et + 8 * gq) = x;
+        *reinterpret_cast<u32x2*>(so + (l & 31) * RS + 32 * et + 8 * gq + 4 * hi) = x;
       }
-    if (a.lse && hi == 0) a.lse[(int64_t)(seq0 + myq) * a.hq + h] = (m_run + __log2f(l_tot)) * kLn2;
+    // The LDS writes and reads below are this wave's alone (in order within
+    // the wave).
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    constexpr int CH = D / 8;  // 16-byte chunks per row
+#pragma unroll
+    for (int i = l; i < 32 * CH; i += 64) {
+      const int rr = i / CH, c = i % CH;
+      const u32x4 x = *reinterpret_cast<const u32x4*>(so + rr * RS + 8 * c);
+      if (row_w + rr < L)
+        *reinterpret_cast<u32x4*>(a.out + ((int64_t)(seq0 + row_w + rr) * a.hq + h) * D + 8 * c) = x;
+    }
+    if (a.lse && hi == 0 && myq < L)
+      a.lse[(int64_t)(seq0 + myq) * a.hq + h] = (m_run + __log2f(l_tot)) * kLn2;
   }
 }
 
