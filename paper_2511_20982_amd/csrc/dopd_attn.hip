@@ -261,6 +261,17 @@ dopd_status launch_prefill_bf16(dopd::PrefillArgs a, int d, const int32_t* cu_ho
     for (int32_t r = 0; r < nreq; ++r) order[r] = r;
     std::stable_sort(order, order + nreq, [&](int x, int y) { return keys(x) > keys(y); });
     for (int32_t r = 0; r < nreq; ++r) a.ord[r] = (uint8_t)order[r];
+    // slots per block, as the kernel groups them
+    const int g = a.hq / a.hkv;
+    const int gs = (g % dopd::kPfHeadsPerWG == 0) ? g / dopd::kPfHeadsPerWG : 1;
+    int sum = 0;
+    for (int32_t i = 0; i < nreq; ++i) {
+      const int r = order[i];
+      sum += gs * ((cu_host[r + 1] - cu_host[r] + dopd::kPfBM - 1) / dopd::kPfBM);
+      a.incl[i] = sum;
+    }
+    for (int32_t r = 0; r <= nreq; ++r) a.cu_h[r] = cu_host[r];
+    for (int32_t r = 0; r < nreq; ++r) a.prefix_h[r] = PAGED ? prefix_host[r] : 0;
     a.xcd_order = 1;
     a.per_xcd = (int)((items + dopd::kNumXcd - 1) / dopd::kNumXcd);
     blocks = (int64_t)a.per_xcd * dopd::kNumXcd;

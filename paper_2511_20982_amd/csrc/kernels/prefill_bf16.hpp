@@ -51,6 +51,11 @@ struct PrefillArgs {
   // run together on one XCD and share its L2.
   int xcd_order, n_items, per_xcd, tiles_total;
   uint8_t ord[64];     // requests by decreasing length
+  // With the XCD order: incl[i] = sum over positions p <= i of the order of
+  // (slots per block) x (q tiles of request ord[p]); copies of cu and prefix.
+  int incl[64];
+  int cu_h[65];
+  int prefix_h[64];
   // Chunk prefill over the paged cache (the paged instantiation only): the
   // chunk rows of request r are q[cu[r] .. cu[r+1]), its keys are the cached
   // positions 0 .. prefix[r] + chunk length - 1, read through the page table.
@@ -116,15 +121,12 @@ __device__ __forceinline__ bool pf_find_item_xcd(const PrefillArgs& a, int b, in
   const int blk = n / per_blk;
   const int rem = n - blk * per_blk;
   const int l = lane_id();
-  const int rr = l < a.nreq ? a.ord[l] : 0;
-  const int nt = l < a.nreq ? pf_tiles(a.cu, rr) : 0;
-  const int cnt = gs * nt;
-  const int incl = wave_inclusive_scan(cnt);
-  const unsigned long long hit = __ballot(rem < incl);
-  const int k = __ffsll((long long)hit) - 1;
-  const int local = rem - __shfl(incl - cnt, k, 64);
-  req = __shfl(rr, k, 64);
-  tile = __shfl(nt, k, 64) - 1 - local / gs;
+  const unsigned long long hit = __ballot(l < a.nreq && rem < a.incl[l]);
+  const int k = __builtin_amdgcn_readfirstlane(__ffsll((long long)hit) - 1);
+  const int before = k > 0 ? a.incl[k - 1] : 0;
+  const int local = rem - before;
+  req = __builtin_amdgcn_readfirstlane(a.ord[k]);
+  tile = (a.incl[k] - before) / gs - 1 - local / gs;
   slot = blk * gs + local % gs;
   return true;
 }
@@ -162,9 +164,12 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_bf16_kernel(PrefillArgs
     const int tid = threadIdx.x, l = lane_id();
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int g = a.hq / a.hkv, kvh = h / g;
-    const int seq0 = a.cu[r], L = a.cu[r + 1] - seq0;
+    // (Copies in the arguments when the XCD order is used: scalar loads.)
+    const int seq0 = __builtin_amdgcn_readfirstlane(a.xcd_order ? a.cu_h[r] : a.cu[r]);
+    const int L = __builtin_amdgcn_readfirstlane(a.xcd_order ? a.cu_h[r + 1] : a.cu[r + 1]) - seq0;
     // Cached tokens before the chunk: query row i sits at key position P + i.
-    const int P = PAGED ? __builtin_amdgcn_readfirstlane(a.prefix[r]) : 0;
+    const int P =
+        PAGED ? __builtin_amdgcn_readfirstlane(a.xcd_order ? a.prefix_h[r] : a.prefix[r]) : 0;
     const int q0 = tile * BM;
     const int kv_end = P + min(L, q0 + BM);   // keys of this item: [0, kv_end)
     const int ntiles = (kv_end + BN - 1) / BN;
@@ -174,15 +179,15 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_bf16_kernel(PrefillArgs
     const int hi = l >> 5;                    // lane half
 
     // Q^T operand, B of the QK MFMA: lane holds Q[myq][16ks + 8hi + 0..7].
+    // Rows past the chunk read its row 0 (finite values; their results are
+    // never stored), so nothing waits for these loads before the tile loads
+    // below are issued.
     bf16x8 qop[KS];
     {
-      const bool ok = myq < L;
-      const uint16_t* qp = a.q + ((int64_t)(seq0 + (ok ? myq : 0)) * a.hq + h) * D + 8 * hi;
+      const uint16_t* qp = a.q + ((int64_t)(seq0 + (myq < L ? myq : 0)) * a.hq + h) * D + 8 * hi;
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks) {
-        u32x4 x = ok ? *reinterpret_cast<const u32x4*>(qp + 16 * ks) : u32x4{0, 0, 0, 0};
-        qop[ks] = __builtin_bit_cast(bf16x8, x);
-      }
+      for (int ks = 0; ks < KS; ++ks)
+        qop[ks] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(qp + 16 * ks));
     }
 
     f32x16 oacc[ET];
@@ -586,7 +591,8 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_bf16_kernel(PrefillArgs
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
     constexpr int CH = D / 8;  // 16-byte chunks per row
 #pragma unroll
-    for (int i = l; i < 32 * CH; i += 64) {
+    for (int u = 0; u < 32 * CH / 64; ++u) {
+      const int i = l + 64 * u;
       const int rr = i / CH, c = i % CH;
       const u32x4 x = *reinterpret_cast<const u32x4*>(so + rr * RS + 8 * c);
       if (row_w + rr < L)
