@@ -34,7 +34,10 @@ __global__ __launch_bounds__(256) void kv_pack_kernel(
     if (aligned) {
       const int nch = nel / kEl;
       for (int i = threadIdx.x; i < nch; i += blockDim.x)
-        reinterpret_cast<u32x4*>(dst)[i] = reinterpret_cast<const u32x4*>(src)[i];
+        // streaming stores: the packed buffer leaves the caches at once
+        // (it goes to another instance), not during the next kernel
+        __builtin_nontemporal_store(reinterpret_cast<const u32x4*>(src)[i],
+                                    reinterpret_cast<u32x4*>(dst) + i);
     } else {
       for (int i = threadIdx.x; i < nel; i += blockDim.x) dst[i] = src[i];
     }
@@ -64,7 +67,7 @@ __global__ __launch_bounds__(256) void kv_pack_kernel(
         else
           x[w] = sv[(e0 + w) * kPage + t];
       }
-      reinterpret_cast<u32x4*>(dst)[i] = x;
+      __builtin_nontemporal_store(x, reinterpret_cast<u32x4*>(dst) + i);
     }
   } else {
     for (int i = threadIdx.x; i < nel; i += blockDim.x) {

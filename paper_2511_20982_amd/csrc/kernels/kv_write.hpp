@@ -50,7 +50,11 @@ __global__ __launch_bounds__(kKvwThreads) void kv_write_kernel(
     const int slot = i / CPR, c = i % CPR;
     if (slot >= s0 && slot < s1) {
       const int64_t src = (src0 + slot - s0) * row_elems + (int64_t)h * D;  // source row
-      reinterpret_cast<u32x4*>(kdst + slot * D)[c] = reinterpret_cast<const u32x4*>(k_new + src)[c];
+      // Streaming (nontemporal) store: the rows are not read again soon, and
+      // they leave the caches now instead of being written back while the
+      // decode that follows streams the pools.
+      __builtin_nontemporal_store(reinterpret_cast<const u32x4*>(k_new + src)[c],
+                                  reinterpret_cast<u32x4*>(kdst + slot * D) + c);
       *reinterpret_cast<u32x4*>(&s_v[slot * TP + c * kEl]) =
           reinterpret_cast<const u32x4*>(v_new + src)[c];
     }

@@ -595,8 +595,11 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_bf16_kernel(PrefillArgs
       const int i = l + 64 * u;
       const int rr = i / CH, c = i % CH;
       const u32x4 x = *reinterpret_cast<const u32x4*>(so + rr * RS + 8 * c);
+      // (streaming store: the output is not read again by this step, and it
+      // is written out now rather than evicted during the next kernel)
       if (row_w + rr < L)
-        *reinterpret_cast<u32x4*>(a.out + ((int64_t)(seq0 + row_w + rr) * a.hq + h) * D + 8 * c) = x;
+        __builtin_nontemporal_store(
+            x, reinterpret_cast<u32x4*>(a.out + ((int64_t)(seq0 + row_w + rr) * a.hq + h) * D + 8 * c));
     }
     if (a.lse && hi == 0 && myq < L)
       a.lse[(int64_t)(seq0 + myq) * a.hq + h] = (m_run + __log2f(l_tot)) * kLn2;

@@ -86,3 +86,20 @@ def test_prefill_bf16_many_requests(d):
     out, lse = G.gpu_prefill(G.A.make_shape(8, 2, d, "bf16"), q, k, v, cu)
     G.assert_attention_close(out, ref, "bf16", f"prefill 100 requests d={d}")
     assert np.max(np.abs(lse - ref_lse)) < 2e-2
+
+
+@pytest.mark.parametrize("hq,hkv", [(8, 2), (7, 7)])
+def test_prefill_bf16_64_requests(hq, hkv):
+    # Exactly 64 requests: the largest batch whose work order, lengths and
+    # per-request prefix sums the kernel takes from its arguments.  Lengths
+    # 0..400 (some empty, some one tile, some ragged), unsorted.
+    rng = np.random.default_rng(75 + hq)
+    lens = rng.integers(0, 401, 64).astype(np.int32)
+    lens[[0, 17, 63]] = 0
+    lens[[5, 6]] = [128, 1]
+    q, k, v = I.prefill_batch(rng, lens, hq, hkv, 128, "bf16")
+    cu = I.cu_from_lens(lens)
+    ref, ref_lse = oracle.prefill(q, k, v, cu, 1.0 / np.sqrt(128))
+    out, lse = G.gpu_prefill(G.A.make_shape(hq, hkv, 128, "bf16"), q, k, v, cu)
+    G.assert_attention_close(out, ref, "bf16", f"prefill 64 requests {hq}/{hkv}")
+    assert np.max(np.abs(lse - ref_lse)) < 2e-2

@@ -140,3 +140,18 @@ def test_prefill_paged_many_requests():
     out, lse = G.gpu_prefill_paged(G.A.make_shape(8, 2, 128, "bf16"), q, kp, vp, pt, cu, pre)
     G.assert_attention_close(out, ref, "bf16", "paged prefill 80 requests")
     assert np.max(np.abs(lse - ref_lse)) < 2e-2
+
+
+def test_prefill_paged_64_requests():
+    # Exactly 64 chunks (the largest batch whose lengths and prefixes the
+    # kernel takes from its arguments), random prefixes, some empty chunks.
+    rng = np.random.default_rng(90)
+    prefix = rng.integers(0, 700, 64)
+    chunk = rng.integers(0, 260, 64)
+    chunk[[2, 63]] = 0
+    prefix[5] = 0
+    q, kp, vp, pt, cu, pre = paged_case(91, prefix, chunk, 8, 2, 128, "bf16")
+    ref, ref_lse = oracle.prefill_paged(q, kp, vp, pt, cu, pre, 1 / np.sqrt(128))
+    out, lse = G.gpu_prefill_paged(G.A.make_shape(8, 2, 128, "bf16"), q, kp, vp, pt, cu, pre)
+    G.assert_attention_close(out, ref, "bf16", "paged prefill 64 requests")
+    assert np.max(np.abs(lse - ref_lse)) < 2e-2
