@@ -33,8 +33,11 @@ __global__ __launch_bounds__(256) void kv_unpack_kernel(
   if (kv == 0) {
     T* dst = k_pool + (lpage * hkv + h) * kPage * D;
     if (aligned) {
+      // streaming stores (here and below): the pages leave the caches now,
+      // not as write-back during the kernels that follow
       for (int i = tid; i < nvalid * CPR; i += 256)
-        reinterpret_cast<u32x4*>(dst)[i] = reinterpret_cast<const u32x4*>(src)[i];
+        __builtin_nontemporal_store(reinterpret_cast<const u32x4*>(src)[i],
+                                    reinterpret_cast<u32x4*>(dst) + i);
     } else {
       for (int i = tid; i < nvalid * D; i += 256) dst[i] = src[i];
     }
@@ -70,7 +73,7 @@ __global__ __launch_bounds__(256) void kv_unpack_kernel(
           x[w] = s_v[(run * kEl + w) * TP + e];
         }
       }
-      *reinterpret_cast<u32x4*>(drow) = x;
+      __builtin_nontemporal_store(x, reinterpret_cast<u32x4*>(drow));
     } else {
       for (int k = 0; k < kEl; ++k) {
         const int s = run * kEl + k;
