@@ -260,7 +260,7 @@ dopd_status launch_prefill_bf16(dopd::PrefillArgs a, int d, const int32_t* cu_ho
     int order[dopd::kPfMaxOrdered];
     for (int32_t r = 0; r < nreq; ++r) order[r] = r;
     std::stable_sort(order, order + nreq, [&](int x, int y) { return keys(x) > keys(y); });
-    for (int32_t r = 0; r < nreq; ++r) a.ord[r] = (uint8_t)order[r];
+    for (int32_t r = 0; r < nreq; ++r) a.ord[r] = order[r];
     // slots per block, as the kernel groups them
     const int g = a.hq / a.hkv;
     const int gs = (g % dopd::kPfHeadsPerWG == 0) ? g / dopd::kPfHeadsPerWG : 1;

@@ -50,7 +50,7 @@ struct PrefillArgs {
   // [x * per_xcd, (x+1) * per_xcd), so the q tiles that share a request's K/V
   // run together on one XCD and share its L2.
   int xcd_order, n_items, per_xcd, tiles_total;
-  uint8_t ord[64];     // requests by decreasing length
+  int ord[64];         // requests by decreasing length
   // With the XCD order: incl[i] = sum over positions p <= i of the order of
   // (slots per block) x (q tiles of request ord[p]); copies of cu and prefix.
   int incl[64];
@@ -164,12 +164,18 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_bf16_kernel(PrefillArgs
     const int tid = threadIdx.x, l = lane_id();
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int g = a.hq / a.hkv, kvh = h / g;
-    // (Copies in the arguments when the XCD order is used: scalar loads.)
-    const int seq0 = __builtin_amdgcn_readfirstlane(a.xcd_order ? a.cu_h[r] : a.cu[r]);
-    const int L = __builtin_amdgcn_readfirstlane(a.xcd_order ? a.cu_h[r + 1] : a.cu[r + 1]) - seq0;
-    // Cached tokens before the chunk: query row i sits at key position P + i.
-    const int P =
-        PAGED ? __builtin_amdgcn_readfirstlane(a.xcd_order ? a.prefix_h[r] : a.prefix[r]) : 0;
+    // With the XCD order the lengths come from the copies in the arguments
+    // (scalar loads, read whatever the order: a select between the two
+    // sources would become one generic load that waits on memory).
+    int seq0 = a.cu_h[min(r, kPfMaxOrdered)];
+    int L = a.cu_h[min(r + 1, kPfMaxOrdered)] - seq0;
+    int P = PAGED ? a.prefix_h[min(r, kPfMaxOrdered - 1)] : 0;
+    if (!a.xcd_order) {
+      seq0 = __builtin_amdgcn_readfirstlane(a.cu[r]);
+      L = __builtin_amdgcn_readfirstlane(a.cu[r + 1]) - seq0;
+      // Cached tokens before the chunk: query row i sits at key position P + i.
+      if constexpr (PAGED) P = __builtin_amdgcn_readfirstlane(a.prefix[r]);
+    }
     const int q0 = tile * BM;
     const int kv_end = P + min(L, q0 + BM);   // keys of this item: [0, kv_end)
     const int ntiles = (kv_end + BN - 1) / BN;
