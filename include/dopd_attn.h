@@ -86,7 +86,8 @@ typedef struct {
  *   cu_seqlens[num_reqs+1]: request r owns rows [cu[r], cu[r+1]); cu[0] = 0,
  *     non-decreasing (an empty request is allowed and produces nothing).
  *   cu_seqlens_host: identical host copy, used to size and order the launch
- *     (longest work first); it must equal the device copy.
+ *     (longest work first; with at most 64 requests the kernel takes the
+ *     lengths from it, passed by value); it must equal the device copy.
  *   lse (nullable): fp32 [T][Hq], natural-log log-sum-exp of each row's
  *     scaled scores.
  * bf16: Q.K and P.V run on bf16 MFMA with fp32 accumulation, P is rounded to
@@ -109,7 +110,8 @@ dopd_status dopd_prefill_attn(const dopd_attn_shape* shape, const void* q, const
  *   cu_seqlens[r] + i of q/out [T][Hq][d]) attends to cached positions
  *   0 .. prefix_lens[r] + i, read through page_table as in dopd_decode_attn.
  *   cu_seqlens / prefix_lens are device arrays with identical host copies
- *   (used to size and order the launch); lse (nullable) fp32 [T][Hq].
+ *   (used to size and order the launch; with at most 64 requests the kernel
+ *   takes the lengths and prefixes from them); lse (nullable) fp32 [T][Hq].
  * A chunk of one token is a decode step with context_lens = prefix_lens + 1;
  * prefix_lens = 0 with the whole prompt written first is dopd_prefill_attn.
  * bf16: the same MFMA path and rounding as dopd_prefill_attn.  Returns
