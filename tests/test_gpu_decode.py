@@ -68,3 +68,19 @@ def test_decode_fp32_matches_oracle(d):
     out, lse = G.gpu_decode(G.shape_of(w), w.q_dec, w.k_pool, w.v_pool, w.page_table, w.context_lens)
     G.assert_attention_close(out, ref, "fp32", "decode fp32")
     assert np.max(np.abs(lse - ref_lse)) < 1e-5
+
+
+@pytest.mark.parametrize("split", [0, 64])
+def test_decode_bf16_thousand_requests(split):
+    # Many more requests than the 64 lanes that look up a slice's first
+    # request at once, and than workgroups: slices span dozens of short
+    # requests; contexts 1..200 with a few long ones.
+    rng = np.random.default_rng(57)
+    ctx = rng.integers(1, 201, 1000)
+    ctx[[10, 500, 999]] = [3000, 1, 4097]
+    w = I.decode_workload("t", 58, ctx, 32, 4, 128, "bf16")
+    ref, ref_lse = oracle.decode(w.q_dec, w.k_pool, w.v_pool, w.page_table, w.context_lens, w.scale)
+    out, lse = G.gpu_decode(G.shape_of(w), w.q_dec, w.k_pool, w.v_pool, w.page_table,
+                            w.context_lens, split=split)
+    G.assert_attention_close(out, ref, "bf16", f"decode 1000 requests split={split}")
+    assert np.max(np.abs(lse - ref_lse)) < 2e-2
