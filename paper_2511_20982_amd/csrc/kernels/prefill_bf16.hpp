@@ -151,6 +151,13 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_bf16_kernel(PrefillArgs
   // global->LDS loads into another, and does not wait for them.
   __shared__ __attribute__((aligned(16))) uint16_t sK0[BN * D], sK1[BN * D];
   __shared__ __attribute__((aligned(16))) uint16_t sV0[BN * D], sV1[BN * D];
+  // Dense kernel: a copy of Q operands KS/2 .. KS-1 of every lane,
+  // [ks - KS/2][thread][8] (16 KiB at d = 128: two workgroups still fit a
+  // CU).  The diagonal steps read them from here, so those registers are free
+  // there and the compiler does not spill the Q operands to scratch (whose
+  // reloads would wait for the step's tile loads).
+  constexpr int kQLds = PAGED ? 8 : (KS / 2) * kPfThreads * 8;
+  __shared__ __attribute__((aligned(16))) uint16_t sQ[kQLds];
   auto kbuf = [&](int b) { return b ? sK1 : sK0; };
   auto vbuf = [&](int b) { return b ? sV1 : sV0; };
 
@@ -196,6 +203,11 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_bf16_kernel(PrefillArgs
         qop[ks] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(qp + 16 * ks));
     }
 
+    if constexpr (!PAGED) {  // (this lane's own slots: no barrier needed)
+#pragma unroll
+      for (int ks = KS / 2; ks < KS; ++ks)
+        *reinterpret_cast<bf16x8*>(sQ + ((ks - KS / 2) * kPfThreads + tid) * 8) = qop[ks];
+    }
     f32x16 oacc[ET];
 #pragma unroll
     for (int et = 0; et < ET; ++et)
@@ -389,6 +401,25 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_bf16_kernel(PrefillArgs
       }
       __builtin_amdgcn_sched_group_barrier(kMfma, 4, 0);
     };
+    // S^T for the diagonal steps of the dense kernel: Q operands KS/2 .. from
+    // this lane's copy in LDS.
+    auto qk_lq = [&](int buf, f32x16* s) {
+      bf16x8 ka[2][KS];
+#pragma unroll
+      for (int tt = 0; tt < 2; ++tt)
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) ka[tt][ks] = kread(buf, tt, ks);
+      zero2(s);
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        const bf16x8 qv =
+            ks < KS / 2 ? qop[ks]
+                        : *reinterpret_cast<const bf16x8*>(sQ + ((ks - KS / 2) * kPfThreads + tid) * 8);
+#pragma unroll
+        for (int tt = 0; tt < 2; ++tt)
+          s[tt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[tt][ks], qv, s[tt], 0, 0, 0);
+      }
+    };
     // O^T += V^T P^T of the tile.
     auto pv = [&](int buf) {
       bf16x8 va[4][ET];
@@ -563,7 +594,10 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_bf16_kernel(PrefillArgs
         softmax_masked(sa, j * BN);
         pv(par());
       }
-      if (wave_active && j + 1 < ntiles && (j + 1) * BN <= P + row_w + 31) qk(par() ^ 1, sa);
+      if (wave_active && j + 1 < ntiles && (j + 1) * BN <= P + row_w + 31) {
+        if constexpr (PAGED) qk(par() ^ 1, sa);
+        else qk_lq(par() ^ 1, sa);
+      }
       if (j + 1 < ntiles) clear_dead_v(par() ^ 1, j + 1);
       __syncthreads();
     };
