@@ -46,6 +46,24 @@ def test_prefill_bf16_long_prompt_sampled_rows():
     assert np.max(np.abs(lse[tok, head] - ref_lse)) < 2e-2
 
 
+def test_prefill_bf16_32k_prompt_sampled_rows():
+    # One 32768-token prompt (256 q tiles, 512 key tiles per row at the end)
+    # beside two short ones; sampled rows across the whole prompt, the last
+    # rows and a row per q-tile boundary region.
+    rng = np.random.default_rng(66)
+    lens = np.array([32768, 5, 130], np.int32)
+    hq, hkv, d = 4, 1, 128
+    q, k, v = I.prefill_batch(rng, lens, hq, hkv, d, "bf16")
+    cu = I.cu_from_lens(lens)
+    out, lse = G.gpu_prefill(G.A.make_shape(hq, hkv, d), q, k, v, cu)
+    tok = np.concatenate([np.arange(0, 32768, 997), [127, 128, 8191, 8192, 32767, 32766],
+                          cu[2] + np.arange(5), cu[3] - 1 - np.arange(8)])
+    head = np.arange(len(tok)) % hq
+    ref, ref_lse = oracle.prefill_rows(q, k, v, cu, 1 / np.sqrt(d), tok, head)
+    G.assert_attention_close(out[tok, head], ref, "bf16", "32k prompt rows")
+    assert np.max(np.abs(lse[tok, head] - ref_lse)) < 2e-2
+
+
 def test_prefill_bf16_scale_variants_and_determinism():
     rng = np.random.default_rng(62)
     lens = np.array([70, 129], np.int32)

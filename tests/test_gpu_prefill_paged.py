@@ -155,3 +155,15 @@ def test_prefill_paged_64_requests():
     out, lse = G.gpu_prefill_paged(G.A.make_shape(8, 2, 128, "bf16"), q, kp, vp, pt, cu, pre)
     G.assert_attention_close(out, ref, "bf16", "paged prefill 64 requests")
     assert np.max(np.abs(lse - ref_lse)) < 2e-2
+
+
+def test_prefill_paged_20k_prefix_sampled_rows():
+    # A chunk of 300 tokens after 20000 cached ones (1255 pages of keys per
+    # row at the end) beside a fresh 64-token chunk; sampled rows.
+    q, kp, vp, pt, cu, pre = paged_case(92, [20000, 0], [300, 64], 4, 1, 128, "bf16")
+    out, lse = G.gpu_prefill_paged(G.A.make_shape(4, 1, 128), q, kp, vp, pt, cu, pre)
+    tok = np.concatenate([np.arange(0, 300, 13), [127, 128, 299, 300, 301, 363]]).astype(np.int32)
+    head = (np.arange(len(tok)) % 4).astype(np.int32)
+    ref, ref_lse = oracle.prefill_paged(q, kp, vp, pt, cu, pre, 1 / np.sqrt(128), tok=tok, head=head)
+    G.assert_attention_close(out[tok, head], ref, "bf16", "20k prefix rows")
+    assert np.max(np.abs(lse[tok, head] - ref_lse)) < 2e-2
