@@ -46,10 +46,12 @@ KERNEL_SOURCES = ("paper_2511_20982_amd/csrc/dopd_attn.hip",
                   "paper_2511_20982_amd/csrc/kernels/kv_pack.hpp",
                   "paper_2511_20982_amd/csrc/kernels/kv_unpack.hpp")
 # Kernels behind each timed call (the decode call is a split kernel plus, when
-# some context exceeds one split, a merge kernel).
+# some context exceeds one split, a merge kernel; a chunk call with key splits
+# adds the prefill merge kernel).
 CALL_KERNELS = {"decode": ("decode_split_kernel", "decode_merge_kernel"),
                 "prefill": ("prefill_bf16_kernel<128, false>", "prefill_bf16_kernel<64, false>"),
-                "prefill_chunked": ("prefill_bf16_kernel<128, true>", "prefill_bf16_kernel<64, true>"),
+                "prefill_chunked": ("prefill_bf16_kernel<128, true>", "prefill_bf16_kernel<64, true>",
+                                    "prefill_split_merge_kernel"),
                 "kv_write": ("kv_write_kernel",),
                 "pack": ("kv_pack_kernel",), "unpack": ("kv_unpack_kernel",)}
 
@@ -252,6 +254,8 @@ def main():
     ap.add_argument("--chunk", type=int, default=512, help="chunked workload: tokens per chunk")
     ap.add_argument("--budget", type=int, default=8192,
                     help="chunked workload: tokens per call (chunks of several prompts)")
+    ap.add_argument("--splits", type=int, default=0,
+                    help="chunked workload: key splits per call (0 = automatic, 1 = none)")
     ap.add_argument("--order", choices=("decode-first", "prefill-first"), default="decode-first",
                     help="mixed step on one stream: the decode batch before the prefill, write "
                          "and pack (its tokens are the TPOT-bound ones), or after the write")
@@ -515,6 +519,12 @@ def main():
                                cu=A.to_device(cu_c), cu_h=cu_c, pre=A.to_device(pre), pre_h=pre,
                                pt=A.to_device(pt_c), n=len(sel)))
         pt = A.to_device(pt_np)
+        # One workspace serves every call (they run in order on one stream);
+        # thin calls split their keys over several workgroups.
+        ws_bytes = max(A.dopd_prefill_paged_workspace_size(shape, ch["cu_h"], ch["pre_h"], ch["n"],
+                                                           args.splits) for ch in chunks)
+        ws_buf = torch.empty(ws_bytes + 256, dtype=torch.uint8, device=dev)
+        ws = ws_buf[(-ws_buf.data_ptr()) % 256:][:ws_bytes]
         tm = {"prefill_chunked": Timer(torch, sA), "kv_write": Timer(torch, sA)}
 
         def step():
@@ -523,9 +533,10 @@ def main():
                                 sA)
             with tm["prefill_chunked"]:
                 for ch in chunks:
-                    A.dopd_prefill_paged_attn(shape, ch["q"], kp, vp, w.num_pages, ch["pt"],
-                                              stride, ch["cu"], ch["cu_h"], ch["pre"], ch["pre_h"],
-                                              ch["n"], ch["out"], None, sA)
+                    A.dopd_prefill_paged_attn_split(shape, ch["q"], kp, vp, w.num_pages,
+                                                    ch["pt"], stride, ch["cu"], ch["cu_h"],
+                                                    ch["pre"], ch["pre_h"], ch["n"], args.splits,
+                                                    ch["out"], None, ws, ws_bytes, sA)
 
         def gather_out():
             for ch in chunks:

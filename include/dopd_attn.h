@@ -126,6 +126,44 @@ dopd_status dopd_prefill_paged_attn(const dopd_attn_shape* shape, const void* q,
                                     int32_t num_reqs, void* out, float* lse, void* stream);
 
 /*
+ * dopd_prefill_paged_attn with the cached keys of each work item split over
+ * several workgroups, for calls with few work items (chunks of one or a few
+ * long prompts fill only part of the GPU): the keys of each (q tile, request,
+ * query head) item are cut into up to 16 contiguous ranges (the ranges that
+ * every row of the item sees in full, and a last one with the rest),
+ * computed by different workgroups, and a second kernel on the same stream
+ * merges their un-normalised partials (o, row max, row sum) exactly by
+ * log-sum-exp rescaling.  The same operation as dopd_prefill_paged_attn; the
+ * result differs from it by rounding only.
+ *   num_splits: 0 = automatic (splits only when the call has at most 256
+ *     work items, one per CU: about 512 / items splits, at most 8, each with
+ *     at least 8 key tiles that every row of the longest item sees), 1 = no
+ *     split, n > 1 = n splits (at most 16).  fp32, and scales <= 0, never
+ *     split.  Each split adds T * Hq * d * 8 bytes of partials written and
+ *     read back.
+ *   workspace: device memory of at least dopd_prefill_paged_workspace_size()
+ *     bytes for the same arguments, 256-byte aligned, any contents; it holds
+ *     the partials ([splits][T][Hq][d + 2] fp32).  May be null when no split
+ *     is made.  Calls that overlap in time must not share it.
+ */
+dopd_status dopd_prefill_paged_attn_split(const dopd_attn_shape* shape, const void* q,
+                                          const void* k_pool, const void* v_pool,
+                                          int32_t num_pages, const int32_t* page_table,
+                                          int32_t page_table_stride, const int32_t* cu_seqlens,
+                                          const int32_t* cu_seqlens_host,
+                                          const int32_t* prefix_lens,
+                                          const int32_t* prefix_lens_host, int32_t num_reqs,
+                                          int32_t num_splits, void* out, float* lse,
+                                          void* workspace, size_t workspace_bytes, void* stream);
+
+/* Workspace bytes dopd_prefill_paged_attn_split needs for these arguments
+ * (at least 256; 0 on bad input). */
+size_t dopd_prefill_paged_workspace_size(const dopd_attn_shape* shape,
+                                         const int32_t* cu_seqlens_host,
+                                         const int32_t* prefix_lens_host, int32_t num_reqs,
+                                         int32_t num_splits);
+
+/*
  * Paged KV write: request r appends n_r = cu_new_tokens[r+1] - cu_new_tokens[r]
  * tokens at logical positions start_pos[r] .. start_pos[r] + n_r - 1, taken
  * from rows cu_new_tokens[r] .. of k_new/v_new[total_new_tokens][Hkv][d].

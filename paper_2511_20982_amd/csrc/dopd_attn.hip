@@ -277,13 +277,55 @@ dopd_status launch_prefill_bf16(dopd::PrefillArgs a, int d, const int32_t* cu_ho
     blocks = (int64_t)a.per_xcd * dopd::kNumXcd;
   }
   if (blocks == 0) return DOPD_OK;
+  blocks *= a.nsplit;  // (nsplit > 1 only on the paged path)
+  if (blocks > INT32_MAX) return DOPD_ERR_INVALID_SHAPE;
   if (d == 64)
     hipLaunchKernelGGL((dopd::prefill_bf16_kernel<64, PAGED>), dim3((unsigned)blocks),
                        dim3(dopd::kPfThreads), 0, strm, a);
   else
     hipLaunchKernelGGL((dopd::prefill_bf16_kernel<128, PAGED>), dim3((unsigned)blocks),
                        dim3(dopd::kPfThreads), 0, strm, a);
+  const dopd_status st = launch_status();
+  if (st != DOPD_OK || a.nsplit == 1) return st;
+  const int64_t threads = (int64_t)a.part_rows * a.hq * (d / 4);
+  const unsigned merge_blocks = (unsigned)((threads + 255) / 256);
+  if (d == 64)
+    hipLaunchKernelGGL(dopd::prefill_split_merge_kernel<64>, dim3(merge_blocks), dim3(256), 0, strm, a);
+  else
+    hipLaunchKernelGGL(dopd::prefill_split_merge_kernel<128>, dim3(merge_blocks), dim3(256), 0, strm, a);
   return launch_status();
+}
+
+// Key splits of the paged prefill: the requested count (at most kPfMaxSplits),
+// or automatically, when the call has at most one work item per CU, about
+// kPfSlots / items splits (at most kPfAutoSplits), each split of the longest
+// item keeping at least 8 key tiles that every row sees.  Each split adds
+// T * Hq * d * 8 bytes of fp32 partials written and read back, which costs
+// more than it gains once the items fill the CUs.
+constexpr int kPfMaxSplits = 16;
+constexpr int kPfAutoSplits = 8;
+int prefill_paged_splits(const dopd_attn_shape* s, const int32_t* cu_host,
+                         const int32_t* prefix_host, int32_t nreq, int32_t num_splits) {
+  if (s->dtype != DOPD_BF16 || !(s->softmax_scale > 0.f)) return 1;
+  if (num_splits > 0) return std::min(num_splits, kPfMaxSplits);
+  int64_t items = 0, max_full = 0;
+  for (int32_t r = 0; r < nreq; ++r) {
+    const int64_t len = cu_host[r + 1] - cu_host[r];
+    const int64_t tiles = (len + dopd::kPfBM - 1) / dopd::kPfBM;
+    items += tiles * s->num_q_heads;
+    if (tiles > 0)
+      max_full = std::max<int64_t>(max_full, (prefix_host[r] + (tiles - 1) * dopd::kPfBM) / dopd::kPfBN);
+  }
+  if (items == 0 || items > dopd::kPfSlots / 2) return 1;
+  int64_t n = dopd::kPfSlots / items;
+  n = std::min<int64_t>(n, 1 + max_full / 8);
+  return (int)std::max<int64_t>(1, std::min<int64_t>(n, kPfAutoSplits));
+}
+
+size_t prefill_paged_ws_bytes(const dopd_attn_shape* s, int64_t T, int nsplit) {
+  if (nsplit <= 1) return 0;
+  const size_t rows = (size_t)nsplit * T * s->num_q_heads;
+  return align256(rows * s->head_dim * sizeof(float)) + align256(rows * 2 * sizeof(float));
 }
 
 dopd::PrefillArgs prefill_args(const dopd_attn_shape* s, const void* q, void* out, float* lse,
@@ -297,6 +339,7 @@ dopd::PrefillArgs prefill_args(const dopd_attn_shape* s, const void* q, void* ou
   a.hq = s->num_q_heads;
   a.hkv = s->num_kv_heads;
   a.scale_log2 = s->softmax_scale * dopd::kLog2e;
+  a.nsplit = 1;
   return a;
 }
 
@@ -336,15 +379,17 @@ dopd_status dopd_prefill_attn(const dopd_attn_shape* s, const void* q, const voi
   return launch_prefill_bf16<false>(a, d, cu_host, nullptr, nreq, strm);
 }
 
-dopd_status dopd_prefill_paged_attn(const dopd_attn_shape* s, const void* q, const void* k_pool,
-                                    const void* v_pool, int32_t num_pages,
-                                    const int32_t* page_table, int32_t pt_stride,
-                                    const int32_t* cu, const int32_t* cu_host,
-                                    const int32_t* prefix, const int32_t* prefix_host,
-                                    int32_t nreq, void* out, float* lse, void* stream) {
+// dopd_prefill_paged_attn(_split): checks, then the fp32 kernel or the bf16
+// kernel with num_splits key splits (1: no workspace needed).
+static dopd_status prefill_paged_impl(const dopd_attn_shape* s, const void* q, const void* k_pool,
+                               const void* v_pool, int32_t num_pages, const int32_t* page_table,
+                               int32_t pt_stride, const int32_t* cu, const int32_t* cu_host,
+                               const int32_t* prefix, const int32_t* prefix_host, int32_t nreq,
+                               int32_t num_splits, void* out, float* lse, void* workspace,
+                               size_t workspace_bytes, void* stream) {
   dopd_status st = check_shape_no_fp8(s);
   if (st != DOPD_OK) return st;
-  if (nreq < 0 || num_pages < 0 || pt_stride < 0) return DOPD_ERR_INVALID_SHAPE;
+  if (nreq < 0 || num_pages < 0 || pt_stride < 0 || num_splits < 0) return DOPD_ERR_INVALID_SHAPE;
   if (nreq == 0) return DOPD_OK;
   if (!q || !k_pool || !v_pool || !page_table || !cu || !cu_host || !prefix || !prefix_host ||
       !out)
@@ -379,7 +424,57 @@ dopd_status dopd_prefill_paged_attn(const dopd_attn_shape* s, const void* q, con
   a.page_table = page_table;
   a.prefix = prefix;
   a.pt_stride = pt_stride;
+  const int nsplit = num_splits == 1 ? 1 : prefill_paged_splits(s, cu_host, prefix_host, nreq,
+                                                                num_splits);
+  if (nsplit > 1) {
+    if (T * hq * (int64_t)nsplit > INT32_MAX / 2) return DOPD_ERR_INVALID_SHAPE;
+    if (!workspace) return DOPD_ERR_NULL_POINTER;
+    if (workspace_bytes < prefill_paged_ws_bytes(s, T, nsplit)) return DOPD_ERR_WORKSPACE_TOO_SMALL;
+    if ((reinterpret_cast<uintptr_t>(workspace) & 255) != 0) return DOPD_ERR_INVALID_SHAPE;
+    const size_t rows = (size_t)nsplit * T * hq;
+    a.nsplit = nsplit;
+    a.part_rows = (int)T;
+    a.part_o = static_cast<float*>(workspace);
+    a.part_ml = reinterpret_cast<float*>(static_cast<char*>(workspace) +
+                                         align256(rows * d * sizeof(float)));
+  }
   return launch_prefill_bf16<true>(a, d, cu_host, prefix_host, nreq, strm);
+}
+
+dopd_status dopd_prefill_paged_attn(const dopd_attn_shape* s, const void* q, const void* k_pool,
+                                    const void* v_pool, int32_t num_pages,
+                                    const int32_t* page_table, int32_t pt_stride,
+                                    const int32_t* cu, const int32_t* cu_host,
+                                    const int32_t* prefix, const int32_t* prefix_host,
+                                    int32_t nreq, void* out, float* lse, void* stream) {
+  return prefill_paged_impl(s, q, k_pool, v_pool, num_pages, page_table, pt_stride, cu, cu_host,
+                            prefix, prefix_host, nreq, 1, out, lse, nullptr, 0, stream);
+}
+
+size_t dopd_prefill_paged_workspace_size(const dopd_attn_shape* s, const int32_t* cu_host,
+                                         const int32_t* prefix_host, int32_t nreq,
+                                         int32_t num_splits) {
+  if (check_shape_no_fp8(s) != DOPD_OK || nreq < 0 || num_splits < 0) return 0;
+  if (nreq == 0) return 256;
+  if (!cu_host || !prefix_host || cu_host[0] != 0) return 0;
+  for (int32_t r = 0; r < nreq; ++r)
+    if (cu_host[r + 1] < cu_host[r] || prefix_host[r] < 0) return 0;
+  const int nsplit = num_splits == 1 ? 1 : prefill_paged_splits(s, cu_host, prefix_host, nreq,
+                                                                num_splits);
+  return std::max<size_t>(256, prefill_paged_ws_bytes(s, cu_host[nreq], nsplit));
+}
+
+dopd_status dopd_prefill_paged_attn_split(const dopd_attn_shape* s, const void* q,
+                                          const void* k_pool, const void* v_pool,
+                                          int32_t num_pages, const int32_t* page_table,
+                                          int32_t pt_stride, const int32_t* cu,
+                                          const int32_t* cu_host, const int32_t* prefix,
+                                          const int32_t* prefix_host, int32_t nreq,
+                                          int32_t num_splits, void* out, float* lse,
+                                          void* workspace, size_t workspace_bytes, void* stream) {
+  return prefill_paged_impl(s, q, k_pool, v_pool, num_pages, page_table, pt_stride, cu, cu_host,
+                            prefix, prefix_host, nreq, num_splits, out, lse, workspace,
+                            workspace_bytes, stream);
 }
 
 // ---------------------------------------------------------------- kv write

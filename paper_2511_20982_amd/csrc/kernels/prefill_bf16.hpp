@@ -64,10 +64,22 @@ struct PrefillArgs {
   const int32_t* page_table;  // [nreq][pt_stride]
   const int32_t* prefix;      // [nreq]
   int pt_stride;
+  // Key splits of the paged kernel (nsplit > 1): workgroup b computes split
+  // b % nsplit of item b / nsplit, keys of tiles [t_s, t_{s+1}) with
+  // t_s = min(s * ntiles / nsplit, nfull) (the last split also takes every
+  // tile a row of the item does not see in full), and writes the
+  // un-normalised (o, m, l) of its rows to split slot s of part_o / part_ml,
+  // [nsplit][T][Hq][D] and [nsplit][T][Hq][2] (m in the exp2 domain); the
+  // merge kernel combines them.
+  int nsplit;
+  float* part_o;
+  float* part_ml;
+  int part_rows;              // T of the call
 };
 
 constexpr int kPfMaxOrdered = 64;
 constexpr int kNumXcd = 8;
+constexpr int kPfSlots = 512;  // resident workgroups: two per CU on 256 CUs
 
 constexpr int kPfBM = 128;          // query rows per workgroup (32 per wave)
 constexpr int kPfHeadsPerWG = 1;    // heads per workgroup
@@ -161,8 +173,10 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_bf16_kernel(PrefillArgs
   auto kbuf = [&](int b) { return b ? sK1 : sK0; };
   auto vbuf = [&](int b) { return b ? sV1 : sV0; };
 
+  const int split = PAGED ? (int)blockIdx.x % a.nsplit : 0;
   int tile, r, h;
-  if (!pf_find_item(a, blockIdx.x, tile, r, h)) return;  // uniform across the workgroup
+  if (!pf_find_item(a, PAGED ? (int)blockIdx.x / a.nsplit : (int)blockIdx.x, tile, r, h))
+    return;  // uniform across the workgroup
   // The item is wave-uniform; say so, so that what derives from it stays scalar.
   tile = __builtin_amdgcn_readfirstlane(tile);
   r = __builtin_amdgcn_readfirstlane(r);
@@ -186,6 +200,16 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_bf16_kernel(PrefillArgs
     const int q0 = tile * BM;
     const int kv_end = P + min(L, q0 + BM);   // keys of this item: [0, kv_end)
     const int ntiles = (kv_end + BN - 1) / BN;
+    // Tiles every row of the item sees in full (positive scales only).
+    const int nfull = a.scale_log2 > 0.f ? (P + q0) / BN : 0;
+    // Key tiles of this workgroup: [jb, je) (all of them without splits).
+    int jb = 0, je = ntiles;
+    if constexpr (PAGED) {
+      if (a.nsplit > 1) {
+        jb = split == 0 ? 0 : min(split * ntiles / a.nsplit, nfull);
+        je = split + 1 == a.nsplit ? ntiles : min((split + 1) * ntiles / a.nsplit, nfull);
+      }
+    }
     const int row_w = q0 + 32 * w;            // first query row of this wave
     const int myq = row_w + (l & 31);         // this lane's query row
     const bool wave_active = row_w < L;
@@ -524,40 +548,40 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_bf16_kernel(PrefillArgs
     // free buffers, computes S^T(j + 1) with the softmax of tile j, then
     // O^T += V^T P^T of tile j; one barrier (which also waits for the loads).
     if constexpr (PAGED) {
-      const int p0 = __builtin_amdgcn_readfirstlane(page_of(0));
-      const int p1 = __builtin_amdgcn_readfirstlane(page_of(1));
-      pid_k = p0;
-      load_k(0, 0);
-      pid_k = p1;
-      if (ntiles > 1) load_k(1, BN);
-      pid_v = p0;
-      load_v(0, 0);
-      clear_dead_v(0, 0);
-      // the first step loads K(2) and V(1); the id of tile 3 is read ahead
-      pid_v = p1;
-      pid_k = __builtin_amdgcn_readfirstlane(page_of(2));
-      pid_ahead = page_of(3);
+      if (jb < je) {  // (an empty split loads and computes nothing)
+        const int p0 = __builtin_amdgcn_readfirstlane(page_of(jb));
+        const int p1 = __builtin_amdgcn_readfirstlane(page_of(jb + 1));
+        pid_k = p0;
+        load_k(0, 0);
+        pid_k = p1;
+        if (je > jb + 1) load_k(1, BN);
+        pid_v = p0;
+        load_v(0, 0);
+        clear_dead_v(0, jb);
+        // the first step loads K(jb + 2) and V(jb + 1); the id of tile jb + 3 is read ahead
+        pid_v = p1;
+        pid_k = __builtin_amdgcn_readfirstlane(page_of(jb + 2));
+        pid_ahead = page_of(jb + 3);
+      }
     } else {
       load_k(0, 0);
       if (ntiles > 1) load_k(1, BN);
       load_v(0, 0);
     }
     __syncthreads();
-    if (wave_active) qk(0, sa);  // every active row sees key 0
+    if (wave_active && jb < je) qk(0, sa);  // every active row sees key jb * BN
     // The steady-state steps form p against the running max without taking
-    // the tile's max, so start it at the first tile's max (tile 0 is
-    // unmasked there).
-    // Tiles every row of the item sees in full (positive scales only).
-    const int nfull = pos_scale ? (P + q0) / BN : 0;
-    if (wave_active && nfull > 0) m_run = row_max(sa);
+    // the tile's max, so start it at the first tile's max (unmasked there).
+    if (wave_active && jb < nfull && jb < je) m_run = row_max(sa);
     // The first step's prefetch writes K tile 2 into K buffer 0: every wave
     // must have read tile 0 from it first.
     __syncthreads();
 
-    int j = 0;
+    int j = jb;
+    const int nfe = min(nfull, je);  // end of the full tiles of this workgroup
     auto prefetch = [&](int jj, auto par) {  // K(jj + 2) -> K buffer par, V(jj + 1) -> V buffer par ^ 1
-      if (jj + 2 < ntiles) load_k(par(), (jj + 2) * BN);
-      if (jj + 1 < ntiles) load_v(par() ^ 1, (jj + 1) * BN);
+      if (jj + 2 < je) load_k(par(), (jj + 2) * BN);
+      if (jj + 1 < je) load_v(par() ^ 1, (jj + 1) * BN);
       if constexpr (PAGED) {  // next step: K(jj + 3), V(jj + 2); read the id of tile jj + 4
         pid_v = pid_k;
         pid_k = __builtin_amdgcn_readfirstlane(pid_ahead);  // landed at the last barrier
@@ -572,16 +596,16 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_bf16_kernel(PrefillArgs
         half_qk(sc, sn, par() ^ 1);
         pv(par());
       }
-      if (j + 1 < ntiles) clear_dead_v(par() ^ 1, j + 1);
+      if (j + 1 < je) clear_dead_v(par() ^ 1, j + 1);
       __syncthreads();
     };
-    for (; j + 1 < nfull; j += 2) {
+    for (; j + 1 < nfe; j += 2) {
       step_full(sa, sb, even);
       ++j;
       step_full(sb, sa, odd);
       --j;
     }
-    if (j < nfull) {
+    if (j < nfe) {
       step_full(sa, sb, even);
       ++j;
 #pragma unroll
@@ -594,19 +618,36 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_bf16_kernel(PrefillArgs
         softmax_masked(sa, j * BN);
         pv(par());
       }
-      if (wave_active && j + 1 < ntiles && (j + 1) * BN <= P + row_w + 31) {
+      if (wave_active && j + 1 < je && (j + 1) * BN <= P + row_w + 31) {
         if constexpr (PAGED) qk(par() ^ 1, sa);
         else qk_lq(par() ^ 1, sa);
       }
-      if (j + 1 < ntiles) clear_dead_v(par() ^ 1, j + 1);
+      if (j + 1 < je) clear_dead_v(par() ^ 1, j + 1);
       __syncthreads();
     };
-    for (; j < ntiles; ++j) {
-      if (j & 1) step_tail(odd);
+    for (; j < je; ++j) {  // tile j sits in buffer (j - jb) % 2
+      if ((j - jb) & 1) step_tail(odd);
       else step_tail(even);
     }
     if (!wave_active) return;
     float l_tot = l_run + __shfl_xor(l_run, 32, 64);
+    if constexpr (PAGED) {
+      if (a.nsplit > 1) {  // partial (o, m, l) of this split; the merge kernel finishes
+        if (myq < L) {
+          const int64_t row = ((int64_t)split * a.part_rows + seq0 + myq) * a.hq + h;
+          float* po = a.part_o + row * D + 4 * hi;
+#pragma unroll
+          for (int et = 0; et < ET; ++et)
+#pragma unroll
+            for (int gq = 0; gq < 4; ++gq)
+              *reinterpret_cast<f32x4*>(po + 32 * et + 8 * gq) =
+                  f32x4{oacc[et][4 * gq], oacc[et][4 * gq + 1], oacc[et][4 * gq + 2],
+                        oacc[et][4 * gq + 3]};
+          if (hi == 0) *reinterpret_cast<float2*>(a.part_ml + row * 2) = float2{m_run, l_tot};
+        }
+        return;
+      }
+    }
     const float inv = 1.f / l_tot;
     // The wave's 32 x D output block goes through LDS (no load is in flight
     // and every wave is past its last tile read: the loop's last barrier), so
@@ -644,6 +685,34 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_bf16_kernel(PrefillArgs
     if (a.lse && hi == 0 && myq < L)
       a.lse[(int64_t)(seq0 + myq) * a.hq + h] = (m_run + __log2f(l_tot)) * kLn2;
   }
+}
+
+// Combines the key splits of the paged prefill.  Thread = one 4-dim chunk of
+// one (row, head): M = max_s m_s, L = sum_s 2^(m_s - M) l_s,
+// o = sum_s 2^(m_s - M) o~_s / L, lse = (M + log2 L) ln 2, splits in order.
+template <int D>
+__global__ __launch_bounds__(256) void prefill_split_merge_kernel(PrefillArgs a) {
+  const int64_t rowheads = (int64_t)a.part_rows * a.hq;
+  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int64_t rh = idx / (D / 4);
+  const int e0 = 4 * (int)(idx % (D / 4));
+  if (rh >= rowheads) return;
+  float M = -INFINITY;
+  for (int s = 0; s < a.nsplit; ++s) M = fmaxf(M, a.part_ml[(s * rowheads + rh) * 2]);
+  float L = 0.f;
+  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+  for (int s = 0; s < a.nsplit; ++s) {
+    const float2 ml = *reinterpret_cast<const float2*>(a.part_ml + (s * rowheads + rh) * 2);
+    const float wgt = __builtin_amdgcn_exp2f(ml.x - M);  // an empty split has m = -inf -> 0
+    L += wgt * ml.y;
+    acc += *reinterpret_cast<const f32x4*>(a.part_o + (s * rowheads + rh) * D + e0) * wgt;
+  }
+  const float inv = 1.f / L;
+  u32x2 x;
+  x[0] = pack_bf16x2(acc[0] * inv, acc[1] * inv);
+  x[1] = pack_bf16x2(acc[2] * inv, acc[3] * inv);
+  *reinterpret_cast<u32x2*>(a.out + rh * D + e0) = x;
+  if (a.lse && e0 == 0) a.lse[rh] = (M + __log2f(L)) * kLn2;
 }
 
 }  // namespace dopd

@@ -72,17 +72,30 @@ def gpu_prefill(shape, q, k, v, cu, with_lse=True, stream=None):
 
 
 def gpu_prefill_paged(shape, q, k_pool, v_pool, page_table, cu, prefix, with_lse=True,
-                      pools_dev=None):
+                      pools_dev=None, splits=None):
+    """dopd_prefill_paged_attn, or with splits = n the split entry point with n
+    (0: automatic) key splits and a NaN-filled workspace whose guard bytes
+    are checked afterwards."""
     if pools_dev is None:
         pools_dev = (A.to_device(k_pool), A.to_device(v_pool))
     kp, vp = pools_dev
     qd = A.to_device(q)
     out, obuf, margin = guarded(qd.shape, qd.dtype)
     lse = torch.full((q.shape[0], q.shape[1]), float("nan"), device=DEV) if with_lse else None
-    A.dopd_prefill_paged_attn(shape, qd, kp, vp, kp.shape[0], A.to_device(page_table),
-                              page_table.shape[1], A.to_device(cu), cu,
-                              A.to_device(np.asarray(prefix, np.int32)), prefix, len(cu) - 1,
-                              out, lse)
+    prefix = np.asarray(prefix, np.int32)
+    args = (shape, qd, kp, vp, kp.shape[0], A.to_device(page_table), page_table.shape[1],
+            A.to_device(cu), cu, A.to_device(prefix), prefix, len(cu) - 1)
+    if splits is None:
+        A.dopd_prefill_paged_attn(*args, out, lse)
+    else:
+        n = A.dopd_prefill_paged_workspace_size(shape, cu, prefix, len(cu) - 1, splits)
+        assert n >= 256 and n % 256 == 0
+        wbuf = torch.full((n + 4096 + 256,), 0xFF, dtype=torch.uint8, device=DEV)
+        off = (-wbuf.data_ptr()) % 256
+        ws = wbuf[off:off + n]
+        A.dopd_prefill_paged_attn_split(*args, splits, out, lse, ws, n)
+        torch.cuda.synchronize()
+        assert bool((wbuf[off + n:] == 0xFF).all()), "paged prefill split wrote past its workspace"
     torch.cuda.synchronize()
     assert canary_intact(obuf, margin, out.numel() * out.element_size()), \
         "paged prefill wrote out of bounds"

@@ -199,3 +199,52 @@ def test_fp8_host_validation(lib):
     lens = np.array([40, 600], np.int32)
     assert lib.dopd_kv_pack_for_handoff(C.byref(f8), 1, p, p, 10, p, 8, p, p, A._hptr(lens), p, 2,
                                         p, None) == A.DOPD_ERR_INVALID_SHAPE   # 600 > 8 pages
+
+
+def _align256(n):
+    return (n + 255) // 256 * 256
+
+
+def test_prefill_paged_split_workspace_size(lib):
+    s = _shape()  # 8 query heads, d = 128
+    cu = np.array([0, 40, 41], np.int32)
+    pre = np.array([600, 0], np.int32)
+    ws = A.dopd_prefill_paged_workspace_size
+
+    def need(n):  # [n][T][Hq][d] partial outputs, then [n][T][Hq][2] (m, l)
+        rows = n * 41 * 8
+        return _align256(rows * 128 * 4) + _align256(rows * 2 * 4)
+    # 2 q tiles x 8 heads = 16 items: automatic wants ceil(1024 / 16) = 64
+    # splits, capped at 1 + (600 // 64) // 8 = 2 by the fully seen key tiles
+    assert ws(s, cu, pre, 2, 0) == need(2)
+    assert ws(s, cu, pre, 2, 3) == need(3)
+    assert ws(s, cu, pre, 2, 40) == need(16)                    # at most 16 splits
+    assert ws(s, cu, pre, 2, 1) == 256                          # no split: nothing needed
+    assert ws(_shape(dtype="fp32"), cu, pre, 2, 8) == 256       # fp32 never splits
+    assert ws(A.make_shape(8, 2, 128, "bf16", 0.0), cu, pre, 2, 8) == 256  # nor scale <= 0
+    assert ws(s, cu, pre, 0, 0) == 256
+    assert ws(s, cu, pre, 2, -1) == 0
+    assert ws(s, np.array([0, 40, 30], np.int32), pre, 2, 0) == 0
+    assert ws(s, cu, np.array([-1, 0], np.int32), 2, 0) == 0
+    # a call with many work items (600 q tiles x 8 heads) is not split
+    big_cu = np.array([0, 600 * 128], np.int32)
+    assert ws(s, big_cu, np.array([5000], np.int32), 1, 0) == 256
+
+
+def test_prefill_paged_split_host_validation(lib):
+    s = _shape()
+    p = C.c_void_p(FAKE)
+    cu = np.array([0, 40, 41], np.int32)
+    pre = np.array([600, 0], np.int32)
+    H = A._hptr
+    need = A.dopd_prefill_paged_workspace_size(s, cu, pre, 2, 4)
+
+    def call(splits, ws, nbytes, stride=64):
+        return lib.dopd_prefill_paged_attn_split(
+            C.byref(s), p, p, p, 100, p, stride, p, H(cu), p, H(pre), 2, splits, p, None,
+            None if ws is None else C.c_void_p(ws), nbytes, None)
+    assert call(4, None, need) == A.DOPD_ERR_NULL_POINTER
+    assert call(4, FAKE, need - 1) == A.DOPD_ERR_WORKSPACE_TOO_SMALL
+    assert call(4, FAKE + 64, need) == A.DOPD_ERR_INVALID_SHAPE   # not 256-byte aligned
+    assert call(-1, FAKE, need) == A.DOPD_ERR_INVALID_SHAPE
+    assert call(4, FAKE, need, stride=39) == A.DOPD_ERR_INVALID_SHAPE  # table too narrow

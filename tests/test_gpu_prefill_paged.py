@@ -167,3 +167,55 @@ def test_prefill_paged_20k_prefix_sampled_rows():
     ref, ref_lse = oracle.prefill_paged(q, kp, vp, pt, cu, pre, 1 / np.sqrt(128), tok=tok, head=head)
     G.assert_attention_close(out[tok, head], ref, "bf16", "20k prefix rows")
     assert np.max(np.abs(lse[tok, head] - ref_lse)) < 2e-2
+
+
+# Key splits (dopd_prefill_paged_attn_split): long prefixes beside short
+# ones, ragged chunks; with 16 splits the short items get empty middle splits.
+SPLIT_PREFIX = [3000, 1, 777, 129, 40]
+SPLIT_CHUNK = [130, 65, 1, 200, 300]
+
+
+@pytest.mark.parametrize("splits", [0, 2, 3, 8, 16])
+@pytest.mark.parametrize("d", [128, 64])
+def test_prefill_paged_split_matches_oracle(splits, d):
+    q, kp, vp, pt, cu, pre = paged_case(93 + d, SPLIT_PREFIX, SPLIT_CHUNK, 8, 2, d, "bf16")
+    sh = G.A.make_shape(8, 2, d)
+    ref, ref_lse = oracle.prefill_paged(q, kp, vp, pt, cu, pre, 1 / np.sqrt(d))
+    out, lse = G.gpu_prefill_paged(sh, q, kp, vp, pt, cu, pre, splits=splits)
+    G.assert_attention_close(out, ref, "bf16", f"paged prefill splits={splits} d={d}")
+    assert np.max(np.abs(lse - ref_lse)) < 2e-2
+    one, one_lse = G.gpu_prefill_paged(sh, q, kp, vp, pt, cu, pre)
+    G.assert_attention_close(out, one, "bf16", f"splits={splits} vs unsplit")
+    assert np.max(np.abs(lse - one_lse)) < 2e-2
+
+
+def test_prefill_paged_split_one_is_the_unsplit_kernel():
+    q, kp, vp, pt, cu, pre = paged_case(95, SPLIT_PREFIX, SPLIT_CHUNK, 8, 2, 128, "bf16")
+    sh = G.A.make_shape(8, 2, 128)
+    out1, lse1 = G.gpu_prefill_paged(sh, q, kp, vp, pt, cu, pre, splits=1)
+    out2, lse2 = G.gpu_prefill_paged(sh, q, kp, vp, pt, cu, pre)
+    assert np.array_equal(out1, out2) and np.array_equal(lse1, lse2)
+
+
+def test_prefill_paged_split_scale_variants_do_not_split():
+    q, kp, vp, pt, cu, pre = paged_case(96, [700, 5], [90, 33], 4, 2, 64, "bf16")
+    for scale in (0.0, -0.2):
+        sh = G.A.make_shape(4, 2, 64, "bf16", scale)
+        assert G.A.dopd_prefill_paged_workspace_size(sh, cu, pre, 2, 8) == 256
+        ref, _ = oracle.prefill_paged(q, kp, vp, pt, cu, pre, scale)
+        out, _ = G.gpu_prefill_paged(sh, q, kp, vp, pt, cu, pre, with_lse=False, splits=8)
+        G.assert_attention_close(out, ref, "bf16", f"split call, scale={scale}")
+
+
+def test_prefill_paged_split_20k_prefix_sampled_rows():
+    # The automatic split count on one 300-token chunk after 20000 cached
+    # tokens (12 items: splits), sampled rows.
+    q, kp, vp, pt, cu, pre = paged_case(97, [20000], [300], 4, 1, 128, "bf16")
+    sh = G.A.make_shape(4, 1, 128)
+    assert G.A.dopd_prefill_paged_workspace_size(sh, cu, pre, 1, 0) > 256
+    out, lse = G.gpu_prefill_paged(sh, q, kp, vp, pt, cu, pre, splits=0)
+    tok = np.concatenate([np.arange(0, 300, 11), [127, 128, 255, 256, 299]]).astype(np.int32)
+    head = (np.arange(len(tok)) % 4).astype(np.int32)
+    ref, ref_lse = oracle.prefill_paged(q, kp, vp, pt, cu, pre, 1 / np.sqrt(128), tok=tok, head=head)
+    G.assert_attention_close(out[tok, head], ref, "bf16", "split 20k prefix rows")
+    assert np.max(np.abs(lse[tok, head] - ref_lse)) < 2e-2
