@@ -76,11 +76,13 @@ def test_prefill_paged_long_prefix_sampled_rows():
     assert np.max(np.abs(lse[tok, head] - ref_lse)) < 2e-2
 
 
+@pytest.mark.parametrize("splits", [None, 4])
 @pytest.mark.parametrize("pieces", [[300], [1, 299], [64, 64, 64, 108], [5, 130, 1, 164]])
-def test_chunked_prefill_equals_one_shot_on_gpu(pieces):
+def test_chunked_prefill_equals_one_shot_on_gpu(pieces, splits):
     """The prompt written and attended chunk by chunk on the GPU (dopd_kv_write
-    at start_pos = cached tokens, then dopd_prefill_paged_attn) agrees with the
-    one-shot dopd_prefill_attn and with the oracle."""
+    at start_pos = cached tokens, then dopd_prefill_paged_attn, or the split
+    entry point with 4 key splits) agrees with the one-shot dopd_prefill_attn
+    and with the oracle."""
     rng = np.random.default_rng(84)
     hq, hkv, d, L = 8, 2, 128, int(sum(pieces))
     q, k, v = I.prefill_batch(rng, np.array([L]), hq, hkv, d, "bf16")
@@ -97,7 +99,8 @@ def test_chunked_prefill_equals_one_shot_on_gpu(pieces):
                           G.A.to_device(pt), pt.shape[1], G.A.to_device(I.cu_from_lens([n])),
                           G.A.to_device(np.array([done], np.int32)), 1, n)
         out, _ = G.gpu_prefill_paged(sh, q[rows], None, None, pt, I.cu_from_lens([n]),
-                                     np.array([done], np.int32), pools_dev=(kpd, vpd))
+                                     np.array([done], np.int32), pools_dev=(kpd, vpd),
+                                     splits=splits)
         outs.append(out)
         done += n
     chunked = np.concatenate(outs)
