@@ -222,3 +222,13 @@ def test_prefill_paged_split_20k_prefix_sampled_rows():
     ref, ref_lse = oracle.prefill_paged(q, kp, vp, pt, cu, pre, 1 / np.sqrt(128), tok=tok, head=head)
     G.assert_attention_close(out[tok, head], ref, "bf16", "split 20k prefix rows")
     assert np.max(np.abs(lse[tok, head] - ref_lse)) < 2e-2
+
+
+def test_prefill_paged_split_gqa_without_lse():
+    # 28 query heads over 4 KV heads, 4 key splits, no lse output (the form
+    # the chunked bench calls), against the oracle.
+    q, kp, vp, pt, cu, pre = paged_case(98, [1500, 64, 0], [200, 37, 90], 28, 4, 128, "bf16")
+    sh = G.A.make_shape(28, 4, 128)
+    ref, _ = oracle.prefill_paged(q, kp, vp, pt, cu, pre, 1 / np.sqrt(128))
+    out, _ = G.gpu_prefill_paged(sh, q, kp, vp, pt, cu, pre, with_lse=False, splits=4)
+    G.assert_attention_close(out, ref, "bf16", "split GQA 28/4 without lse")
