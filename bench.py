@@ -365,7 +365,7 @@ def main():
             if dec_first:
                 decode_call()
             with tm["prefill"]:
-                A.dopd_prefill_attn(shape, q, k, v, out_p, None, cu, w.cu_seqlens, n_pre, sA)
+                A.dopd_prefill_attn(shape, q, k, v, out_p, None, cu, w.cu_seqlens, n_pre, stream=sA)
             if args.streams == 2:
                 decode_call()
             with tm["kv_write"]:
@@ -577,7 +577,7 @@ def main():
 
         def step():
             with tm["prefill"]:
-                A.dopd_prefill_attn(shape, q, k, v, out_p, None, cu, w.cu_seqlens, n_pre, sA)
+                A.dopd_prefill_attn(shape, q, k, v, out_p, None, cu, w.cu_seqlens, n_pre, stream=sA)
             with tm["kv_write"]:
                 write()
 

@@ -64,6 +64,7 @@ enum {
   DOPD_ERR_NULL_POINTER = 1,       /* a required pointer is NULL                 */
   DOPD_ERR_INVALID_SHAPE = 2,      /* counts, lengths or head ratio out of range */
   DOPD_ERR_UNSUPPORTED = 3,        /* dtype / head_dim / page_size not built     */
+  DOPD_ERR_UNSUPPORTED_DTYPE = 3,  /* the same code under its narrower name      */
   DOPD_ERR_WORKSPACE_TOO_SMALL = 4,
   DOPD_ERR_HIP = 5
 };
@@ -80,8 +81,13 @@ typedef struct {
 } dopd_attn_shape;
 
 /*
- * Variable-length causal prefill attention (Eq. 1 over each prompt, causal,
- * no prefix: token i of a request attends to tokens 0..i of the same request).
+ * Variable-length causal prefill attention.
+ * Paper: Eq. 1 (attention) over each prompt of a P-instance's batch; the
+ * batch of prompts with per-request input lengths is the unit of Alg. 1
+ * (Sec. IV-C); prefill is the compute-bound phase (Sec. I, Sec. IV-C) whose
+ * cost grows with the square of the input length (Eq. 2).
+ * Causal, no prefix: token i of a request attends to tokens 0..i of the same
+ * request.
  *   q[T][Hq][d], k/v[T][Hkv][d], out[T][Hq][d]; T = cu_seqlens_host[num_reqs].
  *   cu_seqlens[num_reqs+1]: request r owns rows [cu[r], cu[r+1]); cu[0] = 0,
  *     non-decreasing (an empty request is allowed and produces nothing).
@@ -90,18 +96,37 @@ typedef struct {
  *     lengths from it, passed by value); it must equal the device copy.
  *   lse (nullable): fp32 [T][Hq], natural-log log-sum-exp of each row's
  *     scaled scores.
+ *   workspace / workspace_bytes: device memory of at least
+ *     dopd_prefill_workspace_size() bytes for the same arguments.  The
+ *     present kernels keep no state outside q/k/v/out/lse, so that size is
+ *     0 and workspace may be NULL; a non-NULL workspace must be 256-byte
+ *     aligned.
  * bf16: Q.K and P.V run on bf16 MFMA with fp32 accumulation, P is rounded to
  * bf16 before the P.V product.  fp32: plain fp32 arithmetic.
  */
 dopd_status dopd_prefill_attn(const dopd_attn_shape* shape, const void* q, const void* k,
                               const void* v, void* out, float* lse, const int32_t* cu_seqlens,
-                              const int32_t* cu_seqlens_host, int32_t num_reqs, void* stream);
+                              const int32_t* cu_seqlens_host, int32_t num_reqs, void* workspace,
+                              size_t workspace_bytes, void* stream);
 
 /*
- * Chunk prefill over the paged cache: the prefill of a request that already
- * holds cached tokens, i.e. one chunk of a prompt processed in chunks (chunked
- * prefill, Sec. III-A) or an ultra-short prefill merged into a D-instance's
- * work next to decode (PD-aggregation, Sec. V-E).  Eq. 1 over the cache,
+ * Workspace bytes dopd_prefill_attn needs for these arguments.
+ * Paper: as dopd_prefill_attn (Eq. 1 over the request batch of Alg. 1).
+ * Returns 0: the dense prefill needs none (its work list is derived from
+ * cu_seqlens_host and passed by value).  Returns 0 on bad input as well;
+ * dopd_prefill_attn reports those itself.
+ */
+size_t dopd_prefill_workspace_size(const dopd_attn_shape* shape, const int32_t* cu_seqlens_host,
+                                   int32_t num_reqs);
+
+/*
+ * Chunk prefill over the paged cache.
+ * Paper: Eq. 1 over the KV-cache blocks (Sec. I, Sec. V-C); chunked prefill
+ * (Sec. III-A) and ultra-short prefills run beside decode on a D-instance
+ * (PD-aggregation by the Request Scheduler, Sec. V-E).
+ * The prefill of a request that already holds cached tokens, i.e. one chunk
+ * of a prompt processed in chunks or an ultra-short prefill merged into a
+ * D-instance's work next to decode.  Eq. 1 over the cache,
  * causal with the chunk aligned to the end of the cache:
  *   request r has prefix_lens[r] cached tokens and a chunk of
  *   n_r = cu_seqlens[r+1] - cu_seqlens[r] new tokens whose K/V must already
@@ -126,7 +151,11 @@ dopd_status dopd_prefill_paged_attn(const dopd_attn_shape* shape, const void* q,
                                     int32_t num_reqs, void* out, float* lse, void* stream);
 
 /*
- * dopd_prefill_paged_attn with the cached keys of each work item split over
+ * dopd_prefill_paged_attn with key splits.
+ * Paper: as dopd_prefill_paged_attn (Eq. 1 over the cached blocks, Sec. III-A,
+ * Sec. V-E); the split and its log-sum-exp merge are an exact rewrite of the
+ * softmax of Eq. 1.
+ * The cached keys of each work item are split over
  * several workgroups, for calls with few work items (chunks of one or a few
  * long prompts fill only part of the GPU): the keys of each (q tile, request,
  * query head) item are cut into up to 16 contiguous ranges (the ranges that
@@ -156,15 +185,20 @@ dopd_status dopd_prefill_paged_attn_split(const dopd_attn_shape* shape, const vo
                                           int32_t num_splits, void* out, float* lse,
                                           void* workspace, size_t workspace_bytes, void* stream);
 
-/* Workspace bytes dopd_prefill_paged_attn_split needs for these arguments
- * (at least 256; 0 on bad input). */
+/* Workspace bytes dopd_prefill_paged_attn_split needs for these arguments on
+ * the current device (at least 256; 0 on bad input).
+ * Paper: as dopd_prefill_paged_attn_split (Eq. 1, Sec. III-A, Sec. V-E). */
 size_t dopd_prefill_paged_workspace_size(const dopd_attn_shape* shape,
                                          const int32_t* cu_seqlens_host,
                                          const int32_t* prefix_lens_host, int32_t num_reqs,
                                          int32_t num_splits);
 
 /*
- * Paged KV write: request r appends n_r = cu_new_tokens[r+1] - cu_new_tokens[r]
+ * Paged KV write.
+ * Paper: the KV cache kept per request in fixed-size blocks (Sec. I; block
+ * count and fragmentation, Sec. II-C; the blocks the Connector moves,
+ * Sec. V-C); KV capacity bounds a D-instance's concurrency (Eq. 11, Eq. 13).
+ * Request r appends n_r = cu_new_tokens[r+1] - cu_new_tokens[r]
  * tokens at logical positions start_pos[r] .. start_pos[r] + n_r - 1, taken
  * from rows cu_new_tokens[r] .. of k_new/v_new[total_new_tokens][Hkv][d].
  * Position p goes to page page_table[r*stride + p/16], slot p % 16.  Pure bit
@@ -180,7 +214,11 @@ dopd_status dopd_kv_write(const dopd_attn_shape* shape, const void* k_new, const
                           int32_t num_reqs, int32_t total_new_tokens, void* stream);
 
 /*
- * Paged KV write into E4M3 pools (shape->dtype = DOPD_FP8_E4M3): the same
+ * Paged KV write into E4M3 pools.
+ * Paper: the KV-cache blocks of Sec. I and Sec. V-C stored in FP8, the
+ * precision of the evaluated models (Sec. VI-A); the paper gives no scaling
+ * rule, the per-head scale is this library's.
+ * shape->dtype = DOPD_FP8_E4M3; the same
  * placement as dopd_kv_write, from bf16 k_new/v_new [total_new_tokens][Hkv][d],
  * with element x of KV head h stored as the code
  *     E4M3_rne(sat(x * fp32(1 / scale[h])))
@@ -198,7 +236,11 @@ dopd_status dopd_kv_write_fp8(const dopd_attn_shape* shape, const void* k_new, c
                               int32_t total_new_tokens, void* stream);
 
 /*
- * Paged single-query decode attention: for request r with context_lens[r]
+ * Paged single-query decode attention.
+ * Paper: Eq. 1 for one new token per request over its cached blocks; decode
+ * time is dominated by reading the KV cache from HBM (Sec. I, Sec. IV-B,
+ * Eq. 12; D-instance model, Sec. IV-D).
+ * For request r with context_lens[r]
  * cached tokens (counting the current one, whose K/V must already be in the
  * cache) and every query head h,
  *   out[r][h] = softmax_j(scale * q[r][h] . K_j) V_j,  j < context_lens[r].
@@ -227,7 +269,10 @@ dopd_status dopd_decode_attn(const dopd_attn_shape* shape, const void* q, const 
                              size_t workspace_bytes, void* stream);
 
 /*
- * Decode over E4M3 pools (shape->dtype = DOPD_FP8_E4M3): dopd_decode_attn's
+ * Decode over E4M3 pools.
+ * Paper: Eq. 1 as in dopd_decode_attn over FP8 blocks (the models' precision,
+ * Sec. VI-A), halving the bytes Eq. 12 charges per cached token.
+ * shape->dtype = DOPD_FP8_E4M3: dopd_decode_attn's
  * operation with K_j = code * k_scale[c] and V_j = code * v_scale[c] for KV
  * head c; q and out bf16, lse as there.  The codes are widened to bf16
  * (exactly) for the same MFMA path; the K scale multiplies the softmax scale
@@ -243,14 +288,21 @@ dopd_status dopd_decode_attn_fp8(const dopd_attn_shape* shape, const void* q,
                                  int32_t num_reqs, int32_t split_tokens, void* out, float* lse,
                                  void* workspace, size_t workspace_bytes, void* stream);
 
-/* Workspace bytes dopd_decode_attn(_fp8) needs for these arguments (0 on bad input). */
+/* Workspace bytes dopd_decode_attn(_fp8) needs for these arguments on the
+ * current device (at least 256; 0 on bad input).
+ * Paper: as dopd_decode_attn (Eq. 1, Sec. IV-B, Eq. 12); the split-K partials
+ * are an exact rewrite of the softmax of Eq. 1. */
 size_t dopd_decode_workspace_size(const dopd_attn_shape* shape,
                                   const int32_t* context_lens_host, int32_t num_reqs,
                                   int32_t split_tokens);
 
 /*
- * Handoff pack of prefill-completed requests (the KV blocks that the
- * Connector moves from a P-instance to a D-instance, Sec. V-C): handoff n
+ * Handoff pack of prefill-completed requests.
+ * Paper: a P-instance hands each prefill-completed request with its KV cache
+ * to a D-instance (Sec. IV-B); the Connector's KV transmitter moves the blocks
+ * (Sec. V-C), at a cost that grows with block count and fragmentation
+ * (Sec. II-C), which one contiguous buffer per request removes.
+ * Handoff n
  * (request req_ids[n], seq_lens[n] cached tokens) is written to
  *   out[out_offsets[n] + (((layer*2 + c)*Hkv + h)*len + t)*d + e]
  * with c = 0 for K and 1 for V, i.e. (layer, K/V, head, token, dim) order.
@@ -267,8 +319,10 @@ dopd_status dopd_kv_pack_for_handoff(const dopd_attn_shape* shape, int32_t num_l
                                      int32_t num_handoff, void* out, void* stream);
 
 /*
- * Handoff unpack on the receiving (D) instance, the inverse of
- * dopd_kv_pack_for_handoff (the KV blocks the Connector delivers, Sec. V-C):
+ * Handoff unpack on the receiving (D) instance.
+ * Paper: the KV blocks of a prefill-completed request that the Connector
+ * delivers to a D-instance (Sec. IV-B, Sec. V-C).
+ * The inverse of dopd_kv_pack_for_handoff:
  * element (layer, c, h, t, e) of handoff n, read from
  *   in[in_offsets[n] + (((layer*2 + c)*Hkv + h)*len + t)*d + e],  len = seq_lens[n],
  * is written to slot t % 16 of page page_table[req_ids[n]*stride + t/16] of
@@ -286,7 +340,9 @@ dopd_status dopd_kv_unpack_from_handoff(const dopd_attn_shape* shape, int32_t nu
                                         void* stream);
 
 /*
- * Host check of a page table copy: for each request r, the entries
+ * Host check of a page table copy.
+ * Paper: the per-request KV-cache blocks (Sec. I, Sec. V-C).
+ * For each request r, the entries
  * page_table_host[r*stride + i], i < ceil(lens_host[r]/16), must lie in
  * [0, num_pages).  Returns DOPD_OK or DOPD_ERR_INVALID_SHAPE.
  */
@@ -294,10 +350,12 @@ dopd_status dopd_validate_page_table_host(const int32_t* page_table_host,
                                           int32_t page_table_stride, int32_t num_reqs,
                                           const int32_t* lens_host, int32_t num_pages);
 
-/* Static description of a status code. */
+/* Static description of a status code.
+ * Paper: none (error reporting of this library). */
 const char* dopd_status_string(dopd_status status);
 
-/* hipError_t of the last DOPD_ERR_HIP on the calling thread (0 if none). */
+/* hipError_t of the last DOPD_ERR_HIP on the calling thread (0 if none).
+ * Paper: none (error reporting of this library). */
 int32_t dopd_last_hip_error(void);
 
 #ifdef __cplusplus

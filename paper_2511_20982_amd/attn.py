@@ -20,11 +20,12 @@ LIB_PATH = os.path.join(HERE, "libdopd_attn.so")
 
 DOPD_OK, DOPD_ERR_NULL_POINTER, DOPD_ERR_INVALID_SHAPE = 0, 1, 2
 DOPD_ERR_UNSUPPORTED, DOPD_ERR_WORKSPACE_TOO_SMALL, DOPD_ERR_HIP = 3, 4, 5
+DOPD_ERR_UNSUPPORTED_DTYPE = DOPD_ERR_UNSUPPORTED
 DOPD_BF16, DOPD_FP32, DOPD_FP8_E4M3 = 0, 1, 2
 PAGE_SIZE = 16
 
 EXPORTS = (
-    "dopd_prefill_attn", "dopd_prefill_paged_attn", "dopd_prefill_paged_attn_split",
+    "dopd_prefill_attn", "dopd_prefill_workspace_size", "dopd_prefill_paged_attn", "dopd_prefill_paged_attn_split",
     "dopd_prefill_paged_workspace_size", "dopd_kv_write", "dopd_kv_write_fp8",
     "dopd_decode_attn", "dopd_decode_attn_fp8", "dopd_decode_workspace_size",
     "dopd_kv_pack_for_handoff", "dopd_kv_unpack_from_handoff", "dopd_validate_page_table_host",
@@ -68,7 +69,9 @@ def lib():
         L = C.CDLL(LIB_PATH)
         P, i32, sz = C.c_void_p, C.c_int32, C.c_size_t
         SP = C.POINTER(Shape)
-        L.dopd_prefill_attn.argtypes = [SP, P, P, P, P, P, P, P, i32, P]
+        L.dopd_prefill_attn.argtypes = [SP, P, P, P, P, P, P, P, i32, P, sz, P]
+        L.dopd_prefill_workspace_size.argtypes = [SP, P, i32]
+        L.dopd_prefill_workspace_size.restype = sz
         L.dopd_prefill_paged_attn.argtypes = [SP, P, P, P, i32, P, i32, P, P, P, P, i32, P, P, P]
         L.dopd_prefill_paged_attn_split.argtypes = [SP, P, P, P, i32, P, i32, P, P, P, P, i32,
                                                     i32, P, P, P, sz, P]
@@ -130,11 +133,19 @@ def _check(status: int, where: str):
 
 # ------------------------------------------------------------------ entry points
 def dopd_prefill_attn(shape, q, k, v, out, lse, cu_seqlens, cu_seqlens_host, num_reqs,
-                      stream=None):
+                      workspace=None, workspace_bytes=None, stream=None):
     cu_h = _host_i32(cu_seqlens_host)
+    if workspace_bytes is None:
+        workspace_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
     _check(lib().dopd_prefill_attn(C.byref(shape), _dptr(q), _dptr(k), _dptr(v), _dptr(out),
                                    _dptr(lse), _dptr(cu_seqlens), _hptr(cu_h), int(num_reqs),
-                                   _stream(stream)), "dopd_prefill_attn")
+                                   _dptr(workspace), int(workspace_bytes), _stream(stream)),
+           "dopd_prefill_attn")
+
+
+def dopd_prefill_workspace_size(shape, cu_seqlens_host, num_reqs) -> int:
+    cu_h = _host_i32(cu_seqlens_host)
+    return int(lib().dopd_prefill_workspace_size(C.byref(shape), _hptr(cu_h), int(num_reqs)))
 
 
 def dopd_prefill_paged_attn(shape, q, k_pool, v_pool, num_pages, page_table, page_table_stride,

@@ -7,6 +7,7 @@
 #include <algorithm>
 #include <cstdint>
 #include <cstring>
+#include <mutex>
 
 #include "dopd_attn.h"
 #include "kernels/attn_f32.hpp"
@@ -16,6 +17,7 @@
 #include "kernels/kv_unpack.hpp"
 #include "kernels/kv_write.hpp"
 #include "kernels/prefill_bf16.hpp"
+#include "plan.hpp"
 
 namespace {
 
@@ -51,73 +53,35 @@ dopd_status check_shape_no_fp8(const dopd_attn_shape* s) {
 }
 
 
+// ---- machine shape ----------------------------------------------------------
+// CU and XCD counts of each device, read once (hipDeviceGetAttribute) the
+// first time a call plans a launch on it with that device current.
+constexpr int kMaxDevices = 64;
+std::once_flag g_machine_once[kMaxDevices];
+dopd::MachineShape g_machine[kMaxDevices];
+
+dopd::MachineShape machine_shape() {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) {
+    (void)hipGetLastError();  // no device: host-side sizing only
+    return dopd::kDefaultMachine;
+  }
+  std::call_once(g_machine_once[dev], [dev] {
+    int cus = 0, xcds = 0;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        cus <= 0)
+      cus = dopd::kDefaultMachine.cus;
+    if (hipDeviceGetAttribute(&xcds, hipDeviceAttributeNumberOfXccs, dev) != hipSuccess ||
+        xcds <= 0 || cus % xcds != 0)
+      xcds = 1;  // unknown: one dispatch order (correct, not XCD-aware)
+    (void)hipGetLastError();
+    g_machine[dev] = dopd::MachineShape{cus, xcds};
+  });
+  return g_machine[dev];
+}
+
 // ---- decode planning --------------------------------------------------------
 constexpr int kMaxGroupBf16 = 16;   // query heads per KV head handled by one decode wave
-// Resident four-wave decode workgroups: two per CU on 256 CUs.  The automatic
-// partition gives each of them one equal slice of the pairs (one round).
-constexpr int64_t kDecSlots = 512;
-constexpr int32_t kDecMaxSplitTokens = 4096;  // largest explicit split_tokens
-constexpr int64_t kDecMinPairsPerWg = 4;  // one pair per wave at least
-
-// Work units of the partition: per (r, c), a segment start cost plus its pairs.
-int64_t decode_total_units(const int32_t* ctx, int32_t n, int hkv) {
-  int64_t units = 0;
-  for (int32_t r = 0; r < n; ++r) units += (int64_t)(dopd::kDecSegCost + (ctx[r] + 31) / 32) * hkv;
-  return units;
-}
-
-// Workgroups of the partition: split_tokens / 32 units each when given, else
-// one slice per resident slot.
-int64_t decode_nwg(int64_t total_units, int32_t split_tokens) {
-  if (total_units <= 0) return 0;
-  if (split_tokens > 0) {
-    const int64_t per = split_tokens / 32;
-    return (total_units + per - 1) / per;
-  }
-  return std::max<int64_t>(1, std::min(kDecSlots, (total_units + kDecMinPairsPerWg - 1) /
-                                                      kDecMinPairsPerWg));
-}
-
-struct DecodeLayout {
-  size_t part_o_off, part_ml_off, total;
-};
-
-size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
-
-// Partial slots: at most one per (workgroup, (r, c)) boundary, indexed
-// workgroup + (r * Hkv + c).
-DecodeLayout decode_layout(const dopd_attn_shape* s, const int32_t* ctx, int32_t n,
-                           int32_t split_tokens) {
-  DecodeLayout L{};
-  const int g = s->num_q_heads / s->num_kv_heads;
-  const int64_t nwg = decode_nwg(decode_total_units(ctx, n, s->num_kv_heads), split_tokens);
-  const int64_t slots = nwg + (int64_t)n * s->num_kv_heads;
-  L.part_o_off = 0;
-  L.part_ml_off = align256((size_t)slots * g * s->head_dim * sizeof(float));
-  L.total = L.part_ml_off + align256((size_t)slots * g * 2 * sizeof(float));
-  return L;
-}
-
-// Same slice arithmetic as the kernels: does any (r, c) span two slices?
-bool decode_needs_merge(const int32_t* ctx, int32_t n, int hkv, int64_t total, int64_t nwg) {
-  auto begin = [&](int64_t b) { return b * total / nwg; };
-  auto slice_of = [&](int64_t x) {
-    int64_t b = x * nwg / total;
-    while (b + 1 < nwg && begin(b + 1) <= x) ++b;
-    while (b > 0 && begin(b) > x) --b;
-    return b;
-  };
-  int64_t base = 0;
-  for (int32_t r = 0; r < n; ++r) {
-    const int64_t np = (ctx[r] + 31) / 32, span = dopd::kDecSegCost + np;
-    for (int c = 0; c < hkv; ++c) {
-      const int64_t first = base + c * span + dopd::kDecSegCost;  // unit of the first pair
-      if (slice_of(first) != slice_of(first + np - 1)) return true;
-    }
-    base += span * hkv;
-  }
-  return false;
-}
 
 dopd_status check_decode_host(const dopd_attn_shape* s, const int32_t* ctx_host, int32_t n,
                               int32_t split) {
@@ -127,7 +91,7 @@ dopd_status check_decode_host(const dopd_attn_shape* s, const int32_t* ctx_host,
   if (n > 0 && !ctx_host) return DOPD_ERR_NULL_POINTER;
   for (int32_t r = 0; r < n; ++r)
     if (ctx_host[r] < 1) return DOPD_ERR_INVALID_SHAPE;
-  if (split < 0 || (split > 0 && split % 32 != 0) || split > kDecMaxSplitTokens)
+  if (split < 0 || (split > 0 && split % 32 != 0) || split > dopd::kDecMaxSplitTokens)
     return DOPD_ERR_INVALID_SHAPE;
   if (s->dtype != DOPD_FP32 && s->num_q_heads / s->num_kv_heads > kMaxGroupBf16)
     return DOPD_ERR_UNSUPPORTED;
@@ -145,15 +109,16 @@ dopd_status launch_decode_bf16(const dopd_attn_shape* s, const void* q, const vo
                                void* out, float* lse, void* workspace, size_t workspace_bytes,
                                hipStream_t strm) {
   const int hkv = s->num_kv_heads, hq = s->num_q_heads, d = s->head_dim;
-  const int64_t total = decode_total_units(ctx_host, nreq, hkv);
+  const int64_t total = dopd::decode_total_units(ctx_host, nreq, hkv);
   if (total > INT32_MAX / 2) return DOPD_ERR_INVALID_SHAPE;
-  const int64_t nwg = decode_nwg(total, split_tokens);
-  const DecodeLayout L = decode_layout(s, ctx_host, nreq, split_tokens);
+  const dopd::DecodeLayout L =
+      dopd::decode_layout(hq / hkv, hkv, d, ctx_host, nreq, split_tokens, machine_shape());
+  const int64_t nwg = L.nwg;
   if (!workspace) return DOPD_ERR_NULL_POINTER;
   if (workspace_bytes < L.total) return DOPD_ERR_WORKSPACE_TOO_SMALL;
   if ((reinterpret_cast<uintptr_t>(workspace) & 255) != 0) return DOPD_ERR_INVALID_SHAPE;
   char* ws = static_cast<char*>(workspace);
-  const bool merge = decode_needs_merge(ctx_host, nreq, hkv, total, nwg);
+  const bool merge = dopd::decode_needs_merge(ctx_host, nreq, hkv, total, nwg);
   dopd::DecodeArgs a;
   a.q = (const uint16_t*)q;
   a.k_pool = k_pool;
@@ -273,8 +238,9 @@ dopd_status launch_prefill_bf16(dopd::PrefillArgs a, int d, const int32_t* cu_ho
     for (int32_t r = 0; r <= nreq; ++r) a.cu_h[r] = cu_host[r];
     for (int32_t r = 0; r < nreq; ++r) a.prefix_h[r] = PAGED ? prefix_host[r] : 0;
     a.xcd_order = 1;
-    a.per_xcd = (int)((items + dopd::kNumXcd - 1) / dopd::kNumXcd);
-    blocks = (int64_t)a.per_xcd * dopd::kNumXcd;
+    a.xcds = machine_shape().xcds;
+    a.per_xcd = dopd::pf_per_xcd((int)items, a.xcds);
+    blocks = (int64_t)a.per_xcd * a.xcds;
   }
   if (blocks == 0) return DOPD_OK;
   blocks *= a.nsplit;  // (nsplit > 1 only on the paged path)
@@ -296,36 +262,13 @@ dopd_status launch_prefill_bf16(dopd::PrefillArgs a, int d, const int32_t* cu_ho
   return launch_status();
 }
 
-// Key splits of the paged prefill: the requested count (at most kPfMaxSplits),
-// or automatically, when the call has at most one work item per CU, about
-// kPfSlots / items splits (at most kPfAutoSplits), each split of the longest
-// item keeping at least 8 key tiles that every row sees.  Each split adds
-// T * Hq * d * 8 bytes of fp32 partials written and read back, which costs
-// more than it gains once the items fill the CUs.
-constexpr int kPfMaxSplits = 16;
-constexpr int kPfAutoSplits = 8;
-int prefill_paged_splits(const dopd_attn_shape* s, const int32_t* cu_host,
-                         const int32_t* prefix_host, int32_t nreq, int32_t num_splits) {
-  if (s->dtype != DOPD_BF16 || !(s->softmax_scale > 0.f)) return 1;
-  if (num_splits > 0) return std::min(num_splits, kPfMaxSplits);
-  int64_t items = 0, max_full = 0;
-  for (int32_t r = 0; r < nreq; ++r) {
-    const int64_t len = cu_host[r + 1] - cu_host[r];
-    const int64_t tiles = (len + dopd::kPfBM - 1) / dopd::kPfBM;
-    items += tiles * s->num_q_heads;
-    if (tiles > 0)
-      max_full = std::max<int64_t>(max_full, (prefix_host[r] + (tiles - 1) * dopd::kPfBM) / dopd::kPfBN);
-  }
-  if (items == 0 || items > dopd::kPfSlots / 2) return 1;
-  int64_t n = dopd::kPfSlots / items;
-  n = std::min<int64_t>(n, 1 + max_full / 8);
-  return (int)std::max<int64_t>(1, std::min<int64_t>(n, kPfAutoSplits));
-}
-
-size_t prefill_paged_ws_bytes(const dopd_attn_shape* s, int64_t T, int nsplit) {
-  if (nsplit <= 1) return 0;
-  const size_t rows = (size_t)nsplit * T * s->num_q_heads;
-  return align256(rows * s->head_dim * sizeof(float)) + align256(rows * 2 * sizeof(float));
+// Key splits of a paged prefill call on the current device (bf16 with a
+// positive scale only: the split bounds assume every row sees its first key).
+int paged_splits(const dopd_attn_shape* s, const int32_t* cu_host, const int32_t* prefix_host,
+                 int32_t nreq, int32_t num_splits) {
+  return dopd::prefill_paged_splits(s->num_q_heads,
+                                    s->dtype == DOPD_BF16 && s->softmax_scale > 0.f, cu_host,
+                                    prefix_host, nreq, num_splits, machine_shape());
 }
 
 dopd::PrefillArgs prefill_args(const dopd_attn_shape* s, const void* q, void* out, float* lse,
@@ -346,12 +289,23 @@ dopd::PrefillArgs prefill_args(const dopd_attn_shape* s, const void* q, void* ou
 }  // namespace
 }  // extern "C++"
 
+size_t dopd_prefill_workspace_size(const dopd_attn_shape* s, const int32_t* cu_host,
+                                   int32_t nreq) {
+  (void)s;
+  (void)cu_host;
+  (void)nreq;
+  return 0;  // the work list is derived from cu_host and passed by value
+}
+
 dopd_status dopd_prefill_attn(const dopd_attn_shape* s, const void* q, const void* k,
                               const void* v, void* out, float* lse, const int32_t* cu,
-                              const int32_t* cu_host, int32_t nreq, void* stream) {
+                              const int32_t* cu_host, int32_t nreq, void* workspace,
+                              size_t workspace_bytes, void* stream) {
+  (void)workspace_bytes;  // nothing is needed (dopd_prefill_workspace_size is 0)
   dopd_status st = check_shape_no_fp8(s);
   if (st != DOPD_OK) return st;
   if (nreq < 0) return DOPD_ERR_INVALID_SHAPE;
+  if ((reinterpret_cast<uintptr_t>(workspace) & 255) != 0) return DOPD_ERR_INVALID_SHAPE;
   if (nreq == 0) return DOPD_OK;
   if (!q || !k || !v || !out || !cu || !cu_host) return DOPD_ERR_NULL_POINTER;
   if (cu_host[0] != 0) return DOPD_ERR_INVALID_SHAPE;
@@ -424,19 +378,19 @@ static dopd_status prefill_paged_impl(const dopd_attn_shape* s, const void* q, c
   a.page_table = page_table;
   a.prefix = prefix;
   a.pt_stride = pt_stride;
-  const int nsplit = num_splits == 1 ? 1 : prefill_paged_splits(s, cu_host, prefix_host, nreq,
-                                                                num_splits);
+  const int nsplit = num_splits == 1 ? 1 : paged_splits(s, cu_host, prefix_host, nreq, num_splits);
   if (nsplit > 1) {
     if (T * hq * (int64_t)nsplit > INT32_MAX / 2) return DOPD_ERR_INVALID_SHAPE;
     if (!workspace) return DOPD_ERR_NULL_POINTER;
-    if (workspace_bytes < prefill_paged_ws_bytes(s, T, nsplit)) return DOPD_ERR_WORKSPACE_TOO_SMALL;
+    if (workspace_bytes < dopd::prefill_paged_ws_bytes(hq, d, T, nsplit))
+      return DOPD_ERR_WORKSPACE_TOO_SMALL;
     if ((reinterpret_cast<uintptr_t>(workspace) & 255) != 0) return DOPD_ERR_INVALID_SHAPE;
     const size_t rows = (size_t)nsplit * T * hq;
     a.nsplit = nsplit;
     a.part_rows = (int)T;
     a.part_o = static_cast<float*>(workspace);
     a.part_ml = reinterpret_cast<float*>(static_cast<char*>(workspace) +
-                                         align256(rows * d * sizeof(float)));
+                                         dopd::align256(rows * d * sizeof(float)));
   }
   return launch_prefill_bf16<true>(a, d, cu_host, prefix_host, nreq, strm);
 }
@@ -459,9 +413,9 @@ size_t dopd_prefill_paged_workspace_size(const dopd_attn_shape* s, const int32_t
   if (!cu_host || !prefix_host || cu_host[0] != 0) return 0;
   for (int32_t r = 0; r < nreq; ++r)
     if (cu_host[r + 1] < cu_host[r] || prefix_host[r] < 0) return 0;
-  const int nsplit = num_splits == 1 ? 1 : prefill_paged_splits(s, cu_host, prefix_host, nreq,
-                                                                num_splits);
-  return std::max<size_t>(256, prefill_paged_ws_bytes(s, cu_host[nreq], nsplit));
+  const int nsplit = num_splits == 1 ? 1 : paged_splits(s, cu_host, prefix_host, nreq, num_splits);
+  return std::max<size_t>(256, dopd::prefill_paged_ws_bytes(s->num_q_heads, s->head_dim,
+                                                            cu_host[nreq], nsplit));
 }
 
 dopd_status dopd_prefill_paged_attn_split(const dopd_attn_shape* s, const void* q,
@@ -552,7 +506,9 @@ size_t dopd_decode_workspace_size(const dopd_attn_shape* s, const int32_t* ctx_h
                                   int32_t split_tokens) {
   if (check_decode_host(s, ctx_host, n, split_tokens) != DOPD_OK) return 0;
   if (n == 0 || s->dtype == DOPD_FP32) return 256;
-  return decode_layout(s, ctx_host, n, split_tokens).total;
+  return dopd::decode_layout(s->num_q_heads / s->num_kv_heads, s->num_kv_heads, s->head_dim,
+                             ctx_host, n, split_tokens, machine_shape())
+      .total;
 }
 
 dopd_status dopd_decode_attn(const dopd_attn_shape* s, const void* q, const void* k_pool,

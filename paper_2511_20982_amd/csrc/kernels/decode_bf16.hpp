@@ -48,6 +48,7 @@
 #include <type_traits>
 
 #include "common.hpp"
+#include "../plan.hpp"
 
 namespace dopd {
 
@@ -71,14 +72,13 @@ struct DecodeArgs {
 
 constexpr int kDecWaves = 4;
 constexpr int kDecChunkPairs = 32 * kDecWaves;  // pairs whose page ids one wave holds at once
-constexpr int kDecSegCost = 8;                   // work units of a segment start, in pairs
 
 // First work unit of workgroup b's slice.
 __device__ __forceinline__ int dec_slice_begin(const DecodeArgs& a, int b) {
-  return (int)((int64_t)b * a.total_units / a.nwg);
+  return (int)dec_slice_begin((int64_t)b, a.total_units, a.nwg);
 }
 
-// The workgroup whose slice holds work unit x.
+// The workgroup whose slice holds work unit x (the host planner's search).
 __device__ __forceinline__ int dec_slice_of(const DecodeArgs& a, int x) {
   int b = (int)((int64_t)x * a.nwg / a.total_units);
   while (b + 1 < a.nwg && dec_slice_begin(a, b + 1) <= x) ++b;
@@ -271,9 +271,9 @@ __global__ __launch_bounds__(256, 2) void decode_split_kernel(DecodeArgs a) {
       bf16x8 pb;
   #pragma unroll
       for (int j = 0; j < 8; ++j) {
-        const float p = __builtin_amdgcn_exp2f(x[j] - m_new);
-        psum += p;
-        pb[j] = (__bf16)p;
+        // the row sum adds the bf16-rounded weights the P.V product applies
+        pb[j] = (__bf16)__builtin_amdgcn_exp2f(x[j] - m_new);
+        psum += (float)pb[j];
       }
       l_run = l_run * alpha + psum;
       m_run = m_new;

@@ -31,6 +31,7 @@
 #include <type_traits>
 
 #include "common.hpp"
+#include "../plan.hpp"
 
 namespace dopd {
 
@@ -46,10 +47,10 @@ struct PrefillArgs {
   float scale_log2;
   // XCD-aware order (used when nreq <= kPfMaxOrdered): the work list is
   // (slot block, request by decreasing length, q tile descending, slot of the
-  // block); XCD x = workgroup % 8 takes the contiguous slice
+  // block); XCD x = workgroup % xcds takes the contiguous slice
   // [x * per_xcd, (x+1) * per_xcd), so the q tiles that share a request's K/V
   // run together on one XCD and share its L2.
-  int xcd_order, n_items, per_xcd, tiles_total;
+  int xcd_order, n_items, per_xcd, tiles_total, xcds;
   int ord[64];         // requests by decreasing length
   // With the XCD order: incl[i] = sum over positions p <= i of the order of
   // (slots per block) x (q tiles of request ord[p]); copies of cu and prefix.
@@ -78,13 +79,11 @@ struct PrefillArgs {
 };
 
 constexpr int kPfMaxOrdered = 64;
-constexpr int kNumXcd = 8;
-constexpr int kPfSlots = 512;  // resident workgroups: two per CU on 256 CUs
 
-constexpr int kPfBM = 128;          // query rows per workgroup (32 per wave)
+constexpr int kPfBM = kPfTileRows;  // query rows per workgroup (32 per wave)
 constexpr int kPfHeadsPerWG = 1;    // heads per workgroup
 constexpr int kPfThreads = kPfHeadsPerWG * (kPfBM / 32) * 64;
-constexpr int kPfBN = 64;           // keys per tile
+constexpr int kPfBN = kPfTileKeys;  // keys per tile
 
 // Number of BM-row q tiles of request rr.
 __device__ __forceinline__ int pf_tiles(const int32_t* cu, int rr) {
@@ -124,9 +123,8 @@ __device__ __forceinline__ bool pf_find_item_lpt(const PrefillArgs& a, int b, in
 // slots that read one KV head (GQA) when the group size allows it.
 __device__ __forceinline__ bool pf_find_item_xcd(const PrefillArgs& a, int b, int& tile,
                                                  int& req, int& slot) {
-  const int x = b % kNumXcd, j = b / kNumXcd;
-  const int n = x * a.per_xcd + j;
-  if (j >= a.per_xcd || n >= a.n_items) return false;
+  if (!pf_xcd_valid(b, a.xcds, a.per_xcd, a.n_items)) return false;
+  const int n = pf_xcd_item(b, a.xcds, a.per_xcd);
   const int g = a.hq / a.hkv;
   const int gs = (g % kPfHeadsPerWG == 0) ? g / kPfHeadsPerWG : 1;  // slots per block
   const int per_blk = gs * a.tiles_total;

@@ -183,6 +183,45 @@ def prefill_batch(rng, lens, hq, hkv, d, dtype):
     return q, k, v
 
 
+def steep_score_batch(rng, lens, hq, hkv, d, pattern, rise=40.0):
+    """bf16 Q/K/V of packed requests whose attention scores (at the softmax
+    scale 1/sqrt(d)) climb steeply along each request, far beyond what N(0,1)
+    inputs reach: the inputs that drive an online softmax's rescaling.
+
+    Every query row is a shared direction u (entries +-1, so |u|^2 = d) plus
+    N(0, 1/4) noise; key t of a request is beta_t * u / sqrt(d) plus N(0, 1/4)
+    noise, so its score against any row is about beta_t (in natural-log
+    units) plus O(1).  V is N(0,1).  Patterns (t = position in the request):
+      "ramp":  beta_t = rise * t / 64 (rise per 64-key tile),
+      "jump":  beta_t = 0 for t < 256, then 150 + rise * (t - 256) / 64
+               (a step of more than 128 in the log2 domain),
+      "spike": beta_t = 0 except one key per request at position 64*5 + 17
+               (or the last position of a shorter request) with beta = 450.
+    """
+    lens = np.asarray(lens, np.int64)
+    t = int(lens.sum())
+    u = np.where(rng.integers(0, 2, d) == 1, 1.0, -1.0).astype(np.float32)
+    q = u[None, None, :] + 0.5 * rng.standard_normal((t, hq, d), dtype=np.float32)
+    pos = np.concatenate([np.arange(n) for n in lens]) if t else np.zeros(0, np.int64)
+    if pattern == "ramp":
+        beta = rise * pos / 64.0
+    elif pattern == "jump":
+        beta = np.where(pos < 256, 0.0, 150.0 + rise * (pos - 256) / 64.0)
+    elif pattern == "spike":
+        beta = np.zeros(t)
+        starts = np.concatenate([[0], np.cumsum(lens)[:-1]])
+        for s0, n in zip(starts, lens):
+            if n > 0:
+                beta[s0 + min(64 * 5 + 17, n - 1)] = 450.0
+    else:
+        raise ValueError(pattern)
+    k = (beta[:, None, None] / math.sqrt(d)) * u[None, None, :] + \
+        0.5 * rng.standard_normal((t, hkv, d), dtype=np.float32)
+    v = rng.standard_normal((t, hkv, d), dtype=np.float32)
+    return (f32_to_bf16_bits(q.astype(np.float32)), f32_to_bf16_bits(k.astype(np.float32)),
+            f32_to_bf16_bits(v))
+
+
 def config1(seed=SEED_BASE + 1, n_steps=8) -> Workload:
     """Tiny fp32 check: 4 requests {17,64,5,120}, 8/2 heads, d 64, 64-page pool,
     prefill then ``n_steps`` decode steps per request."""

@@ -65,7 +65,8 @@ def gpu_prefill(shape, q, k, v, cu, with_lse=True, stream=None):
     qd, kd, vd = A.to_device(q), A.to_device(k), A.to_device(v)
     out, obuf, margin = guarded(qd.shape, qd.dtype)
     lse = torch.full((q.shape[0], q.shape[1]), float("nan"), device=DEV) if with_lse else None
-    A.dopd_prefill_attn(shape, qd, kd, vd, out, lse, A.to_device(cu), cu, len(cu) - 1, stream)
+    A.dopd_prefill_attn(shape, qd, kd, vd, out, lse, A.to_device(cu), cu, len(cu) - 1,
+                        stream=stream)
     torch.cuda.synchronize()
     assert canary_intact(obuf, margin, out.numel() * out.element_size()), "prefill wrote out of bounds"
     return widen(A.to_host(out)), (lse.cpu().numpy().astype(np.float64) if with_lse else None)

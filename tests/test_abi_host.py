@@ -36,6 +36,31 @@ def test_every_declared_symbol_is_exported(lib):
         assert hasattr(lib, n), n
 
 
+def declaration_comments():
+    """{function name: the comment block right before its declaration}."""
+    src = open(HEADER).read()
+    out = {}
+    for m in re.finditer(r"/\*((?:(?!\*/).)*)\*/\s*(?:dopd_status|size_t|const char\*|int32_t)\s+"
+                         r"(dopd_[a-z_0-9]+)\s*\(", src, flags=re.S):
+        out[m.group(2)] = m.group(1)
+    return out
+
+
+# Library bookkeeping with no passage of the paper behind it.
+NO_PASSAGE = {"dopd_status_string", "dopd_last_hip_error"}
+
+
+def test_every_declaration_cites_its_passage():
+    com = declaration_comments()
+    assert set(com) == set(declared_functions())
+    for name, text in com.items():
+        if name in NO_PASSAGE:
+            assert "Paper: none" in text, name
+        else:
+            assert re.search(r"Paper:.*?\b(Sec\.|Eq\.|Alg\.)", text, flags=re.S), \
+                f"{name}: its comment block cites no Sec., Eq. or Alg."
+
+
 def test_status_strings(lib):
     for s in range(6):
         assert A.status_string(s)
@@ -51,7 +76,8 @@ def _prefill(lib, shape, cu_host, ptrs=FAKE, nreq=None):
     cu = np.asarray(cu_host, np.int32)
     n = len(cu) - 1 if nreq is None else nreq
     p = C.c_void_p(ptrs) if ptrs else None
-    return lib.dopd_prefill_attn(C.byref(shape), p, p, p, p, None, p, A._hptr(cu), n, None)
+    return lib.dopd_prefill_attn(C.byref(shape), p, p, p, p, None, p, A._hptr(cu), n, None, 0,
+                                 None)
 
 
 def test_prefill_host_validation(lib):
@@ -64,8 +90,14 @@ def test_prefill_host_validation(lib):
     assert _prefill(lib, _shape(), [0], nreq=-1) == A.DOPD_ERR_INVALID_SHAPE
     assert _prefill(lib, _shape(), [0], nreq=0) == A.DOPD_OK                  # empty batch
     assert _prefill(lib, _shape(), [0, 0, 0]) == A.DOPD_OK                    # all-empty requests
-    assert lib.dopd_prefill_attn(None, None, None, None, None, None, None, None, 1, None) == \
-        A.DOPD_ERR_NULL_POINTER
+    assert lib.dopd_prefill_attn(None, None, None, None, None, None, None, None, 1, None, 0,
+                                 None) == A.DOPD_ERR_NULL_POINTER
+    # a workspace that is given must be 256-byte aligned; the prefill needs none
+    p = C.c_void_p(FAKE)
+    cu = np.array([0, 4], np.int32)
+    assert lib.dopd_prefill_attn(C.byref(_shape()), p, p, p, p, None, p, A._hptr(cu), 1,
+                                 C.c_void_p(FAKE + 8), 64, None) == A.DOPD_ERR_INVALID_SHAPE
+    assert A.dopd_prefill_workspace_size(_shape(), cu, 1) == 0
 
 
 def _decode(lib, shape, ctx, split=0, ws_bytes=1 << 30, pt_stride=1024, ws=FAKE, nreq=None):

@@ -1,6 +1,5 @@
 """GPU: the five seeded workloads at full size, in the launch configuration the
-benchmark times, against the fp64 oracle (all outputs where the oracle is
-cheap, sampled rows for the large prefill)."""
+benchmark times, against the fp64 oracle on every output."""
 import numpy as np
 import pytest
 import torch
@@ -63,19 +62,16 @@ def test_full_size_decode(cfg):
 
 
 def test_full_size_prefill_and_write_config3():
+    """Every (row, head) output and lse of the varlen prefill batch (16 prompts,
+    32 heads, d 128) against the oracle, and the paged write of the whole batch
+    bit-exact."""
     w = I.config3()
     sh = G.shape_of(w)
     out, lse = G.gpu_prefill(sh, w.q, w.k, w.v, w.cu_seqlens)
-    rng = np.random.default_rng(3)
-    # sampled rows: the last rows of every prompt (longest rows), tile edges and random rows
-    last = np.concatenate([w.cu_seqlens[1:] - 1 - i for i in range(3)])
-    edges = np.concatenate([w.cu_seqlens[:-1] + e for e in (0, 63, 64, 255, 256)])
-    edges = edges[edges < w.cu_seqlens[-1]]
-    tok = np.concatenate([last, edges, rng.integers(0, w.cu_seqlens[-1], 200)]).astype(np.int32)
-    head = rng.integers(0, w.hq, len(tok)).astype(np.int32)
-    ref, ref_lse = oracle.prefill_rows(w.q, w.k, w.v, w.cu_seqlens, w.scale, tok, head)
-    G.assert_attention_close(out[tok, head], ref, "bf16", "config3 prefill rows")
-    assert np.max(np.abs(lse[tok, head] - ref_lse)) < 2e-2
+    ref, ref_lse = oracle.prefill(w.q, w.k, w.v, w.cu_seqlens, w.scale)
+    G.assert_attention_close(out, ref, "bf16", "config3 prefill, all rows")
+    assert np.max(np.abs(lse - ref_lse)) < 2e-2
+    del out, ref
     # paged write of the whole batch, bit-exact
     n = len(w.prefill_lens)
     gk, gv = G.gpu_kv_write(sh, w.k, w.v, w.k_pool, w.v_pool, w.page_table, w.cu_seqlens,
@@ -85,8 +81,51 @@ def test_full_size_prefill_and_write_config3():
     assert np.array_equal(gk, ref_k) and np.array_equal(gv, ref_v)
 
 
+def test_full_size_mixed_step_one_stream_decode_first_config5():
+    """The mixed step exactly as the benchmark times it: one stream, the decode
+    batch first, then prefill, paged write and pack.  Every decode and prefill
+    output against the oracle (absolute and per-(row, head) normalised
+    error), the write and the pack bit-exact."""
+    w = I.config5()
+    sh = G.shape_of(w)
+    s = torch.cuda.current_stream()
+    kp, vp = A.to_device(w.k_pool), A.to_device(w.v_pool)
+    pt = A.to_device(w.page_table)
+    stride = w.page_table.shape[1]
+    q, k, v = A.to_device(w.q), A.to_device(w.k), A.to_device(w.v)
+    cu = A.to_device(w.cu_seqlens)
+    out_p = torch.empty_like(q)
+    n_pre, n_dec = len(w.prefill_lens), len(w.context_lens)
+    q_dec = A.to_device(w.q_dec)
+    out_d = torch.empty_like(q_dec)
+    ws = A.decode_workspace(sh, w.context_lens, n_dec)
+    offs = I.handoff_offsets(w.handoff_lens, 1, w.hkv, w.d)
+    out_h = torch.empty(int(offs[-1]), dtype=torch.bfloat16, device="cuda")
+    ctx_d, start_d = A.to_device(w.context_lens), torch.zeros(n_pre, dtype=torch.int32, device="cuda")
+    hreq, hlen, offs_d = A.to_device(w.handoff_reqs), A.to_device(w.handoff_lens), A.to_device(offs)
+    torch.cuda.synchronize()
+    A.dopd_decode_attn(sh, q_dec, kp, vp, w.num_pages, pt, stride, ctx_d, w.context_lens, n_dec,
+                       0, out_d, None, ws, stream=s)
+    A.dopd_prefill_attn(sh, q, k, v, out_p, None, cu, w.cu_seqlens, n_pre, stream=s)
+    A.dopd_kv_write(sh, k, v, kp, vp, w.num_pages, pt[n_dec:], stride, cu, start_d, n_pre,
+                    int(w.cu_seqlens[-1]), s)
+    A.dopd_kv_pack_for_handoff(sh, 1, kp, vp, w.num_pages, pt, stride, hreq, hlen,
+                               w.handoff_lens, offs_d, n_pre, out_h, s)
+    torch.cuda.synchronize()
+    ref_d, _ = oracle.decode(w.q_dec, w.k_pool, w.v_pool, w.page_table, w.context_lens, w.scale)
+    G.assert_attention_close(G.widen(A.to_host(out_d)), ref_d, "bf16", "config5 decode (timed order)")
+    ref_p, _ = oracle.prefill(w.q, w.k, w.v, w.cu_seqlens, w.scale)
+    G.assert_attention_close(G.widen(A.to_host(out_p)), ref_p, "bf16", "config5 prefill (timed order)")
+    ref_kp, ref_vp = oracle.kv_write(w.k, w.v, w.k_pool, w.v_pool, w.page_table[n_dec:],
+                                     w.cu_seqlens, np.zeros(n_pre, np.int32))
+    assert np.array_equal(A.to_host(kp), ref_kp) and np.array_equal(A.to_host(vp), ref_vp)
+    ref_h = oracle.pack(ref_kp, ref_vp, 1, w.page_table, w.handoff_reqs, w.handoff_lens, offs)
+    assert np.array_equal(A.to_host(out_h), ref_h)
+
+
 def test_full_size_mixed_step_two_streams_config5():
-    """Prefill + write + pack on one stream, decode on another, as timed."""
+    """The mixed step's two-stream form (the benchmark's --streams 2): prefill,
+    write and pack on one stream, the decode on another, against the oracle."""
     w = I.config5()
     sh = G.shape_of(w)
     sA = torch.cuda.current_stream()
@@ -107,7 +146,7 @@ def test_full_size_mixed_step_two_streams_config5():
     hreq, hlen, offs_d = A.to_device(w.handoff_reqs), A.to_device(w.handoff_lens), A.to_device(offs)
     torch.cuda.synchronize()
     sB.wait_stream(sA)
-    A.dopd_prefill_attn(sh, q, k, v, out_p, None, cu, w.cu_seqlens, n_pre, sA)
+    A.dopd_prefill_attn(sh, q, k, v, out_p, None, cu, w.cu_seqlens, n_pre, stream=sA)
     A.dopd_decode_attn(sh, q_dec, kp, vp, w.num_pages, pt, w.page_table.shape[1], ctx_d,
                        w.context_lens, n_dec, 0, out_d, None, ws, stream=sB)
     A.dopd_kv_write(sh, k, v, kp, vp, w.num_pages, pt[n_dec:], w.page_table.shape[1], cu,

@@ -1,0 +1,92 @@
+"""GPU: the online softmax's rescaling paths against the fp64 oracle.
+
+N(0,1) inputs at scale 1/sqrt(d) keep every score within a few units of the
+running maximum, so the prefill kernels' steady state (which forms p against
+the running maximum without taking the tile's maximum, and rescales only when
+a half-row sum exceeds 2^20 or is not finite) and the masked tiles' lazy
+rescale are not exercised.  These inputs make the scores climb by 58 log2
+units per 64-key tile ("ramp"), step up by more than 128 log2 units so that
+2^(s - m) overflows to inf before the rescale ("jump"), or plant one key 450
+natural-log units above the rest in a late full tile ("spike"); logits reach
+about 460.  The dense, paged and key-split prefill entry points and the
+decode are compared on every output (Eq. 1; the oracle takes the exact max).
+"""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2511_20982_amd import inputs as I
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(autouse=True)
+def _gpu(require_gpu):
+    pass
+
+
+from tests import gpu_util as G  # noqa: E402
+
+PATTERNS = ["ramp", "jump", "spike"]
+LENS = [700, 333, 64, 1000, 1]
+
+
+def _finite_close(out, ref, what):
+    assert np.all(np.isfinite(out)), f"{what}: non-finite output"
+    G.assert_attention_close(out, ref, "bf16", what)
+
+
+@pytest.mark.parametrize("pattern", PATTERNS)
+@pytest.mark.parametrize("d", [128, 64])
+def test_dense_prefill_rescale(pattern, d):
+    rng = np.random.default_rng(300 + d)
+    lens = np.array(LENS, np.int32)
+    q, k, v = I.steep_score_batch(rng, lens, 8, 2, d, pattern)
+    cu = I.cu_from_lens(lens)
+    ref, ref_lse = oracle.prefill(q, k, v, cu, 1 / np.sqrt(d))
+    out, lse = G.gpu_prefill(G.A.make_shape(8, 2, d), q, k, v, cu)
+    _finite_close(out, ref, f"dense prefill {pattern} d={d}")
+    assert np.max(np.abs(lse - ref_lse) / np.maximum(1.0, np.abs(ref_lse))) < 1e-3
+
+
+def _paged_steep(seed, prefix, chunk, hq, hkv, d, pattern):
+    """Pools holding prefix + chunk tokens of steep-score K/V per request, and
+    the chunk rows of Q."""
+    rng = np.random.default_rng(seed)
+    prefix, chunk = np.asarray(prefix, np.int32), np.asarray(chunk, np.int32)
+    total = prefix + chunk
+    pt, num_pages = I.allocate_pages(rng, np.maximum(total, 1))
+    kp, vp = I.empty_pools(num_pages, hkv, d, "bf16")
+    qf, kf, vf = I.steep_score_batch(rng, total, hq, hkv, d, pattern)
+    kp, vp = oracle.kv_write(kf, vf, kp, vp, pt, I.cu_from_lens(total),
+                             np.zeros(len(total), np.int32))
+    cu_t = I.cu_from_lens(total)
+    rows = np.concatenate([cu_t[r] + prefix[r] + np.arange(chunk[r]) for r in range(len(total))])
+    return np.ascontiguousarray(qf[rows]), kp, vp, pt, I.cu_from_lens(chunk), prefix
+
+
+@pytest.mark.parametrize("splits", [None, 4])
+@pytest.mark.parametrize("pattern", PATTERNS)
+@pytest.mark.parametrize("d", [128, 64])
+def test_paged_prefill_rescale(pattern, d, splits):
+    q, kp, vp, pt, cu, pre = _paged_steep(310 + d, [0, 400, 129, 700], [700, 300, 200, 64],
+                                          8, 2, d, pattern)
+    ref, ref_lse = oracle.prefill_paged(q, kp, vp, pt, cu, pre, 1 / np.sqrt(d))
+    out, lse = G.gpu_prefill_paged(G.A.make_shape(8, 2, d), q, kp, vp, pt, cu, pre,
+                                   splits=splits)
+    _finite_close(out, ref, f"paged prefill {pattern} d={d} splits={splits}")
+    assert np.max(np.abs(lse - ref_lse) / np.maximum(1.0, np.abs(ref_lse))) < 1e-3
+
+
+@pytest.mark.parametrize("pattern", PATTERNS)
+def test_decode_rescale(pattern):
+    """One query per request over the same steep caches (the decode's online
+    softmax keeps the exact running max; its split-K merge rescales)."""
+    q, kp, vp, pt, cu, pre = _paged_steep(320, [699, 299, 1000, 63], [1, 1, 1, 1], 8, 2, 128,
+                                          pattern)
+    ctx = (pre + 1).astype(np.int32)
+    for split in (0, 64):
+        ref, ref_lse = oracle.decode(q, kp, vp, pt, ctx, 1 / np.sqrt(128))
+        out, lse = G.gpu_decode(G.A.make_shape(8, 2, 128), q, kp, vp, pt, ctx, split=split)
+        _finite_close(out, ref, f"decode {pattern} split={split}")
+        assert np.max(np.abs(lse - ref_lse) / np.maximum(1.0, np.abs(ref_lse))) < 1e-3
