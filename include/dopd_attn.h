@@ -296,6 +296,33 @@ size_t dopd_decode_workspace_size(const dopd_attn_shape* shape,
                                   const int32_t* context_lens_host, int32_t num_reqs,
                                   int32_t split_tokens);
 
+/* Size of the static device scratch of dopd_decode_attn_noalloc (32 MiB). */
+#define DOPD_DECODE_NOALLOC_SCRATCH_BYTES ((size_t)32 << 20)
+
+/*
+ * dopd_decode_attn without a caller workspace, for callers that cannot
+ * allocate device memory: code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation.  Same operation, arguments (minus the
+ * workspace), kernels and results as dopd_decode_attn (bf16 and fp32 caches;
+ * E4M3 returns DOPD_ERR_UNSUPPORTED).  The split-K partials go to a static
+ * device array of DOPD_DECODE_NOALLOC_SCRATCH_BYTES (32 MiB) that the library
+ * holds on every device it runs on until the process ends; its address is
+ * looked up once per device (hipGetSymbolAddress, with that device current).
+ * Nothing is allocated or freed by the call.  A call whose partials need
+ * more than that (dopd_decode_workspace_size with the same arguments above
+ * the limit) returns DOPD_ERR_WORKSPACE_TOO_SMALL before any device work.
+ * The array keeps the last call's contents and needs no clearing (every
+ * partial is written before it is read).  All calls on one device share it:
+ * calls that overlap in time on one device (two streams, two threads) race
+ * and must be serialised by the caller.
+ */
+dopd_status dopd_decode_attn_noalloc(const dopd_attn_shape* shape, const void* q,
+                                     const void* k_pool, const void* v_pool, int32_t num_pages,
+                                     const int32_t* page_table, int32_t page_table_stride,
+                                     const int32_t* context_lens,
+                                     const int32_t* context_lens_host, int32_t num_reqs,
+                                     int32_t split_tokens, void* out, float* lse, void* stream);
+
 /*
  * Handoff pack of prefill-completed requests.
  * Paper: a P-instance hands each prefill-completed request with its KV cache

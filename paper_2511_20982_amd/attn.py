@@ -28,6 +28,7 @@ EXPORTS = (
     "dopd_prefill_attn", "dopd_prefill_workspace_size", "dopd_prefill_paged_attn", "dopd_prefill_paged_attn_split",
     "dopd_prefill_paged_workspace_size", "dopd_kv_write", "dopd_kv_write_fp8",
     "dopd_decode_attn", "dopd_decode_attn_fp8", "dopd_decode_workspace_size",
+    "dopd_decode_attn_noalloc",
     "dopd_kv_pack_for_handoff", "dopd_kv_unpack_from_handoff", "dopd_validate_page_table_host",
     "dopd_status_string",
     "dopd_last_hip_error",
@@ -63,6 +64,10 @@ _LIB = None
 def lib():
     global _LIB
     if _LIB is None:
+        # PyTorch ships its own HIP runtime under the same soname as the one
+        # the library links; importing it first makes the process load one
+        # runtime (its), whatever the caller touches first.
+        import torch  # noqa: F401
         if not os.path.exists(LIB_PATH):
             raise RuntimeError(f"{LIB_PATH} is not built; run __graft_entry__.build() "
                                "or python paper_2511_20982_amd/build.py")
@@ -82,6 +87,7 @@ def lib():
         L.dopd_kv_write_fp8.argtypes = [SP, P, P, P, P, P, P, i32, P, i32, P, P, i32, i32, P]
         L.dopd_decode_attn_fp8.argtypes = [SP, P, P, P, P, P, i32, P, i32, P, P, i32, i32, P, P,
                                            P, sz, P]
+        L.dopd_decode_attn_noalloc.argtypes = [SP, P, P, P, i32, P, i32, P, P, i32, i32, P, P, P]
         L.dopd_decode_workspace_size.argtypes = [SP, P, i32, i32]
         L.dopd_decode_workspace_size.restype = sz
         L.dopd_kv_pack_for_handoff.argtypes = [SP, i32, P, P, i32, P, i32, P, P, P, P, i32, P, P]
@@ -93,6 +99,7 @@ def lib():
         for f in ("dopd_prefill_attn", "dopd_prefill_paged_attn",
                   "dopd_prefill_paged_attn_split", "dopd_kv_write",
                   "dopd_kv_write_fp8", "dopd_decode_attn", "dopd_decode_attn_fp8",
+                  "dopd_decode_attn_noalloc",
                   "dopd_kv_pack_for_handoff", "dopd_kv_unpack_from_handoff",
                   "dopd_validate_page_table_host"):
             getattr(L, f).restype = i32
@@ -220,6 +227,21 @@ def dopd_decode_attn(shape, q, k_pool, v_pool, num_pages, page_table, page_table
                                   _dptr(context_lens), _hptr(ctx), int(num_reqs),
                                   int(split_tokens), _dptr(out), _dptr(lse), _dptr(workspace),
                                   int(workspace_bytes), _stream(stream)), "dopd_decode_attn")
+
+
+DECODE_NOALLOC_SCRATCH_BYTES = 32 << 20
+
+
+def dopd_decode_attn_noalloc(shape, q, k_pool, v_pool, num_pages, page_table, page_table_stride,
+                             context_lens, context_lens_host, num_reqs, split_tokens, out, lse,
+                             stream=None):
+    ctx = _host_i32(context_lens_host)
+    _check(lib().dopd_decode_attn_noalloc(C.byref(shape), _dptr(q), _dptr(k_pool), _dptr(v_pool),
+                                          int(num_pages), _dptr(page_table),
+                                          int(page_table_stride), _dptr(context_lens),
+                                          _hptr(ctx), int(num_reqs), int(split_tokens),
+                                          _dptr(out), _dptr(lse), _stream(stream)),
+           "dopd_decode_attn_noalloc")
 
 
 def dopd_decode_attn_fp8(shape, q, k_pool, v_pool, k_scale, v_scale, num_pages, page_table,

@@ -80,6 +80,32 @@ dopd::MachineShape machine_shape() {
   return g_machine[dev];
 }
 
+// ---- static decode scratch (dopd_decode_attn_noalloc) ------------------------
+// The split-K partials of dopd_decode_attn_noalloc live in this file-scope
+// device array instead of a caller's workspace; every device the library runs
+// on holds its own copy until the process ends.  In host code `scratch` is
+// only a stand-in for the symbol: the device address comes from
+// hipGetSymbolAddress, once per device with that device current.
+static __device__ __align__(256) unsigned char scratch[DOPD_DECODE_NOALLOC_SCRATCH_BYTES];
+
+std::once_flag g_scratch_once[kMaxDevices];
+void* g_scratch_ptr[kMaxDevices];
+hipError_t g_scratch_err[kMaxDevices];
+
+// Device address of the current device's scratch array.
+dopd_status scratch_address(void** ptr) {
+  int dev = -1;
+  const hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_status(e);
+  if (dev < 0 || dev >= kMaxDevices) return DOPD_ERR_INVALID_SHAPE;
+  std::call_once(g_scratch_once[dev], [dev] {
+    g_scratch_err[dev] = hipGetSymbolAddress(&g_scratch_ptr[dev], HIP_SYMBOL(scratch));
+  });
+  if (g_scratch_err[dev] != hipSuccess) return hip_status(g_scratch_err[dev]);
+  *ptr = g_scratch_ptr[dev];
+  return DOPD_OK;
+}
+
 // ---- decode planning --------------------------------------------------------
 constexpr int kMaxGroupBf16 = 16;   // query heads per KV head handled by one decode wave
 
@@ -563,6 +589,28 @@ dopd_status dopd_decode_attn_fp8(const dopd_attn_shape* s, const void* q, const 
   return launch_decode_bf16<true>(s, q, k_pool, v_pool, k_scale, v_scale, pt, pt_stride, ctx,
                                   ctx_host, nreq, split_tokens, out, lse, workspace,
                                   workspace_bytes, as_stream(stream));
+}
+
+dopd_status dopd_decode_attn_noalloc(const dopd_attn_shape* s, const void* q,
+                                     const void* k_pool, const void* v_pool, int32_t num_pages,
+                                     const int32_t* pt, int32_t pt_stride, const int32_t* ctx,
+                                     const int32_t* ctx_host, int32_t nreq, int32_t split_tokens,
+                                     void* out, float* lse, void* stream) {
+  dopd_status st = check_decode_host(s, ctx_host, nreq, split_tokens);
+  if (st != DOPD_OK) return st;
+  if (s->dtype == DOPD_FP8_E4M3) return DOPD_ERR_UNSUPPORTED;
+  if (nreq == 0) return DOPD_OK;
+  size_t need = 0;
+  if (s->dtype == DOPD_BF16)
+    need = dopd::decode_layout(s->num_q_heads / s->num_kv_heads, s->num_kv_heads, s->head_dim,
+                               ctx_host, nreq, split_tokens, machine_shape())
+               .total;
+  if (need > DOPD_DECODE_NOALLOC_SCRATCH_BYTES) return DOPD_ERR_WORKSPACE_TOO_SMALL;
+  void* ws = nullptr;
+  st = scratch_address(&ws);
+  if (st != DOPD_OK) return st;
+  return dopd_decode_attn(s, q, k_pool, v_pool, num_pages, pt, pt_stride, ctx, ctx_host, nreq,
+                          split_tokens, out, lse, ws, DOPD_DECODE_NOALLOC_SCRATCH_BYTES, stream);
 }
 
 // ---------------------------------------------------------------- handoff pack
