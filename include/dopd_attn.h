@@ -324,6 +324,83 @@ dopd_status dopd_decode_attn_noalloc(const dopd_attn_shape* shape, const void* q
                                      int32_t split_tokens, void* out, float* lse, void* stream);
 
 /*
+ * Paged KV write of fresh prompts that also emits their handoff buffer.
+ * Paper: a prefill-completed request is handed to a D-instance with its KV
+ * cache (Sec. IV-B) by the Connector (Sec. V-C); the KV-cache blocks of
+ * Sec. I.  A fresh prompt's cache is exactly the K/V rows its prefill
+ * produced, so the buffer dopd_kv_pack_for_handoff would gather from the
+ * pages afterwards is written from those rows in the same pass as the pages.
+ * Request r (rows cu_seqlens[r] .. cu_seqlens[r+1] - 1 of
+ * k_new/v_new[T][Hkv][d], bf16) is written at positions 0 .. n_r - 1 of its
+ * pages exactly as dopd_kv_write with start_pos = 0, and, when out is not
+ * NULL, to
+ *   out[out_offsets[r] + ((c*Hkv + h)*n_r + t)*d + e]   (c = 0: K, 1: V),
+ * the one-layer (K/V, head, token, dim) block of dopd_kv_pack_for_handoff.
+ * out_offsets [num_reqs] (int64 element offsets, device); out and
+ * out_offsets are both NULL or both given.  cu_seqlens / cu_seqlens_host as
+ * in dopd_prefill_attn.  bf16 only.  Bit copy; other slots untouched.
+ */
+dopd_status dopd_kv_write_pack_for_handoff(const dopd_attn_shape* shape, const void* k_new,
+                                           const void* v_new, void* k_pool, void* v_pool,
+                                           int32_t num_pages, const int32_t* page_table,
+                                           int32_t page_table_stride, const int32_t* cu_seqlens,
+                                           const int32_t* cu_seqlens_host, int32_t num_reqs,
+                                           const int64_t* out_offsets, void* out, void* stream);
+
+/* Block order of dopd_pd_step's single launch. */
+enum {
+  DOPD_PD_AUTO = 0,           /* the library's choice (DOPD_PD_PREFILL_FIRST)          */
+  DOPD_PD_PREFILL_FIRST = 1,  /* write/pack and prefill workgroups dispatched first,
+                                 then the decode slices (two per CU)                   */
+  DOPD_PD_DECODE_FIRST = 2    /* the decode slices first, one per CU, then the
+                                 write/pack and prefill workgroups in the other slot    */
+};
+
+/*
+ * One PD-aggregated step in a single launch: the decode of a batch of
+ * requests and the prefill of a batch of fresh prompts on the same instance,
+ * with the prompts' paged KV write and (optionally) their handoff buffer.
+ * Paper: PD-aggregation, ultra-short requests prefilled on a D-instance next
+ * to its decode (Request Scheduler, Sec. V-E); co-scheduling prefill and
+ * decode work in one kernel (POD-style, Sec. III-A); Eq. 1 for both.
+ * Same results as, in one stream order,
+ *   dopd_decode_attn(q_dec, dec_page_table, context_lens ..., out_dec, lse_dec)
+ *   dopd_prefill_attn(q, k, v, cu_seqlens ..., out_pre, lse_pre)
+ *   dopd_kv_write_pack_for_handoff(k, v, pre_page_table ..., handoff_offsets,
+ *                                  handoff_out)
+ * (the decode's automatic partition; results equal those calls' up to the
+ * rounding of a different split), run as workgroups of three kinds in one
+ * grid (plus the decode's merge kernel when a context spans several slices),
+ * so that memory-bound decode slices and compute-bound prefill items share
+ * the CUs.  The decode requests' pages and the prompts' pages must be
+ * disjoint (the decode never reads what the write fills in this step).
+ *   dec_page_table / pre_page_table: rows of the decode requests and of the
+ *     prompts, both of page_table_stride columns, into the same pools.
+ *   schedule: DOPD_PD_* block order.
+ *   workspace: dopd_pd_step_workspace_size() bytes (decode partials),
+ *     256-byte aligned, any contents.
+ * bf16 only.  Either batch may be empty.
+ */
+dopd_status dopd_pd_step(const dopd_attn_shape* shape, const void* q_dec,
+                         const int32_t* dec_page_table, const int32_t* context_lens,
+                         const int32_t* context_lens_host, int32_t num_dec, void* out_dec,
+                         float* lse_dec, const void* q, const void* k, const void* v,
+                         const int32_t* cu_seqlens, const int32_t* cu_seqlens_host,
+                         int32_t num_pre, const int32_t* pre_page_table, void* out_pre,
+                         float* lse_pre, void* k_pool, void* v_pool, int32_t num_pages,
+                         int32_t page_table_stride, const int64_t* handoff_offsets,
+                         void* handoff_out, int32_t schedule, void* workspace,
+                         size_t workspace_bytes, void* stream);
+
+/* Workspace bytes dopd_pd_step needs for this decode batch and schedule on
+ * the current device (at least 256; 0 on bad input).
+ * Paper: as dopd_pd_step (Sec. V-E, Sec. III-A; the split-K partials of the
+ * decode are an exact rewrite of the softmax of Eq. 1). */
+size_t dopd_pd_step_workspace_size(const dopd_attn_shape* shape,
+                                   const int32_t* context_lens_host, int32_t num_dec,
+                                   int32_t schedule);
+
+/*
  * Handoff pack of prefill-completed requests.
  * Paper: a P-instance hands each prefill-completed request with its KV cache
  * to a D-instance (Sec. IV-B); the Connector's KV transmitter moves the blocks

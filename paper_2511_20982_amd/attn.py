@@ -22,6 +22,7 @@ DOPD_OK, DOPD_ERR_NULL_POINTER, DOPD_ERR_INVALID_SHAPE = 0, 1, 2
 DOPD_ERR_UNSUPPORTED, DOPD_ERR_WORKSPACE_TOO_SMALL, DOPD_ERR_HIP = 3, 4, 5
 DOPD_ERR_UNSUPPORTED_DTYPE = DOPD_ERR_UNSUPPORTED
 DOPD_BF16, DOPD_FP32, DOPD_FP8_E4M3 = 0, 1, 2
+DOPD_PD_AUTO, DOPD_PD_PREFILL_FIRST, DOPD_PD_DECODE_FIRST = 0, 1, 2
 PAGE_SIZE = 16
 
 EXPORTS = (
@@ -30,6 +31,7 @@ EXPORTS = (
     "dopd_decode_attn", "dopd_decode_attn_fp8", "dopd_decode_workspace_size",
     "dopd_decode_attn_noalloc",
     "dopd_kv_pack_for_handoff", "dopd_kv_unpack_from_handoff", "dopd_validate_page_table_host",
+    "dopd_kv_write_pack_for_handoff", "dopd_pd_step", "dopd_pd_step_workspace_size",
     "dopd_status_string",
     "dopd_last_hip_error",
 )
@@ -93,6 +95,12 @@ def lib():
         L.dopd_kv_pack_for_handoff.argtypes = [SP, i32, P, P, i32, P, i32, P, P, P, P, i32, P, P]
         L.dopd_kv_unpack_from_handoff.argtypes = [SP, i32, P, P, P, P, P, i32, P, P, i32, P, i32, P]
         L.dopd_validate_page_table_host.argtypes = [P, i32, i32, P, i32]
+        L.dopd_kv_write_pack_for_handoff.argtypes = [SP, P, P, P, P, i32, P, i32, P, P, i32, P,
+                                                     P, P]
+        L.dopd_pd_step.argtypes = [SP, P, P, P, P, i32, P, P, P, P, P, P, P, i32, P, P, P, P, P,
+                                   i32, i32, P, P, i32, P, sz, P]
+        L.dopd_pd_step_workspace_size.argtypes = [SP, P, i32, i32]
+        L.dopd_pd_step_workspace_size.restype = sz
         L.dopd_status_string.argtypes = [i32]
         L.dopd_status_string.restype = C.c_char_p
         L.dopd_last_hip_error.restype = i32
@@ -101,7 +109,8 @@ def lib():
                   "dopd_kv_write_fp8", "dopd_decode_attn", "dopd_decode_attn_fp8",
                   "dopd_decode_attn_noalloc",
                   "dopd_kv_pack_for_handoff", "dopd_kv_unpack_from_handoff",
-                  "dopd_validate_page_table_host"):
+                  "dopd_validate_page_table_host", "dopd_kv_write_pack_for_handoff",
+                  "dopd_pd_step"):
             getattr(L, f).restype = i32
         _LIB = L
     return _LIB
@@ -281,6 +290,52 @@ def dopd_kv_unpack_from_handoff(shape, num_layers, buf, in_offsets, req_ids, seq
                                              _dptr(v_pool), int(num_pages), _dptr(page_table),
                                              int(page_table_stride), _stream(stream)),
            "dopd_kv_unpack_from_handoff")
+
+
+def dopd_kv_write_pack_for_handoff(shape, k_new, v_new, k_pool, v_pool, num_pages, page_table,
+                                   page_table_stride, cu_seqlens, cu_seqlens_host, num_reqs,
+                                   out_offsets, out, stream=None):
+    cu_h = _host_i32(cu_seqlens_host)
+    _check(lib().dopd_kv_write_pack_for_handoff(
+        C.byref(shape), _dptr(k_new), _dptr(v_new), _dptr(k_pool), _dptr(v_pool), int(num_pages),
+        _dptr(page_table), int(page_table_stride), _dptr(cu_seqlens), _hptr(cu_h),
+        int(num_reqs), _dptr(out_offsets), _dptr(out), _stream(stream)),
+        "dopd_kv_write_pack_for_handoff")
+
+
+def dopd_pd_step_workspace_size(shape, context_lens_host, num_dec, schedule=DOPD_PD_AUTO) -> int:
+    ctx = _host_i32(context_lens_host)
+    return int(lib().dopd_pd_step_workspace_size(C.byref(shape), _hptr(ctx), int(num_dec),
+                                                 int(schedule)))
+
+
+def dopd_pd_step(shape, q_dec, dec_page_table, context_lens, context_lens_host, num_dec, out_dec,
+                 lse_dec, q, k, v, cu_seqlens, cu_seqlens_host, num_pre, pre_page_table,
+                 out_pre, lse_pre, k_pool, v_pool, num_pages, page_table_stride,
+                 handoff_offsets, handoff_out, schedule, workspace, workspace_bytes=None,
+                 stream=None):
+    ctx = _host_i32(context_lens_host)
+    cu_h = _host_i32(cu_seqlens_host)
+    if workspace_bytes is None:
+        workspace_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check(lib().dopd_pd_step(
+        C.byref(shape), _dptr(q_dec), _dptr(dec_page_table), _dptr(context_lens), _hptr(ctx),
+        int(num_dec), _dptr(out_dec), _dptr(lse_dec), _dptr(q), _dptr(k), _dptr(v),
+        _dptr(cu_seqlens), _hptr(cu_h), int(num_pre), _dptr(pre_page_table), _dptr(out_pre),
+        _dptr(lse_pre), _dptr(k_pool), _dptr(v_pool), int(num_pages), int(page_table_stride),
+        _dptr(handoff_offsets), _dptr(handoff_out), int(schedule), _dptr(workspace),
+        int(workspace_bytes), _stream(stream)), "dopd_pd_step")
+
+
+def pd_step_workspace(shape, context_lens_host, num_dec, schedule=DOPD_PD_AUTO, device="cuda"):
+    """A 256-byte aligned workspace for dopd_pd_step."""
+    import torch
+    n = dopd_pd_step_workspace_size(shape, context_lens_host, num_dec, schedule)
+    if n == 0:
+        raise DopdError(DOPD_ERR_INVALID_SHAPE, "dopd_pd_step_workspace_size")
+    ws = torch.empty(n + 256, dtype=torch.uint8, device=device)
+    off = (-ws.data_ptr()) % 256
+    return ws[off:off + n]
 
 
 def dopd_validate_page_table_host(page_table_host, page_table_stride, num_reqs, lens_host,

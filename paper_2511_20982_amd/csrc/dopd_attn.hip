@@ -16,6 +16,8 @@
 #include "kernels/kv_pack.hpp"
 #include "kernels/kv_unpack.hpp"
 #include "kernels/kv_write.hpp"
+#include "kernels/kv_write_pack.hpp"
+#include "kernels/pd_step.hpp"
 #include "kernels/prefill_bf16.hpp"
 #include "plan.hpp"
 
@@ -124,28 +126,28 @@ dopd_status check_decode_host(const dopd_attn_shape* s, const int32_t* ctx_host,
   return DOPD_OK;
 }
 
-// The bf16-operand decode (bf16 or E4M3 pools) after the host checks: plan
-// the partition, check the workspace, launch the split kernel and, when some
-// (request, KV head) spans two slices, the merge kernel.
+// Decode arguments and workspace layout of the bf16-operand decode (bf16 or
+// E4M3 pools) after the host checks; wg_per_cu: resident decode workgroups per
+// CU the automatic partition plans for.
 template <bool KV8>
-dopd_status launch_decode_bf16(const dopd_attn_shape* s, const void* q, const void* k_pool,
-                               const void* v_pool, const float* k_scale, const float* v_scale,
-                               const int32_t* pt, int32_t pt_stride, const int32_t* ctx,
-                               const int32_t* ctx_host, int32_t nreq, int32_t split_tokens,
-                               void* out, float* lse, void* workspace, size_t workspace_bytes,
-                               hipStream_t strm) {
+dopd_status plan_decode_bf16(const dopd_attn_shape* s, const void* q, const void* k_pool,
+                             const void* v_pool, const float* k_scale, const float* v_scale,
+                             const int32_t* pt, int32_t pt_stride, const int32_t* ctx,
+                             const int32_t* ctx_host, int32_t nreq, int32_t split_tokens,
+                             void* out, float* lse, void* workspace, size_t workspace_bytes,
+                             int wg_per_cu, dopd::DecodeArgs* a_out, bool* merge_out) {
   const int hkv = s->num_kv_heads, hq = s->num_q_heads, d = s->head_dim;
   const int64_t total = dopd::decode_total_units(ctx_host, nreq, hkv);
   if (total > INT32_MAX / 2) return DOPD_ERR_INVALID_SHAPE;
-  const dopd::DecodeLayout L =
-      dopd::decode_layout(hq / hkv, hkv, d, ctx_host, nreq, split_tokens, machine_shape());
+  const dopd::DecodeLayout L = dopd::decode_layout(hq / hkv, hkv, d, ctx_host, nreq,
+                                                   split_tokens, machine_shape(), wg_per_cu);
   const int64_t nwg = L.nwg;
   if (!workspace) return DOPD_ERR_NULL_POINTER;
   if (workspace_bytes < L.total) return DOPD_ERR_WORKSPACE_TOO_SMALL;
   if ((reinterpret_cast<uintptr_t>(workspace) & 255) != 0) return DOPD_ERR_INVALID_SHAPE;
   char* ws = static_cast<char*>(workspace);
-  const bool merge = dopd::decode_needs_merge(ctx_host, nreq, hkv, total, nwg);
-  dopd::DecodeArgs a;
+  *merge_out = dopd::decode_needs_merge(ctx_host, nreq, hkv, total, nwg);
+  dopd::DecodeArgs& a = *a_out;
   a.q = (const uint16_t*)q;
   a.k_pool = k_pool;
   a.v_pool = v_pool;
@@ -164,19 +166,44 @@ dopd_status launch_decode_bf16(const dopd_attn_shape* s, const void* q, const vo
   a.total_units = (int)total;
   a.nwg = (int)nwg;
   a.scale_log2 = s->softmax_scale * dopd::kLog2e;
-  const int64_t items = nwg;
-  const int64_t merge_items = merge ? (int64_t)nreq * hkv : 0;
+  return DOPD_OK;
+}
+
+// The decode's second kernel: merges the (request, KV head) pairs whose keys
+// span several slices.
+dopd_status launch_decode_merge(const dopd::DecodeArgs& a, int d, hipStream_t strm) {
+  const unsigned items = (unsigned)((int64_t)a.nreq * a.hkv);
   if (d == 64)
-    hipLaunchKernelGGL((dopd::decode_split_kernel<64, KV8>), dim3((unsigned)items), dim3(256), 0, strm, a);
+    hipLaunchKernelGGL(dopd::decode_merge_kernel<64>, dim3(items), dim3(256), 0, strm, a);
   else
-    hipLaunchKernelGGL((dopd::decode_split_kernel<128, KV8>), dim3((unsigned)items), dim3(256), 0, strm, a);
-  const dopd_status st = launch_status();
-  if (st != DOPD_OK || merge_items == 0) return st;
-  if (d == 64)
-    hipLaunchKernelGGL(dopd::decode_merge_kernel<64>, dim3((unsigned)merge_items), dim3(256), 0, strm, a);
-  else
-    hipLaunchKernelGGL(dopd::decode_merge_kernel<128>, dim3((unsigned)merge_items), dim3(256), 0, strm, a);
+    hipLaunchKernelGGL(dopd::decode_merge_kernel<128>, dim3(items), dim3(256), 0, strm, a);
   return launch_status();
+}
+
+// The bf16-operand decode after the host checks: plan the partition, check the
+// workspace, launch the split kernel and, when some (request, KV head) spans
+// two slices, the merge kernel.
+template <bool KV8>
+dopd_status launch_decode_bf16(const dopd_attn_shape* s, const void* q, const void* k_pool,
+                               const void* v_pool, const float* k_scale, const float* v_scale,
+                               const int32_t* pt, int32_t pt_stride, const int32_t* ctx,
+                               const int32_t* ctx_host, int32_t nreq, int32_t split_tokens,
+                               void* out, float* lse, void* workspace, size_t workspace_bytes,
+                               hipStream_t strm) {
+  dopd::DecodeArgs a;
+  bool merge = false;
+  const dopd_status pst = plan_decode_bf16<KV8>(s, q, k_pool, v_pool, k_scale, v_scale, pt,
+                                                pt_stride, ctx, ctx_host, nreq, split_tokens,
+                                                out, lse, workspace, workspace_bytes,
+                                                dopd::kWgPerCu, &a, &merge);
+  if (pst != DOPD_OK) return pst;
+  if (s->head_dim == 64)
+    hipLaunchKernelGGL((dopd::decode_split_kernel<64, KV8>), dim3((unsigned)a.nwg), dim3(256), 0, strm, a);
+  else
+    hipLaunchKernelGGL((dopd::decode_split_kernel<128, KV8>), dim3((unsigned)a.nwg), dim3(256), 0, strm, a);
+  const dopd_status st = launch_status();
+  if (st != DOPD_OK || !merge) return st;
+  return launch_decode_merge(a, s->head_dim, strm);
 }
 
 }  // namespace
@@ -218,13 +245,14 @@ dopd_status dopd_validate_page_table_host(const int32_t* pt, int32_t stride, int
 extern "C++" {
 namespace {
 
-// Plans and launches the bf16 prefill kernel over chunk lengths cu_host (and,
-// on the paged path, the cached prefixes prefix_host).  Work items are
-// (q tile, request, head); with at most 64 requests the XCD-aware order is
-// used, requests ranked by the keys their last row sees.
+// Fills the work-order fields of `a` for chunk lengths cu_host (and, on the
+// paged path, cached prefixes prefix_host) and returns the prefill's block
+// count: items are (q tile, request, head), with at most 64 requests in the
+// XCD-aware order (requests ranked by the keys their last row sees, dealt to
+// the XCDs in contiguous slices), else heaviest q tile first.
 template <bool PAGED>
-dopd_status launch_prefill_bf16(dopd::PrefillArgs a, int d, const int32_t* cu_host,
-                                const int32_t* prefix_host, int32_t nreq, hipStream_t strm) {
+dopd_status plan_prefill_bf16(dopd::PrefillArgs& a, const int32_t* cu_host,
+                              const int32_t* prefix_host, int32_t nreq, int64_t* blocks_out) {
   int max_len = 0;
   int64_t tiles = 0;
   for (int32_t r = 0; r < nreq; ++r) {
@@ -242,6 +270,7 @@ dopd_status launch_prefill_bf16(dopd::PrefillArgs a, int d, const int32_t* cu_ho
   a.n_items = (int)items;
   a.tiles_total = (int)tiles;
   a.per_xcd = 0;
+  a.xcds = 1;
   std::memset(a.ord, 0, sizeof(a.ord));
   if (nreq <= dopd::kPfMaxOrdered) {
     // requests by decreasing key count (stable), dealt to XCDs in contiguous slices
@@ -268,9 +297,23 @@ dopd_status launch_prefill_bf16(dopd::PrefillArgs a, int d, const int32_t* cu_ho
     a.per_xcd = dopd::pf_per_xcd((int)items, a.xcds);
     blocks = (int64_t)a.per_xcd * a.xcds;
   }
-  if (blocks == 0) return DOPD_OK;
   blocks *= a.nsplit;  // (nsplit > 1 only on the paged path)
-  if (blocks > INT32_MAX) return DOPD_ERR_INVALID_SHAPE;
+  if (blocks > INT32_MAX / 2) return DOPD_ERR_INVALID_SHAPE;
+  *blocks_out = blocks;
+  return DOPD_OK;
+}
+
+// Plans and launches the bf16 prefill kernel over chunk lengths cu_host (and,
+// on the paged path, the cached prefixes prefix_host).  Work items are
+// (q tile, request, head); with at most 64 requests the XCD-aware order is
+// used, requests ranked by the keys their last row sees.
+template <bool PAGED>
+dopd_status launch_prefill_bf16(dopd::PrefillArgs a, int d, const int32_t* cu_host,
+                                const int32_t* prefix_host, int32_t nreq, hipStream_t strm) {
+  int64_t blocks = 0;
+  const dopd_status pst = plan_prefill_bf16<PAGED>(a, cu_host, prefix_host, nreq, &blocks);
+  if (pst != DOPD_OK) return pst;
+  if (blocks == 0) return DOPD_OK;
   if (d == 64)
     hipLaunchKernelGGL((dopd::prefill_bf16_kernel<64, PAGED>), dim3((unsigned)blocks),
                        dim3(dopd::kPfThreads), 0, strm, a);
@@ -611,6 +654,176 @@ dopd_status dopd_decode_attn_noalloc(const dopd_attn_shape* s, const void* q,
   if (st != DOPD_OK) return st;
   return dopd_decode_attn(s, q, k_pool, v_pool, num_pages, pt, pt_stride, ctx, ctx_host, nreq,
                           split_tokens, out, lse, ws, DOPD_DECODE_NOALLOC_SCRATCH_BYTES, stream);
+}
+
+// ---------------------------------------------------------------- write + pack
+extern "C++" {
+namespace {
+
+// Host checks shared by the write+pack and the PD step: bf16 fresh prompts
+// with start position 0, each prompt's pages inside the page-table row.
+dopd_status check_fresh_prompts(const int32_t* cu_host, int32_t nreq, int32_t pt_stride,
+                                int64_t* pages_out) {
+  if (cu_host[0] != 0) return DOPD_ERR_INVALID_SHAPE;
+  int64_t pages = 0;
+  for (int32_t r = 0; r < nreq; ++r) {
+    const int64_t n = (int64_t)cu_host[r + 1] - cu_host[r];
+    if (n < 0) return DOPD_ERR_INVALID_SHAPE;
+    const int64_t np = (n + dopd::kPage - 1) / dopd::kPage;
+    if (np > pt_stride) return DOPD_ERR_INVALID_SHAPE;
+    pages += np;
+  }
+  *pages_out = pages;
+  return DOPD_OK;
+}
+
+dopd::WritePackArgs write_pack_args(const void* k_new, const void* v_new, void* k_pool,
+                                    void* v_pool, const int32_t* pt, int32_t pt_stride,
+                                    const int32_t* cu, int32_t nreq, int hkv,
+                                    const int64_t* out_offsets, void* out) {
+  dopd::WritePackArgs w;
+  w.k_new = (const uint16_t*)k_new;
+  w.v_new = (const uint16_t*)v_new;
+  w.k_pool = (uint16_t*)k_pool;
+  w.v_pool = (uint16_t*)v_pool;
+  w.page_table = pt;
+  w.pt_stride = pt_stride;
+  w.cu = cu;
+  w.nreq = nreq;
+  w.hkv = hkv;
+  w.out = (uint16_t*)out;
+  w.out_off = out_offsets;
+  return w;
+}
+
+}  // namespace
+}  // extern "C++"
+
+dopd_status dopd_kv_write_pack_for_handoff(const dopd_attn_shape* s, const void* k_new,
+                                           const void* v_new, void* k_pool, void* v_pool,
+                                           int32_t num_pages, const int32_t* pt,
+                                           int32_t pt_stride, const int32_t* cu,
+                                           const int32_t* cu_host, int32_t nreq,
+                                           const int64_t* out_offsets, void* out, void* stream) {
+  dopd_status st = check_shape(s);
+  if (st != DOPD_OK) return st;
+  if (s->dtype != DOPD_BF16) return DOPD_ERR_UNSUPPORTED;
+  if (nreq < 0 || num_pages < 0 || pt_stride < 0) return DOPD_ERR_INVALID_SHAPE;
+  if (nreq == 0) return DOPD_OK;
+  if (!k_new || !v_new || !k_pool || !v_pool || !pt || !cu || !cu_host)
+    return DOPD_ERR_NULL_POINTER;
+  if ((out == nullptr) != (out_offsets == nullptr)) return DOPD_ERR_NULL_POINTER;
+  int64_t pages = 0;
+  st = check_fresh_prompts(cu_host, nreq, pt_stride, &pages);
+  if (st != DOPD_OK) return st;
+  const int64_t blocks = pages * s->num_kv_heads;
+  if (blocks == 0) return DOPD_OK;
+  if (blocks > INT32_MAX) return DOPD_ERR_INVALID_SHAPE;
+  const dopd::WritePackArgs w = write_pack_args(k_new, v_new, k_pool, v_pool, pt, pt_stride, cu,
+                                                nreq, s->num_kv_heads, out_offsets, out);
+  hipStream_t strm = as_stream(stream);
+  if (s->head_dim == 64)
+    hipLaunchKernelGGL(dopd::kv_write_pack_kernel<64>, dim3((unsigned)blocks), dim3(256), 0, strm, w);
+  else
+    hipLaunchKernelGGL(dopd::kv_write_pack_kernel<128>, dim3((unsigned)blocks), dim3(256), 0, strm, w);
+  return launch_status();
+}
+
+// ---------------------------------------------------------------- PD step
+size_t dopd_pd_step_workspace_size(const dopd_attn_shape* s, const int32_t* ctx_host,
+                                   int32_t num_dec, int32_t schedule) {
+  if (check_decode_host(s, ctx_host, num_dec, 0) != DOPD_OK) return 0;
+  if (s->dtype != DOPD_BF16 || schedule < DOPD_PD_AUTO || schedule > DOPD_PD_DECODE_FIRST)
+    return 0;
+  if (num_dec == 0) return 256;
+  const int wg_per_cu = schedule == DOPD_PD_DECODE_FIRST ? 1 : dopd::kWgPerCu;
+  return dopd::decode_layout(s->num_q_heads / s->num_kv_heads, s->num_kv_heads, s->head_dim,
+                             ctx_host, num_dec, 0, machine_shape(), wg_per_cu)
+      .total;
+}
+
+dopd_status dopd_pd_step(const dopd_attn_shape* s, const void* q_dec,
+                         const int32_t* dec_page_table, const int32_t* ctx,
+                         const int32_t* ctx_host, int32_t num_dec, void* out_dec,
+                         float* lse_dec, const void* q, const void* k, const void* v,
+                         const int32_t* cu, const int32_t* cu_host, int32_t num_pre,
+                         const int32_t* pre_page_table, void* out_pre, float* lse_pre,
+                         void* k_pool, void* v_pool, int32_t num_pages, int32_t pt_stride,
+                         const int64_t* handoff_offsets, void* handoff_out, int32_t schedule,
+                         void* workspace, size_t workspace_bytes, void* stream) {
+  dopd_status st = check_decode_host(s, ctx_host, num_dec, 0);
+  if (st != DOPD_OK) return st;
+  if (s->dtype != DOPD_BF16) return DOPD_ERR_UNSUPPORTED;
+  if (schedule < DOPD_PD_AUTO || schedule > DOPD_PD_DECODE_FIRST || num_pre < 0 ||
+      num_pages < 0 || pt_stride < 0)
+    return DOPD_ERR_INVALID_SHAPE;
+  if (num_dec == 0 && num_pre == 0) return DOPD_OK;
+  if (!k_pool || !v_pool) return DOPD_ERR_NULL_POINTER;
+  if (num_dec > 0 && (!q_dec || !dec_page_table || !ctx || !out_dec)) return DOPD_ERR_NULL_POINTER;
+  if (num_pre > 0 && (!q || !k || !v || !cu || !cu_host || !pre_page_table || !out_pre))
+    return DOPD_ERR_NULL_POINTER;
+  if ((handoff_out == nullptr) != (handoff_offsets == nullptr)) return DOPD_ERR_NULL_POINTER;
+  for (int32_t r = 0; r < num_dec; ++r)
+    if ((int64_t)(ctx_host[r] + dopd::kPage - 1) / dopd::kPage > pt_stride)
+      return DOPD_ERR_INVALID_SHAPE;
+  int64_t pages = 0;
+  if (num_pre > 0) {
+    st = check_fresh_prompts(cu_host, num_pre, pt_stride, &pages);
+    if (st != DOPD_OK) return st;
+  }
+  if (schedule == DOPD_PD_AUTO) schedule = DOPD_PD_PREFILL_FIRST;
+  const int hkv = s->num_kv_heads, d = s->head_dim;
+  dopd::PdStepArgs p;
+  std::memset(&p, 0, sizeof(p));
+  bool merge = false;
+  if (num_dec > 0) {
+    st = plan_decode_bf16<false>(s, q_dec, k_pool, v_pool, nullptr, nullptr, dec_page_table,
+                                 pt_stride, ctx, ctx_host, num_dec, 0, out_dec, lse_dec,
+                                 workspace, workspace_bytes,
+                                 schedule == DOPD_PD_DECODE_FIRST ? 1 : dopd::kWgPerCu, &p.dec,
+                                 &merge);
+    if (st != DOPD_OK) return st;
+    p.n_dec = p.dec.nwg;
+  }
+  int64_t pf_blocks = 0;
+  if (num_pre > 0 && cu_host[num_pre] > 0) {
+    p.pf = prefill_args(s, q, out_pre, lse_pre, cu);
+    p.pf.k = (const uint16_t*)k;
+    p.pf.v = (const uint16_t*)v;
+    st = plan_prefill_bf16<false>(p.pf, cu_host, nullptr, num_pre, &pf_blocks);
+    if (st != DOPD_OK) return st;
+    p.wp = write_pack_args(k, v, k_pool, v_pool, pre_page_table, pt_stride, cu, num_pre, hkv,
+                           handoff_offsets, handoff_out);
+  }
+  p.n_pf = (int)pf_blocks;
+  if (pages * hkv > INT32_MAX / 4) return DOPD_ERR_INVALID_SHAPE;
+  p.n_wp = (int)(pages * hkv);
+  // Block ranges; the prefill range starts on a multiple of the XCD count so
+  // its XCD-aware order holds (blocks in the gaps exit at once).
+  const int64_t xc = std::max(1, p.pf.xcds);
+  auto round_up = [&](int64_t x) { return (x + xc - 1) / xc * xc; };
+  int64_t total;
+  if (schedule == DOPD_PD_PREFILL_FIRST) {
+    p.wp_first = 0;
+    p.pf_first = (int)round_up(p.n_wp);
+    p.dec_first = p.pf_first + p.n_pf;
+    total = (int64_t)p.dec_first + p.n_dec;
+  } else {
+    p.dec_first = 0;
+    p.wp_first = p.n_dec;
+    p.pf_first = (int)round_up((int64_t)p.n_dec + p.n_wp);
+    total = (int64_t)p.pf_first + p.n_pf;
+  }
+  if (total > INT32_MAX / 2) return DOPD_ERR_INVALID_SHAPE;
+  if (total == 0) return DOPD_OK;
+  hipStream_t strm = as_stream(stream);
+  if (d == 64)
+    hipLaunchKernelGGL(dopd::pd_step_kernel<64>, dim3((unsigned)total), dim3(dopd::kPfThreads), 0, strm, p);
+  else
+    hipLaunchKernelGGL(dopd::pd_step_kernel<128>, dim3((unsigned)total), dim3(dopd::kPfThreads), 0, strm, p);
+  st = launch_status();
+  if (st != DOPD_OK || !merge) return st;
+  return launch_decode_merge(p.dec, d, strm);
 }
 
 // ---------------------------------------------------------------- handoff pack

@@ -109,18 +109,28 @@ __device__ __forceinline__ bf16x8 dec_k_operand(const KArr& k, int i) {
   }
 }
 
+// LDS of the wave merge of one decode workgroup: (m, l) of waves 1..3,
+// [wave - 1][2][64] floats, and their partial outputs, one block of
+// [D / 16][64] f32x4 per wave (8 KiB at d = 128).
+template <int D>
+constexpr int dec_wave_o_bytes() { return (D / 16) * 64 * 16; }
+constexpr int kDecMlBytes = (kDecWaves - 1) * 2 * 64 * 4;
+
+// Workgroup b of the decode partition (its slice of the work units).
+// s_ml: kDecMlBytes of LDS; s_o1, s_o2, s_o3: the partial-output blocks of
+// waves 1, 2 and 3.
 template <int D, bool KV8>
-__global__ __launch_bounds__(256, 2) void decode_split_kernel(DecodeArgs a) {
+__device__ __forceinline__ void decode_workgroup(const DecodeArgs& a, int b, float* s_ml,
+                                                 f32x4* s_o1, f32x4* s_o2, f32x4* s_o3) {
+  auto s_o = [&](int i) { return i == 0 ? s_o1 : (i == 1 ? s_o2 : s_o3); };
   using KT = std::conditional_t<KV8, uint8_t, uint16_t>;
   constexpr int NQK = D / 32;  // QK MFMAs (k = 32) per 16-token row block
   constexpr int NT = D / 16;   // O^T tiles of 16 dims
   constexpr int SPAN = D / 4;  // contiguous dims of a K row read by one lane
-  __shared__ float s_ml[kDecWaves - 1][2][64];
-  __shared__ f32x4 s_o[kDecWaves - 1][NT][64];
 
   const int tid = threadIdx.x, l = lane_id(), w = tid >> 6;
   const int hq = a.hq, hkv = a.hkv, g = hq / hkv;
-  const int b = blockIdx.x;
+  if (b >= a.nwg) return;  // uniform
   const int lo = dec_slice_begin(a, b), hi_unit = dec_slice_begin(a, b + 1);
   if (lo >= hi_unit) return;  // uniform
 
@@ -313,10 +323,10 @@ __global__ __launch_bounds__(256, 2) void decode_split_kernel(DecodeArgs a) {
 
     // ---- merge the four waves in wave 0 (identical lane layouts)
     if (w > 0) {
-      s_ml[w - 1][0][l] = m_run;
-      s_ml[w - 1][1][l] = l_tot;
+      s_ml[(w - 1) * 128 + l] = m_run;
+      s_ml[(w - 1) * 128 + 64 + l] = l_tot;
 #pragma unroll
-      for (int n = 0; n < NT; ++n) s_o[w - 1][n][l] = oacc[n];
+      for (int n = 0; n < NT; ++n) s_o(w - 1)[n * 64 + l] = oacc[n];
     }
     __syncthreads();
     if (w == 0) {
@@ -326,8 +336,8 @@ __global__ __launch_bounds__(256, 2) void decode_split_kernel(DecodeArgs a) {
       float M = m_run;
 #pragma unroll
       for (int i = 1; i < kDecWaves; ++i) {
-        mw[i] = s_ml[i - 1][0][l];
-        lw[i] = s_ml[i - 1][1][l];
+        mw[i] = s_ml[(i - 1) * 128 + l];
+        lw[i] = s_ml[(i - 1) * 128 + 64 + l];
         M = fmaxf(M, mw[i]);
       }
       float sc[kDecWaves], L = 0.f;
@@ -341,7 +351,7 @@ __global__ __launch_bounds__(256, 2) void decode_split_kernel(DecodeArgs a) {
       for (int n = 0; n < NT; ++n) {
         f32x4 o = oacc[n] * sc[0];
 #pragma unroll
-        for (int i = 1; i < kDecWaves; ++i) o += s_o[i - 1][n][l] * sc[i];
+        for (int i = 1; i < kDecWaves; ++i) o += s_o(i - 1)[n * 64 + l] * sc[i];
         oacc[n] = KV8 ? o * vsc : o;
       }
       const int head = c * g + hl;
@@ -368,6 +378,13 @@ __global__ __launch_bounds__(256, 2) void decode_split_kernel(DecodeArgs a) {
     }
     __syncthreads();  // the LDS merge buffers are reused by the next segment
   }
+}
+
+template <int D, bool KV8>
+__global__ __launch_bounds__(256, 2) void decode_split_kernel(DecodeArgs a) {
+  __shared__ __attribute__((aligned(16))) float s_ml[kDecMlBytes / 4];
+  __shared__ __attribute__((aligned(16))) f32x4 s_o[kDecWaves - 1][D / 16 * 64];
+  decode_workgroup<D, KV8>(a, (int)blockIdx.x, s_ml, s_o[0], s_o[1], s_o[2]);
 }
 
 // Merges the partials of every (r, c) whose pairs span more than one slice.

@@ -147,33 +147,40 @@ __device__ __forceinline__ bool pf_find_item(const PrefillArgs& a, int b, int& t
                      : pf_find_item_lpt(a, b, tile, req, slot);
 }
 
+// LDS of one prefill workgroup: K and V tiles, double-buffered, BN x D bf16
+// each, and (dense kernel) a copy of Q operands KS/2 .. KS-1 of every lane,
+// [ks - KS/2][thread][8] (16 KiB at d = 128: two workgroups still fit a CU).
+// The diagonal steps read those from LDS, so the registers are free there and
+// the compiler does not spill the Q operands to scratch (whose reloads would
+// wait for the step's tile loads).
+template <int D>
+constexpr int pf_tile_elems() { return kPfBN * D; }
+template <int D, bool PAGED>
+constexpr int pf_q_lds_elems() { return PAGED ? 8 : (D / 32) * kPfThreads * 8; }
+
+// One prefill work item (q tile, request, head; with key splits one split of
+// it): workgroup `bid` of the prefill's own numbering.  The LDS buffers are
+// separate __shared__ arrays of the calling kernel, one per (K/V, buffer):
+// with compile-time buffer choices the compiler can tell that LDS reads of one
+// buffer never alias the in-flight global->LDS loads into another, and does
+// not wait for them.
 // PAGED = false: fresh prompts, K/V token-major beside Q (dopd_prefill_attn).
 // PAGED = true: chunks attending to the paged cache (dopd_prefill_paged_attn).
 template <int D, bool PAGED>
-__global__ __launch_bounds__(kPfThreads, 2) void prefill_bf16_kernel(PrefillArgs a) {
+__device__ __forceinline__ void prefill_workgroup(const PrefillArgs& a, int bid, uint16_t* sK0,
+                                                  uint16_t* sK1, uint16_t* sV0, uint16_t* sV1,
+                                                  uint16_t* sQ) {
   constexpr int BM = kPfBM, BN = kPfBN;
   constexpr int KS = D / 16;     // k-steps of the QK MFMA
   constexpr int ET = D / 32;     // O^T tiles of 32 dims
   constexpr int CPR = D / 8;     // 16-byte chunks per K/V row
   constexpr int KQW = BN * CPR / kPfThreads;   // 16-byte chunks of a K (or V) tile per thread
-  // One array per (K/V, buffer): with compile-time buffer choices the
-  // compiler can tell that LDS reads of one buffer never alias the in-flight
-  // global->LDS loads into another, and does not wait for them.
-  __shared__ __attribute__((aligned(16))) uint16_t sK0[BN * D], sK1[BN * D];
-  __shared__ __attribute__((aligned(16))) uint16_t sV0[BN * D], sV1[BN * D];
-  // Dense kernel: a copy of Q operands KS/2 .. KS-1 of every lane,
-  // [ks - KS/2][thread][8] (16 KiB at d = 128: two workgroups still fit a
-  // CU).  The diagonal steps read them from here, so those registers are free
-  // there and the compiler does not spill the Q operands to scratch (whose
-  // reloads would wait for the step's tile loads).
-  constexpr int kQLds = PAGED ? 8 : (KS / 2) * kPfThreads * 8;
-  __shared__ __attribute__((aligned(16))) uint16_t sQ[kQLds];
   auto kbuf = [&](int b) { return b ? sK1 : sK0; };
   auto vbuf = [&](int b) { return b ? sV1 : sV0; };
 
-  const int split = PAGED ? (int)blockIdx.x % a.nsplit : 0;
+  const int split = PAGED ? bid % a.nsplit : 0;
   int tile, r, h;
-  if (!pf_find_item(a, PAGED ? (int)blockIdx.x / a.nsplit : (int)blockIdx.x, tile, r, h))
+  if (!pf_find_item(a, PAGED ? bid / a.nsplit : bid, tile, r, h))
     return;  // uniform across the workgroup
   // The item is wave-uniform; say so, so that what derives from it stays scalar.
   tile = __builtin_amdgcn_readfirstlane(tile);
@@ -683,6 +690,14 @@ __global__ __launch_bounds__(kPfThreads, 2) void prefill_bf16_kernel(PrefillArgs
     if (a.lse && hi == 0 && myq < L)
       a.lse[(int64_t)(seq0 + myq) * a.hq + h] = (m_run + __log2f(l_tot)) * kLn2;
   }
+}
+
+template <int D, bool PAGED>
+__global__ __launch_bounds__(kPfThreads, 2) void prefill_bf16_kernel(PrefillArgs a) {
+  __shared__ __attribute__((aligned(16))) uint16_t sK0[pf_tile_elems<D>()], sK1[pf_tile_elems<D>()];
+  __shared__ __attribute__((aligned(16))) uint16_t sV0[pf_tile_elems<D>()], sV1[pf_tile_elems<D>()];
+  __shared__ __attribute__((aligned(16))) uint16_t sQ[pf_q_lds_elems<D, PAGED>()];
+  prefill_workgroup<D, PAGED>(a, (int)blockIdx.x, sK0, sK1, sV0, sV1, sQ);
 }
 
 // Combines the key splits of the paged prefill.  Thread = one 4-dim chunk of

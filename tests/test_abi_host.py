@@ -284,3 +284,63 @@ def test_prefill_paged_split_host_validation(lib):
     assert call(4, FAKE + 64, need) == A.DOPD_ERR_INVALID_SHAPE   # not 256-byte aligned
     assert call(-1, FAKE, need) == A.DOPD_ERR_INVALID_SHAPE
     assert call(4, FAKE, need, stride=39) == A.DOPD_ERR_INVALID_SHAPE  # table too narrow
+
+
+def _write_pack(lib, shape, cu, stride=64, out=FAKE, offs=FAKE, nreq=None):
+    cu = np.asarray(cu, np.int32)
+    p = C.c_void_p(FAKE)
+    n = len(cu) - 1 if nreq is None else nreq
+    return lib.dopd_kv_write_pack_for_handoff(
+        C.byref(shape), p, p, p, p, 100, p, stride, p, A._hptr(cu), n,
+        C.c_void_p(offs) if offs else None, C.c_void_p(out) if out else None, None)
+
+
+def test_write_pack_host_validation(lib):
+    s = _shape()
+    assert _write_pack(lib, _shape(dtype="fp32"), [0, 4]) == A.DOPD_ERR_UNSUPPORTED
+    assert _write_pack(lib, _shape(dtype="fp8"), [0, 4]) == A.DOPD_ERR_UNSUPPORTED
+    assert _write_pack(lib, s, [0, 4], out=0) == A.DOPD_ERR_NULL_POINTER      # offsets without buffer
+    assert _write_pack(lib, s, [0, 4], offs=0) == A.DOPD_ERR_NULL_POINTER     # buffer without offsets
+    assert _write_pack(lib, s, [1, 4]) == A.DOPD_ERR_INVALID_SHAPE           # cu[0] != 0
+    assert _write_pack(lib, s, [0, 4, 2]) == A.DOPD_ERR_INVALID_SHAPE        # negative length
+    assert _write_pack(lib, s, [0, 100], stride=6) == A.DOPD_ERR_INVALID_SHAPE  # 7 pages > 6 columns
+    assert _write_pack(lib, s, [0], nreq=0) == A.DOPD_OK
+    assert _write_pack(lib, s, [0, 0, 0]) == A.DOPD_OK                       # nothing to write
+
+
+def _pd(lib, shape, ctx, cu, schedule=0, stride=1024, ws_bytes=1 << 30, ws=FAKE, h_out=FAKE,
+        h_offs=FAKE):
+    ctx = np.asarray(ctx, np.int32)
+    cu = np.asarray(cu, np.int32)
+    p = C.c_void_p(FAKE)
+    return lib.dopd_pd_step(
+        C.byref(shape), p, p, p, A._hptr(ctx), len(ctx), p, None, p, p, p, p, A._hptr(cu),
+        len(cu) - 1, p, p, None, p, p, 100, stride, C.c_void_p(h_offs) if h_offs else None,
+        C.c_void_p(h_out) if h_out else None, schedule, C.c_void_p(ws) if ws else None, ws_bytes,
+        None)
+
+
+def test_pd_step_host_validation(lib):
+    s = _shape(hq=28, hkv=4)
+    assert _pd(lib, _shape(dtype="fp32"), [5], [0, 4]) == A.DOPD_ERR_UNSUPPORTED
+    assert _pd(lib, s, [5, 0], [0, 4]) == A.DOPD_ERR_INVALID_SHAPE      # context < 1
+    assert _pd(lib, s, [5], [0, 4], schedule=3) == A.DOPD_ERR_INVALID_SHAPE
+    assert _pd(lib, s, [5], [2, 4]) == A.DOPD_ERR_INVALID_SHAPE         # cu[0] != 0
+    assert _pd(lib, s, [5000], [0, 4], stride=8) == A.DOPD_ERR_INVALID_SHAPE
+    assert _pd(lib, s, [5], [0, 400], stride=8) == A.DOPD_ERR_INVALID_SHAPE
+    assert _pd(lib, s, [5], [0, 4], h_out=0) == A.DOPD_ERR_NULL_POINTER
+    assert _pd(lib, s, [5], [0, 4], ws=0) == A.DOPD_ERR_NULL_POINTER
+    assert _pd(lib, s, [5], [0, 4], ws=FAKE + 8) == A.DOPD_ERR_INVALID_SHAPE  # misaligned
+    for sched in (A.DOPD_PD_AUTO, A.DOPD_PD_PREFILL_FIRST, A.DOPD_PD_DECODE_FIRST):
+        need = A.dopd_pd_step_workspace_size(s, [3000, 17], 2, sched)
+        assert need >= 256 and need % 256 == 0
+        assert _pd(lib, s, [3000, 17], [0, 4], schedule=sched, ws_bytes=need - 1) == \
+            A.DOPD_ERR_WORKSPACE_TOO_SMALL
+    # one decode slice per CU needs no more partial slots than two
+    assert A.dopd_pd_step_workspace_size(s, [16384] * 8, 8, A.DOPD_PD_DECODE_FIRST) <= \
+        A.dopd_pd_step_workspace_size(s, [16384] * 8, 8, A.DOPD_PD_PREFILL_FIRST)
+    assert A.dopd_pd_step_workspace_size(s, [5], 1, 7) == 0
+    # both batches empty: nothing to do
+    assert lib.dopd_pd_step(C.byref(s), None, None, None, None, 0, None, None, None, None, None,
+                            None, None, 0, None, None, None, None, None, 0, 0, None, None, 0,
+                            None, 0, None) == A.DOPD_OK
