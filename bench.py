@@ -15,7 +15,8 @@ MALL (write 1 GiB, read another 1 GiB; outside the timed region), and as many
 warm reps.  Every C-ABI call is bracketed by HIP events on the stream it runs
 on; the per-call tables give median, p10 and p90.  The headline value is the
 decode call's algorithmic HBM bytes over its cold median.  After the headline,
-the same step as one PD-aggregated launch (``pd_step``), and the decode MHA
+the same step as one PD-aggregated launch (``pd_step``), the step's write and
+pack as separate calls and as one pass (``write_pack``), and the decode MHA
 7B-shaped, varlen prefill + paged write and GQA 70B-shaped decode workloads
 are measured the same way (``configs``), each with its own oracle baseline on
 the host cores.  ``--workload`` selects any single workload
@@ -42,7 +43,11 @@ HBM_PEAK_GBS = 8000.0       # MI355X HBM3E
 BF16_PEAK_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PROFILES = os.path.join(ROOT, "profiles")
 KERNEL_SOURCES = ("paper_2511_20982_amd/csrc/dopd_attn.hip",
+                  "paper_2511_20982_amd/csrc/plan.hpp",
+                  "paper_2511_20982_amd/csrc/kernels/kv_write_pack.hpp",
+                  "paper_2511_20982_amd/csrc/kernels/pd_step.hpp",
                   "paper_2511_20982_amd/csrc/kernels/common.hpp",
+                  "paper_2511_20982_amd/csrc/kernels/attn_f32.hpp",
                   "paper_2511_20982_amd/csrc/kernels/decode_bf16.hpp",
                   "paper_2511_20982_amd/csrc/kernels/prefill_bf16.hpp",
                   "paper_2511_20982_amd/csrc/kernels/kv_write.hpp",
@@ -57,7 +62,8 @@ CALL_KERNELS = {"decode": ("decode_split_kernel", "decode_merge_kernel"),
                                     "prefill_split_merge_kernel"),
                 "kv_write": ("kv_write_kernel",),
                 "pack": ("kv_pack_kernel",), "unpack": ("kv_unpack_kernel",),
-                "pd_step": ("pd_step_kernel", "decode_merge_kernel")}
+                "pd_step": ("pd_step_kernel", "decode_merge_kernel"),
+                "kv_write_pack": ("kv_write_pack_kernel",)}
 
 WORKLOADS = {
     "mixed": ("mixed P/D step + handoff: prefill 8x512, decode 192 req ctx lognormal(2048,0.7) "
@@ -75,6 +81,9 @@ WORKLOADS = {
     "pd_step": ("the mixed P/D step + handoff of the mixed workload as one PD-aggregated launch "
                 "(dopd_pd_step: decode slices, prefill items and write+pack workgroups in one "
                 "grid, then the decode merge)", 5),
+    "write_pack": ("paged write + handoff pack of the mixed step's 8 x 512 fresh prompts (28/4 "
+                   "heads, d128, bf16, 1 layer): the separate write and pack calls, then the "
+                   "one-pass write+pack (dopd_kv_write_pack_for_handoff)", 5),
     "handoff": ("P->D handoff on one GPU: pack 8 prefilled requests x 512 tokens from the P pool, "
                 "unpack into a D pool with another page order; 28/4 heads, d128, bf16, "
                 "--pack-layers layers", 5),
@@ -94,6 +103,14 @@ def decode_bytes(ctx, hq, hkv, d, s=2, kv_s=None):
 def prefill_flops(lens, hq, d):
     lens = np.asarray(lens, np.int64)
     return int((4 * d * hq * lens * (lens + 1) // 2).sum())
+
+
+def write_pack_bytes(lens, hkv, d, s=2):
+    """K and V read once, written to the pages and to the handoff buffer; page ids, lengths."""
+    lens = np.asarray(lens, np.int64)
+    t = int(lens.sum())
+    return int(2 * t * hkv * d * 3 * s + 4 * ((lens + 15) // 16).sum() + 8 * len(lens) +
+               8 * len(lens))
 
 
 def write_bytes(lens, hkv, d, s=2, out_s=None):
@@ -166,14 +183,17 @@ def summarize(args):
         # its launches per launch of the call's first kernel.
         kcalls = {}
         for call, kernels in CALL_KERNELS.items():
-            match = [r for r in rows if any(k in r["Name"] for k in kernels)]
-            if not match:
+            # a call is present when its first kernel ran (the others it may add
+            # are shared with other calls: the decode merge kernel)
+            if not any(kernels[0] in r["Name"] for r in rows):
                 continue
+            match = [r for r in rows if any(k in r["Name"] for k in kernels)]
             first = next(r for k in kernels for r in match if k in r["Name"])
             n_calls = float(first["Calls"])
             us = sum(float(r["AverageNs"]) * float(r["Calls"]) for r in match) / n_calls / 1e3
             kcalls[call] = {"avg_us": round(us, 3), "calls": int(n_calls),
                             "kernels": [r["Name"][:90] for r in match]}
+        os.makedirs(args.traffic_dir, exist_ok=True)
         with open(os.path.join(args.traffic_dir, f"kernels_{args.label}.json"), "w") as f:
             json.dump({"workload": args.label, "source_hash": source_hash(), "calls": kcalls,
                        "command": args.command}, f, indent=1)
@@ -206,13 +226,15 @@ def summarize(args):
         out.append("| kernel | dispatches | FETCH_SIZE KiB | WRITE_SIZE KiB |")
         out.append("|---|---|---|---|")
         calls = {}
+        present = {call for call, kernels in CALL_KERNELS.items()
+                   if any(kernels[0] in kname for kname in per)}
         for kname, ctrs in sorted(per.items()):
             f_k = float(np.median(ctrs["FETCH_SIZE"])) if "FETCH_SIZE" in ctrs else float("nan")
             w_k = float(np.median(ctrs["WRITE_SIZE"])) if "WRITE_SIZE" in ctrs else float("nan")
             n = max(len(ctrs.get("FETCH_SIZE", [])), len(ctrs.get("WRITE_SIZE", [])))
             out.append(f"| {kname[:90]} | {n} | {f_k:.0f} | {w_k:.0f} |")
             for call, kernels in CALL_KERNELS.items():
-                if any(k in kname for k in kernels):
+                if call in present and any(k in kname for k in kernels):
                     c = calls.setdefault(call, {"fetch_kib": 0.0, "write_kib": 0.0, "kernels": []})
                     c["fetch_kib"] += f_k
                     c["write_kib"] += w_k
@@ -463,6 +485,51 @@ def build_workload(name, args, torch, A, I, sA):
 
         return Workload(name, desc, w.seed, [("pd_step", step)], work, "pd_step", cpu,
                         extra={"schedule": args.schedule})
+
+    if name == "write_pack":
+        n_pre, n_dec = len(w.prefill_lens), len(w.context_lens)
+        kp, vp = A.to_device(w.k_pool), A.to_device(w.v_pool)
+        pt = A.to_device(w.page_table)
+        stride = w.page_table.shape[1]
+        k, v = A.to_device(w.k), A.to_device(w.v)
+        cu = A.to_device(w.cu_seqlens)
+        start = torch.zeros(n_pre, dtype=torch.int32, device=dev)
+        offs_np = I.handoff_offsets(w.prefill_lens, 1, w.hkv, w.d)
+        offs = A.to_device(offs_np)
+        hreq, hlen = A.to_device(w.handoff_reqs), A.to_device(w.handoff_lens)
+        out_h = torch.empty(int(offs_np[-1]), dtype=torch.bfloat16, device=dev)
+        out_h2 = torch.empty_like(out_h)
+        T = int(w.cu_seqlens[-1])
+
+        def write():
+            A.dopd_kv_write(shape, k, v, kp, vp, w.num_pages, pt[n_dec:], stride, cu, start,
+                            n_pre, T, sA)
+
+        def pack():
+            A.dopd_kv_pack_for_handoff(shape, 1, kp, vp, w.num_pages, pt, stride, hreq, hlen,
+                                       w.handoff_lens, offs, n_pre, out_h, sA)
+
+        def write_pack():
+            A.dopd_kv_write_pack_for_handoff(shape, k, v, kp, vp, w.num_pages, pt[n_dec:],
+                                             stride, cu, w.cu_seqlens, n_pre, offs, out_h2, sA)
+
+        work = {"kv_write": ("GB/s", write_bytes(w.prefill_lens, w.hkv, w.d)),
+                "pack": ("GB/s", pack_bytes(w.handoff_lens, 1, w.hkv, w.d)),
+                "kv_write_pack": ("GB/s", write_pack_bytes(w.prefill_lens, w.hkv, w.d))}
+
+        def cpu():
+            import oracle
+            rk, rv = oracle.kv_write(w.k, w.v, w.k_pool, w.v_pool, w.page_table[n_dec:],
+                                     w.cu_seqlens, np.zeros(n_pre, np.int32))
+            ref_h = oracle.pack(rk, rv, 1, w.page_table, w.handoff_reqs, w.handoff_lens, offs_np)
+            return None, {"kv_write_bit_exact": bool(np.array_equal(A.to_host(kp), rk) and
+                                                     np.array_equal(A.to_host(vp), rv)),
+                          "pack_bit_exact": bool(np.array_equal(A.to_host(out_h), ref_h)),
+                          "write_pack_bit_exact": bool(np.array_equal(A.to_host(out_h2), ref_h))}
+
+        return Workload(name, desc, w.seed, [("kv_write", write), ("pack", pack),
+                                             ("kv_write_pack", write_pack)], work,
+                        "kv_write_pack", cpu)
 
     if name in ("decode_mha", "decode_gqa"):
         kp, vp = A.to_device(w.k_pool), A.to_device(w.v_pool)
@@ -762,8 +829,8 @@ def main():
                          "warm reps)")
     ap.add_argument("--workload", choices=sorted(WORKLOADS), default="mixed")
     ap.add_argument("--no-configs", action="store_true",
-                    help="with the mixed workload: skip the pd_step, decode_mha, prefill and "
-                         "decode_gqa workloads measured after it")
+                    help="with the mixed workload: skip the pd_step, write_pack, decode_mha, "
+                         "prefill and decode_gqa workloads measured after it")
     ap.add_argument("--pack-layers", type=int, default=1,
                     help="layers packed per handoff in the mixed step (1 = the configured step)")
     ap.add_argument("--split", type=int, default=0, help="decode split tokens (0 = automatic)")
@@ -775,9 +842,10 @@ def main():
     ap.add_argument("--order", choices=("decode-first", "prefill-first"), default="decode-first",
                     help="mixed step: the decode batch before the prefill, write and pack (its "
                          "tokens are the TPOT-bound ones), or after the write")
-    ap.add_argument("--schedule", type=int, default=0, choices=(0, 1, 2),
+    ap.add_argument("--schedule", type=int, default=0, choices=(0, 1, 2, 3),
                     help="pd_step workload: block order of the single launch (0 = automatic, "
-                         "1 = prefill first, 2 = decode first with one decode slice per CU)")
+                         "1 = prefill first, 2 = decode first with one decode slice per CU, "
+                         "3 = decode first with three slices per two CUs)")
     ap.add_argument("--kv", choices=("bf16", "fp8"), default="bf16",
                     help="KV cache element type (fp8 = E4M3 pages with per-KV-head scales): "
                          "decode workloads read it (written by the fp8 writer before timing), "
@@ -843,7 +911,7 @@ def main():
     if args.workload == "mixed" and not args.no_configs:
         sub = argparse.Namespace(**vars(args))
         sub.cpu_seconds = args.cpu_seconds / 2
-        for name in ("pd_step", "decode_mha", "prefill", "decode_gqa"):
+        for name in ("pd_step", "write_pack", "decode_mha", "prefill", "decode_gqa"):
             wl2 = build_workload(name, sub, torch, A, I, sA)
             configs[name] = run_workload(wl2, sub, torch, sA, flush, 0, args.warmup, args.reps)
             configs[name].pop("ms_per_step")

@@ -352,8 +352,10 @@ enum {
   DOPD_PD_AUTO = 0,           /* the library's choice (DOPD_PD_PREFILL_FIRST)          */
   DOPD_PD_PREFILL_FIRST = 1,  /* write/pack and prefill workgroups dispatched first,
                                  then the decode slices (two per CU)                   */
-  DOPD_PD_DECODE_FIRST = 2    /* the decode slices first, one per CU, then the
+  DOPD_PD_DECODE_FIRST = 2,   /* the decode slices first, one per CU, then the
                                  write/pack and prefill workgroups in the other slot    */
+  DOPD_PD_DECODE_FIRST_WIDE = 3 /* the decode slices first, three per two CUs; the
+                                 write/pack and prefill workgroups in the slots left    */
 };
 
 /*

@@ -22,7 +22,7 @@ DOPD_OK, DOPD_ERR_NULL_POINTER, DOPD_ERR_INVALID_SHAPE = 0, 1, 2
 DOPD_ERR_UNSUPPORTED, DOPD_ERR_WORKSPACE_TOO_SMALL, DOPD_ERR_HIP = 3, 4, 5
 DOPD_ERR_UNSUPPORTED_DTYPE = DOPD_ERR_UNSUPPORTED
 DOPD_BF16, DOPD_FP32, DOPD_FP8_E4M3 = 0, 1, 2
-DOPD_PD_AUTO, DOPD_PD_PREFILL_FIRST, DOPD_PD_DECODE_FIRST = 0, 1, 2
+DOPD_PD_AUTO, DOPD_PD_PREFILL_FIRST, DOPD_PD_DECODE_FIRST, DOPD_PD_DECODE_FIRST_WIDE = 0, 1, 2, 3
 PAGE_SIZE = 16
 
 EXPORTS = (

@@ -127,20 +127,20 @@ dopd_status check_decode_host(const dopd_attn_shape* s, const int32_t* ctx_host,
 }
 
 // Decode arguments and workspace layout of the bf16-operand decode (bf16 or
-// E4M3 pools) after the host checks; wg_per_cu: resident decode workgroups per
-// CU the automatic partition plans for.
+// E4M3 pools) after the host checks; quarter_wgs: resident decode workgroups
+// per CU, in quarters, the automatic partition plans for.
 template <bool KV8>
 dopd_status plan_decode_bf16(const dopd_attn_shape* s, const void* q, const void* k_pool,
                              const void* v_pool, const float* k_scale, const float* v_scale,
                              const int32_t* pt, int32_t pt_stride, const int32_t* ctx,
                              const int32_t* ctx_host, int32_t nreq, int32_t split_tokens,
                              void* out, float* lse, void* workspace, size_t workspace_bytes,
-                             int wg_per_cu, dopd::DecodeArgs* a_out, bool* merge_out) {
+                             int quarter_wgs, dopd::DecodeArgs* a_out, bool* merge_out) {
   const int hkv = s->num_kv_heads, hq = s->num_q_heads, d = s->head_dim;
   const int64_t total = dopd::decode_total_units(ctx_host, nreq, hkv);
   if (total > INT32_MAX / 2) return DOPD_ERR_INVALID_SHAPE;
   const dopd::DecodeLayout L = dopd::decode_layout(hq / hkv, hkv, d, ctx_host, nreq,
-                                                   split_tokens, machine_shape(), wg_per_cu);
+                                                   split_tokens, machine_shape(), quarter_wgs);
   const int64_t nwg = L.nwg;
   if (!workspace) return DOPD_ERR_NULL_POINTER;
   if (workspace_bytes < L.total) return DOPD_ERR_WORKSPACE_TOO_SMALL;
@@ -195,7 +195,7 @@ dopd_status launch_decode_bf16(const dopd_attn_shape* s, const void* q, const vo
   const dopd_status pst = plan_decode_bf16<KV8>(s, q, k_pool, v_pool, k_scale, v_scale, pt,
                                                 pt_stride, ctx, ctx_host, nreq, split_tokens,
                                                 out, lse, workspace, workspace_bytes,
-                                                dopd::kWgPerCu, &a, &merge);
+                                                4 * dopd::kWgPerCu, &a, &merge);
   if (pst != DOPD_OK) return pst;
   if (s->head_dim == 64)
     hipLaunchKernelGGL((dopd::decode_split_kernel<64, KV8>), dim3((unsigned)a.nwg), dim3(256), 0, strm, a);
@@ -730,15 +730,30 @@ dopd_status dopd_kv_write_pack_for_handoff(const dopd_attn_shape* s, const void*
 }
 
 // ---------------------------------------------------------------- PD step
+extern "C++" {
+namespace {
+constexpr int kPdLastSchedule = DOPD_PD_DECODE_FIRST_WIDE;
+constexpr int kPdAutoSchedule = DOPD_PD_PREFILL_FIRST;
+
+// Decode workgroups per CU (in quarters) of a fused-step schedule.
+int pd_decode_quarters(int schedule) {
+  if (schedule == DOPD_PD_AUTO) schedule = kPdAutoSchedule;
+  switch (schedule) {
+    case DOPD_PD_DECODE_FIRST: return 4;       // one per CU
+    case DOPD_PD_DECODE_FIRST_WIDE: return 6;  // three per two CUs
+    default: return 4 * dopd::kWgPerCu;        // every slot
+  }
+}
+}  // namespace
+}  // extern "C++"
+
 size_t dopd_pd_step_workspace_size(const dopd_attn_shape* s, const int32_t* ctx_host,
                                    int32_t num_dec, int32_t schedule) {
   if (check_decode_host(s, ctx_host, num_dec, 0) != DOPD_OK) return 0;
-  if (s->dtype != DOPD_BF16 || schedule < DOPD_PD_AUTO || schedule > DOPD_PD_DECODE_FIRST)
-    return 0;
+  if (s->dtype != DOPD_BF16 || schedule < DOPD_PD_AUTO || schedule > kPdLastSchedule) return 0;
   if (num_dec == 0) return 256;
-  const int wg_per_cu = schedule == DOPD_PD_DECODE_FIRST ? 1 : dopd::kWgPerCu;
   return dopd::decode_layout(s->num_q_heads / s->num_kv_heads, s->num_kv_heads, s->head_dim,
-                             ctx_host, num_dec, 0, machine_shape(), wg_per_cu)
+                             ctx_host, num_dec, 0, machine_shape(), pd_decode_quarters(schedule))
       .total;
 }
 
@@ -754,7 +769,7 @@ dopd_status dopd_pd_step(const dopd_attn_shape* s, const void* q_dec,
   dopd_status st = check_decode_host(s, ctx_host, num_dec, 0);
   if (st != DOPD_OK) return st;
   if (s->dtype != DOPD_BF16) return DOPD_ERR_UNSUPPORTED;
-  if (schedule < DOPD_PD_AUTO || schedule > DOPD_PD_DECODE_FIRST || num_pre < 0 ||
+  if (schedule < DOPD_PD_AUTO || schedule > kPdLastSchedule || num_pre < 0 ||
       num_pages < 0 || pt_stride < 0)
     return DOPD_ERR_INVALID_SHAPE;
   if (num_dec == 0 && num_pre == 0) return DOPD_OK;
@@ -771,7 +786,7 @@ dopd_status dopd_pd_step(const dopd_attn_shape* s, const void* q_dec,
     st = check_fresh_prompts(cu_host, num_pre, pt_stride, &pages);
     if (st != DOPD_OK) return st;
   }
-  if (schedule == DOPD_PD_AUTO) schedule = DOPD_PD_PREFILL_FIRST;
+  if (schedule == DOPD_PD_AUTO) schedule = kPdAutoSchedule;
   const int hkv = s->num_kv_heads, d = s->head_dim;
   dopd::PdStepArgs p;
   std::memset(&p, 0, sizeof(p));
@@ -779,9 +794,8 @@ dopd_status dopd_pd_step(const dopd_attn_shape* s, const void* q_dec,
   if (num_dec > 0) {
     st = plan_decode_bf16<false>(s, q_dec, k_pool, v_pool, nullptr, nullptr, dec_page_table,
                                  pt_stride, ctx, ctx_host, num_dec, 0, out_dec, lse_dec,
-                                 workspace, workspace_bytes,
-                                 schedule == DOPD_PD_DECODE_FIRST ? 1 : dopd::kWgPerCu, &p.dec,
-                                 &merge);
+                                 workspace, workspace_bytes, pd_decode_quarters(schedule),
+                                 &p.dec, &merge);
     if (st != DOPD_OK) return st;
     p.n_dec = p.dec.nwg;
   }

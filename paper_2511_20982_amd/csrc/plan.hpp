@@ -42,17 +42,23 @@ inline int64_t decode_total_units(const int32_t* ctx, int32_t n, int hkv) {
   return units;
 }
 
+// Resident decode workgroup slots the automatic partition fills: quarter_wgs / 4
+// workgroups per CU (8 = two per CU, every slot; fewer leaves slots to the
+// prefill items of a fused step).
+inline int64_t decode_slots(const MachineShape& m, int quarter_wgs = 4 * kWgPerCu) {
+  return std::max<int64_t>(1, (int64_t)std::max(1, m.cus) * std::max(1, quarter_wgs) / 4);
+}
+
 // Workgroups of the partition: split_tokens / 32 units each when given, else
-// one slice per resident workgroup slot of the machine (one round), with
-// wg_per_cu decode workgroups resident per CU.
+// one slice per resident slot (one round).
 inline int64_t decode_nwg(int64_t total_units, int32_t split_tokens, const MachineShape& m,
-                          int wg_per_cu = kWgPerCu) {
+                          int quarter_wgs = 4 * kWgPerCu) {
   if (total_units <= 0) return 0;
   if (split_tokens > 0) {
     const int64_t per = split_tokens / 32;
     return (total_units + per - 1) / per;
   }
-  const int64_t slots = (int64_t)std::max(1, wg_per_cu) * std::max(1, m.cus);
+  const int64_t slots = decode_slots(m, quarter_wgs);
   return std::max<int64_t>(1, std::min(slots, (total_units + kDecMinPairsPerWg - 1) /
                                                   kDecMinPairsPerWg));
 }
@@ -67,9 +73,9 @@ struct DecodeLayout {
 
 inline DecodeLayout decode_layout(int g, int hkv, int d, const int32_t* ctx, int32_t n,
                                   int32_t split_tokens, const MachineShape& m,
-                                  int wg_per_cu = kWgPerCu) {
+                                  int quarter_wgs = 4 * kWgPerCu) {
   DecodeLayout L{};
-  L.nwg = decode_nwg(decode_total_units(ctx, n, hkv), split_tokens, m, wg_per_cu);
+  L.nwg = decode_nwg(decode_total_units(ctx, n, hkv), split_tokens, m, quarter_wgs);
   L.slots = L.nwg + (int64_t)n * hkv;
   L.part_o_off = 0;
   L.part_ml_off = align256((size_t)L.slots * g * d * sizeof(float));

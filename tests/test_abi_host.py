@@ -324,14 +324,15 @@ def test_pd_step_host_validation(lib):
     s = _shape(hq=28, hkv=4)
     assert _pd(lib, _shape(dtype="fp32"), [5], [0, 4]) == A.DOPD_ERR_UNSUPPORTED
     assert _pd(lib, s, [5, 0], [0, 4]) == A.DOPD_ERR_INVALID_SHAPE      # context < 1
-    assert _pd(lib, s, [5], [0, 4], schedule=3) == A.DOPD_ERR_INVALID_SHAPE
+    assert _pd(lib, s, [5], [0, 4], schedule=4) == A.DOPD_ERR_INVALID_SHAPE
     assert _pd(lib, s, [5], [2, 4]) == A.DOPD_ERR_INVALID_SHAPE         # cu[0] != 0
     assert _pd(lib, s, [5000], [0, 4], stride=8) == A.DOPD_ERR_INVALID_SHAPE
     assert _pd(lib, s, [5], [0, 400], stride=8) == A.DOPD_ERR_INVALID_SHAPE
     assert _pd(lib, s, [5], [0, 4], h_out=0) == A.DOPD_ERR_NULL_POINTER
     assert _pd(lib, s, [5], [0, 4], ws=0) == A.DOPD_ERR_NULL_POINTER
     assert _pd(lib, s, [5], [0, 4], ws=FAKE + 8) == A.DOPD_ERR_INVALID_SHAPE  # misaligned
-    for sched in (A.DOPD_PD_AUTO, A.DOPD_PD_PREFILL_FIRST, A.DOPD_PD_DECODE_FIRST):
+    for sched in (A.DOPD_PD_AUTO, A.DOPD_PD_PREFILL_FIRST, A.DOPD_PD_DECODE_FIRST,
+                  A.DOPD_PD_DECODE_FIRST_WIDE):
         need = A.dopd_pd_step_workspace_size(s, [3000, 17], 2, sched)
         assert need >= 256 and need % 256 == 0
         assert _pd(lib, s, [3000, 17], [0, 4], schedule=sched, ws_bytes=need - 1) == \
@@ -340,6 +341,8 @@ def test_pd_step_host_validation(lib):
     assert A.dopd_pd_step_workspace_size(s, [16384] * 8, 8, A.DOPD_PD_DECODE_FIRST) <= \
         A.dopd_pd_step_workspace_size(s, [16384] * 8, 8, A.DOPD_PD_PREFILL_FIRST)
     assert A.dopd_pd_step_workspace_size(s, [5], 1, 7) == 0
+    assert A.dopd_pd_step_workspace_size(s, [16384] * 8, 8, A.DOPD_PD_DECODE_FIRST_WIDE) <= \
+        A.dopd_pd_step_workspace_size(s, [16384] * 8, 8, A.DOPD_PD_PREFILL_FIRST)
     # both batches empty: nothing to do
     assert lib.dopd_pd_step(C.byref(s), None, None, None, None, 0, None, None, None, None, None,
                             None, None, 0, None, None, None, None, None, 0, 0, None, None, 0,

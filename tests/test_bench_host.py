@@ -43,6 +43,11 @@ def test_prefill_flops_closed_form():
     assert B.prefill_flops([1, 4], hq=3, d=8) == 4 * 8 * 3 * (1 + 10)
 
 
+def test_write_pack_bytes_closed_form():
+    # K and V read once and written twice (pages and handoff buffer), page ids, lengths, offsets
+    assert B.write_pack_bytes([17], hkv=1, d=4) == 2 * 17 * 4 * 3 * 2 + 4 * 2 + 8 + 8
+
+
 def test_write_and_pack_bytes_closed_form():
     assert B.write_bytes([17], hkv=1, d=4) == 2 * 17 * 4 * 4 + 4 * 2 + 8
     assert B.write_bytes([17], hkv=1, d=4, out_s=1) == 2 * 17 * 4 * 3 + 4 * 2 + 8

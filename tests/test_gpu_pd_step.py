@@ -19,7 +19,8 @@ def _gpu(require_gpu):
 
 from tests import gpu_util as G  # noqa: E402
 
-SCHEDULES = [A.DOPD_PD_AUTO, A.DOPD_PD_PREFILL_FIRST, A.DOPD_PD_DECODE_FIRST]
+SCHEDULES = [A.DOPD_PD_AUTO, A.DOPD_PD_PREFILL_FIRST, A.DOPD_PD_DECODE_FIRST,
+             A.DOPD_PD_DECODE_FIRST_WIDE]
 
 
 def _handoff_ref(k, v, kp, vp, pt, cu, lens, offs, hkv, d):
@@ -150,7 +151,7 @@ def _small_case(seed, dec_ctx, pre_lens, hq, hkv, d):
     return w
 
 
-@pytest.mark.parametrize("schedule", [A.DOPD_PD_PREFILL_FIRST, A.DOPD_PD_DECODE_FIRST])
+@pytest.mark.parametrize("schedule", SCHEDULES[1:])
 @pytest.mark.parametrize("hq,hkv,d", [(28, 4, 128), (8, 8, 64), (7, 1, 128)])
 def test_pd_step_ragged(hq, hkv, d, schedule):
     """Ragged decode contexts and prompt lengths (empty prompts included)."""
@@ -192,7 +193,7 @@ def test_pd_step_one_batch_empty(which):
 def test_pd_step_repeat_runs_bit_identical():
     w = I.config5()
     sh = G.shape_of(w)
-    for schedule in (A.DOPD_PD_PREFILL_FIRST, A.DOPD_PD_DECODE_FIRST):
+    for schedule in SCHEDULES[1:]:
         a = _run_pd_step(w, sh, schedule)
         b = _run_pd_step(w, sh, schedule)
         for key in ("out_d", "out_p", "lse_d", "lse_p", "kp", "vp", "out_h"):
