@@ -45,9 +45,12 @@ def _lib():
         lib.oracle_e4m3_quantize.argtypes = [i32, C.c_int64, i32, i32, P, P, P]
         lib.oracle_decode_e4m3.argtypes = [i32, i32, i32, i32, C.c_float, P, P, P, P, P, P, i32,
                                            P, i32, P, P]
+        lib.oracle_prefill_paged_e4m3.argtypes = [i32, i32, i32, i32, C.c_float, P, P, P, P, P,
+                                                  P, i32, P, P, i32, P, P, i32, P, P]
         for f in (lib.oracle_prefill, lib.oracle_prefill_rows, lib.oracle_decode,
                   lib.oracle_kv_write, lib.oracle_pack, lib.oracle_unpack,
-                  lib.oracle_prefill_paged, lib.oracle_e4m3_quantize, lib.oracle_decode_e4m3):
+                  lib.oracle_prefill_paged, lib.oracle_e4m3_quantize, lib.oracle_decode_e4m3,
+                  lib.oracle_prefill_paged_e4m3):
             f.restype = i32
         _LIB = lib
     return _LIB
@@ -244,4 +247,39 @@ def decode_e4m3(q, k_pool, v_pool, k_scale, v_scale, page_table, context_lens, s
                                    _p(out), _p(lse))
     if rc:
         raise ValueError(f"oracle_decode_e4m3 rc={rc}")
+    return out, lse
+
+
+def prefill_paged_e4m3(q, k_pool, v_pool, k_scale, v_scale, page_table, cu_q, prefix_lens, scale,
+                       tok=None, head=None):
+    """Chunk prefill over E4M3 pools (uint8 codes, same page layouts) with
+    per-KV-head scales (key = value(code) * k_scale[c], value = value(code) *
+    v_scale[c]); q bf16 bits or fp32 [T][Hq][d] -> (out[T][Hq][d], lse[T][Hq]),
+    or, with tok/head given, the (out[n][d], lse[n]) of those rows only."""
+    q = _c(q)
+    k_pool, v_pool = _c(k_pool, np.uint8), _c(v_pool, np.uint8)
+    ks, vs = _c(k_scale, np.float32), _c(v_scale, np.float32)
+    pt = _c(page_table, np.int32)
+    cu = _c(cu_q, np.int32)
+    pre = _c(prefix_lens, np.int32)
+    t, hq, d = q.shape
+    hkv = k_pool.shape[-3]
+    if tok is None:
+        tk = hd = None
+        nrows = 0
+        out = np.zeros((t, hq, d), np.float64)
+        lse = np.zeros((t, hq), np.float64)
+    else:
+        tk, hd = _c(tok, np.int32), _c(head, np.int32)
+        nrows = len(tk)
+        out = np.zeros((nrows, d), np.float64)
+        lse = np.zeros((nrows,), np.float64)
+    rc = _lib().oracle_prefill_paged_e4m3(_dt(q), hq, hkv, d, float(scale), _p(q), _p(k_pool),
+                                          _p(v_pool), _p(ks), _p(vs), _p(pt), pt.shape[1],
+                                          _p(cu), _p(pre), len(cu) - 1,
+                                          _p(tk) if tk is not None else None,
+                                          _p(hd) if hd is not None else None, nrows, _p(out),
+                                          _p(lse))
+    if rc:
+        raise ValueError(f"oracle_prefill_paged_e4m3 rc={rc}")
     return out, lse

@@ -286,11 +286,12 @@ int oracle_decode_e4m3(int qdtype, int hq, int hkv, int d, float scale, const vo
  * of the cache.  q/out [T][Hq][d], lse [T][Hq].  With rows != NULL only the
  * nrows (token, head) pairs tok[n], head[n] are computed, into out[n][d] and
  * lse[n]. */
-int oracle_prefill_paged(int dtype, int hq, int hkv, int d, float scale, const void *q,
-                         const void *k_pool, const void *v_pool, const int32_t *page_table,
-                         int pt_stride, const int32_t *cu_q, const int32_t *prefix_lens,
-                         int nreq, const int32_t *tok, const int32_t *head, int nrows,
-                         double *out, double *lse) {
+static int prefill_paged_impl(int qdt, int kvdt, const float *k_scale, const float *v_scale,
+                              int hq, int hkv, int d, float scale, const void *q,
+                              const void *k_pool, const void *v_pool, const int32_t *page_table,
+                              int pt_stride, const int32_t *cu_q, const int32_t *prefix_lens,
+                              int nreq, const int32_t *tok, const int32_t *head, int nrows,
+                              double *out, double *lse) {
   if (hkv <= 0 || hq % hkv) return 1;
   const int g = hq / hkv;
   const double sigma = (double)scale;
@@ -327,14 +328,42 @@ int oracle_prefill_paged(int dtype, int hq, int hkv, int d, float scale, const v
         voff[j] = (page * hkv + c) * (int64_t)d * OR_PAGE + slot;
       }
       const int64_t orow = tok ? n : t * hq + h;
-      attend_row(dtype, d, sigma, q, (t * hq + h) * d, k_pool, koff, 1, v_pool, voff, OR_PAGE,
-                 nkeys, sc, out + orow * d, lse ? lse + orow : NULL);
+      attend_row_kv(qdt, kvdt, k_scale ? (double)k_scale[c] : 1.0,
+                    v_scale ? (double)v_scale[c] : 1.0, d, sigma, q, (t * hq + h) * d, k_pool,
+                    koff, 1, v_pool, voff, OR_PAGE, nkeys, sc, out + orow * d,
+                    lse ? lse + orow : NULL);
     }
     free(sc);
     free(koff);
     free(voff);
   }
   return bad ? 2 : 0;
+}
+
+int oracle_prefill_paged(int dtype, int hq, int hkv, int d, float scale, const void *q,
+                         const void *k_pool, const void *v_pool, const int32_t *page_table,
+                         int pt_stride, const int32_t *cu_q, const int32_t *prefix_lens,
+                         int nreq, const int32_t *tok, const int32_t *head, int nrows,
+                         double *out, double *lse) {
+  return prefill_paged_impl(dtype, dtype, NULL, NULL, hq, hkv, d, scale, q, k_pool, v_pool,
+                            page_table, pt_stride, cu_q, prefix_lens, nreq, tok, head, nrows,
+                            out, lse);
+}
+
+/* The same chunk prefill over E4M3 pools (codes, same page layouts) with
+ * per-KV-head scales: key j of head c is value(code) * k_scale[c], value j is
+ * value(code) * v_scale[c], in double (the FP8 cache of the paper's FP8
+ * models, Sec. VI-A, read by Eq. 1).  q (bf16 or fp32 by qdtype) [T][Hq][d];
+ * tok/head/nrows select rows as in oracle_prefill_paged. */
+int oracle_prefill_paged_e4m3(int qdtype, int hq, int hkv, int d, float scale, const void *q,
+                              const uint8_t *k_pool, const uint8_t *v_pool, const float *k_scale,
+                              const float *v_scale, const int32_t *page_table, int pt_stride,
+                              const int32_t *cu_q, const int32_t *prefix_lens, int nreq,
+                              const int32_t *tok, const int32_t *head, int nrows, double *out,
+                              double *lse) {
+  return prefill_paged_impl(qdtype, OR_E4M3, k_scale, v_scale, hq, hkv, d, scale, q, k_pool,
+                            v_pool, page_table, pt_stride, cu_q, prefix_lens, nreq, tok, head,
+                            nrows, out, lse);
 }
 
 /* Paged write: for request r, new tokens at logical positions

@@ -5,7 +5,8 @@ float8_e4m3fn type (a library routine); the encoder against brute force over
 the 253 finite values, the tie-to-even midpoints and saturation; the decode
 over E4M3 pools against the dense brute force over the dequantised values, the
 fp32 decode over the same values where they are exact in fp32, and the exact
-scale identities.
+scale identities, for the decode and for the chunk prefill over E4M3 pools
+(against the dense brute force over the dequantised values as well).
 """
 import numpy as np
 import pytest
@@ -205,3 +206,110 @@ def test_fp8_pages_write_pack_bit_exact():
         blk = buf[off[r]:off[r + 1]].reshape(2, hkv, lens[r], d)
         assert np.array_equal(blk[0], k[cu[r]:cu[r + 1]].transpose(1, 0, 2))
         assert np.array_equal(blk[1], v[cu[r]:cu[r + 1]].transpose(1, 0, 2))
+
+
+# ---- chunk prefill over E4M3 pools -------------------------------------------
+def _quantize_pools(kp, vp, ks, vs):
+    """E4M3 codes of bf16 pools [P][Hkv][16][d] / [P][Hkv][d][16], one scale per
+    KV head (poisoned slots stay NaN codes)."""
+    p, hkv, _, d = kp.shape
+    k8 = oracle.e4m3_quantize(kp.transpose(0, 2, 1, 3).reshape(-1, hkv, d), ks)
+    k8 = k8.reshape(p, 16, hkv, d).transpose(0, 2, 1, 3).copy()
+    v8 = oracle.e4m3_quantize(vp.transpose(0, 3, 1, 2).reshape(-1, hkv, d), vs)
+    v8 = v8.reshape(p, 16, hkv, d).transpose(0, 2, 3, 1).copy()
+    return k8, v8
+
+
+def _paged_fp8_case(seed, prefix, chunk, hq, hkv, d, ks, vs):
+    rng = np.random.default_rng(seed)
+    prefix, chunk = np.asarray(prefix, np.int32), np.asarray(chunk, np.int32)
+    total = prefix + chunk
+    pt, num_pages = I.allocate_pages(rng, np.maximum(total, 1))
+    kp, vp = I.empty_pools(num_pages, hkv, d, "bf16")
+    _, kf, vf = I.prefill_batch(rng, total, hq, hkv, d, "bf16")
+    kp, vp = oracle.kv_write(kf, vf, kp, vp, pt, I.cu_from_lens(total),
+                             np.zeros(len(total), np.int32))
+    k8, v8 = _quantize_pools(kp, vp, ks, vs)
+    q = I.normal(rng, (int(chunk.sum()), hq, d), "bf16")
+    return q, k8, v8, pt, I.cu_from_lens(chunk), prefix
+
+
+def _dequant(k8, v8, ks, vs):
+    return (oracle.e4m3_value(k8) * ks.astype(np.float64)[None, :, None, None],
+            oracle.e4m3_value(v8) * vs.astype(np.float64)[None, :, None, None])
+
+
+PF_PREFIX = [0, 1, 15, 16, 17, 40, 0, 33]
+PF_CHUNK = [3, 1, 16, 2, 20, 9, 0, 1]
+
+
+def test_prefill_paged_e4m3_against_brute_force():
+    ks = np.array([6 / 448, 5 / 448], np.float32)
+    vs = np.array([4 / 448, 7 / 448], np.float32)
+    q, k8, v8, pt, cu, pre = _paged_fp8_case(14, PF_PREFIX, PF_CHUNK, 8, 2, 16, ks, vs)
+    out, lse = oracle.prefill_paged_e4m3(q, k8, v8, ks, vs, pt, cu, pre, 0.25)
+    assert np.isfinite(out).all() and np.isfinite(lse).all()
+    kd, vd = _dequant(k8, v8, ks, vs)
+    ref = brute.prefill_paged(q, kd, vd, pt, cu, pre, 0.25)
+    assert np.max(np.abs(out - ref)) < 1e-12
+    qf = brute.widen(q)
+    for r in range(len(pre)):
+        for i in range(cu[r + 1] - cu[r]):
+            kk, _ = brute.gather_context(kd, vd, pt, r, int(pre[r]) + i + 1)
+            for h in range(8):
+                s = 0.25 * (kk[:, h // 4] @ qf[cu[r] + i, h])
+                assert abs(lse[cu[r] + i, h] - np.logaddexp.reduce(s)) < 1e-11
+
+
+def test_prefill_paged_e4m3_equals_fp32_prefill_of_exact_values():
+    ks = np.array([49 / 4096, 3 / 256], np.float32)
+    vs = np.array([5 / 512, 1 / 64], np.float32)
+    q, k8, v8, pt, cu, pre = _paged_fp8_case(15, PF_PREFIX, PF_CHUNK, 4, 2, 16, ks, vs)
+    kd, vd = _dequant(k8, v8, ks, vs)
+    fin = np.isfinite(kd)
+    assert np.array_equal(kd[fin].astype(np.float32).astype(np.float64), kd[fin])
+    q32 = I.bf16_bits_to_f32(q)
+    a, la = oracle.prefill_paged_e4m3(q32, k8, v8, ks, vs, pt, cu, pre, 0.125)
+    b, lb = oracle.prefill_paged(q32, kd.astype(np.float32), vd.astype(np.float32), pt, cu, pre,
+                                 0.125)
+    assert np.array_equal(a, b) and np.array_equal(la, lb)
+
+
+def test_prefill_paged_e4m3_chunk_of_one_is_decode():
+    ks = np.array([0.01, 0.02], np.float32)
+    vs = np.array([0.03, 0.015], np.float32)
+    prefix = np.array([30, 0, 17, 64], np.int32)
+    q, k8, v8, pt, cu, pre = _paged_fp8_case(16, prefix, [1, 1, 1, 1], 4, 2, 32, ks, vs)
+    out, lse = oracle.prefill_paged_e4m3(q, k8, v8, ks, vs, pt, cu, pre, 0.2)
+    dec, dlse = oracle.decode_e4m3(q, k8, v8, ks, vs, pt, pre + 1, 0.2)
+    assert np.max(np.abs(out - dec)) < 1e-14 and np.max(np.abs(lse - dlse)) < 1e-13
+
+
+def test_prefill_paged_e4m3_scale_identities():
+    ks = np.array([0.01, 0.02], np.float32)
+    vs = np.array([0.03, 0.015], np.float32)
+    q, k8, v8, pt, cu, pre = _paged_fp8_case(17, PF_PREFIX, PF_CHUNK, 4, 2, 32, ks, vs)
+    base, lse = oracle.prefill_paged_e4m3(q, k8, v8, ks, vs, pt, cu, pre, 0.125)
+    o2, l2 = oracle.prefill_paged_e4m3(q, k8, v8, ks, vs * 2, pt, cu, pre, 0.125)
+    assert np.array_equal(o2, 2 * base) and np.array_equal(l2, lse)
+    o3, l3 = oracle.prefill_paged_e4m3(q, k8, v8, ks * 2, vs, pt, cu, pre, 0.125)
+    o4, l4 = oracle.prefill_paged_e4m3(q, k8, v8, ks, vs, pt, cu, pre, 0.25)
+    assert np.max(np.abs(o3 - o4)) < 1e-13 and np.max(np.abs(l3 - l4)) < 1e-12
+    # The first row of a chunk with no prefix sees only its own key: its output
+    # is that token's dequantised V.
+    for r in np.flatnonzero((pre == 0) & (np.diff(cu) > 0)):
+        p = pt[r, 0]
+        for h in range(4):
+            assert np.array_equal(base[cu[r], h],
+                                  oracle.e4m3_value(v8[p, h // 2, :, 0]) * vs[h // 2])
+
+
+def test_prefill_paged_e4m3_selected_rows_equal_full():
+    ks = np.array([0.01, 0.02], np.float32)
+    vs = np.array([0.03, 0.015], np.float32)
+    q, k8, v8, pt, cu, pre = _paged_fp8_case(18, PF_PREFIX, PF_CHUNK, 4, 2, 16, ks, vs)
+    full, flse = oracle.prefill_paged_e4m3(q, k8, v8, ks, vs, pt, cu, pre, 0.3)
+    tok = np.array([0, 5, int(cu[-1]) - 1, 20, 3], np.int32)
+    head = np.array([3, 0, 1, 2, 3], np.int32)
+    out, lse = oracle.prefill_paged_e4m3(q, k8, v8, ks, vs, pt, cu, pre, 0.3, tok, head)
+    assert np.array_equal(out, full[tok, head]) and np.array_equal(lse, flse[tok, head])

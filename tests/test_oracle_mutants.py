@@ -43,10 +43,14 @@ MUTANTS = {
                                 "const int nkeys = (int)(t - cu_q[r]) + 1;")],
     "paged_prefill_prefix_off_by_one": [("const int nkeys = prefix_lens[r] + (int)(t - cu_q[r]) + 1;",
                                          "const int nkeys = (prefix_lens[r] > 0 ? prefix_lens[r] - 1 : 0) + (int)(t - cu_q[r]) + 1;")],
-    "paged_prefill_chunk_row_as_q_row": [("attend_row(dtype, d, sigma, q, (t * hq + h) * d, k_pool",
-                                          "attend_row(dtype, d, sigma, q, ((t - cu_q[r]) * hq + h) * d, k_pool")],
-    "paged_prefill_v_token_major": [("k_pool, koff, 1, v_pool, voff, OR_PAGE,\n                 nkeys",
-                                     "k_pool, koff, 1, v_pool, koff, 1,\n                 nkeys")],
+    "paged_prefill_chunk_row_as_q_row": [("d, sigma, q, (t * hq + h) * d, k_pool",
+                                          "d, sigma, q, ((t - cu_q[r]) * hq + h) * d, k_pool")],
+    "paged_prefill_v_token_major": [("koff, 1, v_pool, voff, OR_PAGE, nkeys",
+                                     "koff, 1, v_pool, koff, 1, nkeys")],
+    "paged_e4m3_scales_swapped": [("prefill_paged_impl(qdtype, OR_E4M3, k_scale, v_scale,",
+                                   "prefill_paged_impl(qdtype, OR_E4M3, v_scale, k_scale,")],
+    "paged_e4m3_v_scale_dropped": [("v_scale ? (double)v_scale[c] : 1.0, d, sigma, q, (t * hq",
+                                    "1.0, d, sigma, q, (t * hq")],
     "e4m3_exponent_bias_8": [("ldexp((double)(8 + m), e - 10)", "ldexp((double)(8 + m), e - 11)")],
     "e4m3_encode_ties_away": [("int m = (int)nearbyint(ldexp(a, 3 - E));", "int m = (int)round(ldexp(a, 3 - E));")],
     "e4m3_overflow_to_nan": [("if (a >= 448.0) return s | 0x7E;", "if (a >= 464.0) return s | 0x7F;")],
@@ -78,7 +82,8 @@ def _load(path):
     real = oracle._lib()
     for f in ("oracle_prefill", "oracle_prefill_rows", "oracle_decode", "oracle_kv_write",
               "oracle_pack", "oracle_unpack", "oracle_prefill_paged", "oracle_e4m3_value",
-              "oracle_e4m3_encode", "oracle_e4m3_quantize", "oracle_decode_e4m3"):
+              "oracle_e4m3_encode", "oracle_e4m3_quantize", "oracle_decode_e4m3",
+              "oracle_prefill_paged_e4m3"):
         getattr(lib, f).argtypes = getattr(real, f).argtypes
         getattr(lib, f).restype = getattr(real, f).restype
     return lib
@@ -275,10 +280,30 @@ def chk_decode_e4m3_brute():
     return _close(out, ref, 1e-12)
 
 
+def chk_paged_prefill_e4m3_brute():
+    rng = np.random.default_rng(34)
+    prefix, chunk = [18, 0, 3], [4, 9, 14]
+    total = np.asarray(prefix) + np.asarray(chunk)
+    pt, num_pages = I.allocate_pages(rng, total, pool_pages=int(np.sum((total + 15) // 16)) + 1)
+    kp = rng.integers(0, 0x7F, (num_pages, 2, 16, 8)).astype(np.uint8) | (
+        rng.integers(0, 2, (num_pages, 2, 16, 8)).astype(np.uint8) << 7)
+    vp = rng.integers(0, 0x7F, (num_pages, 2, 8, 16)).astype(np.uint8)
+    q = I.normal(rng, (int(np.sum(chunk)), 4, 8), "bf16")
+    cu, pre = I.cu_from_lens(chunk), np.asarray(prefix, np.int32)
+    ks = np.array([0.02, 0.06], np.float32)
+    vs = np.array([0.03, 0.004], np.float32)
+    out, _ = oracle.prefill_paged_e4m3(q, kp, vp, ks, vs, pt, cu, pre, 0.3)
+    tab = torch.arange(256, dtype=torch.uint8).view(torch.float8_e4m3fn).to(torch.float64).numpy()
+    kd = tab[kp] * ks.astype(np.float64)[None, :, None, None]
+    vd = tab[vp] * vs.astype(np.float64)[None, :, None, None]
+    return _close(out, brute.prefill_paged(q, kd, vd, pt, cu, pre, 0.3), 1e-12)
+
+
 CHECKS = [chk_e4m3_table, chk_e4m3_encode, chk_e4m3_quantize, chk_decode_e4m3_brute,
           chk_prefill_brute, chk_prefill_sdpa, chk_lse, chk_decode_brute,
           chk_last_row_equals_decode, chk_write_pack_transpose, chk_closed_forms,
-          chk_unpack_matches_write, chk_paged_prefill_brute, chk_chunked_equals_one_shot]
+          chk_unpack_matches_write, chk_paged_prefill_brute, chk_chunked_equals_one_shot,
+          chk_paged_prefill_e4m3_brute]
 
 
 def _run_checks():
