@@ -45,6 +45,7 @@ PROFILES = os.path.join(ROOT, "profiles")
 KERNEL_SOURCES = ("paper_2511_20982_amd/csrc/dopd_attn.hip",
                   "paper_2511_20982_amd/csrc/plan.hpp",
                   "paper_2511_20982_amd/csrc/kernels/kv_write_pack.hpp",
+                  "paper_2511_20982_amd/csrc/kernels/kv_dequant.hpp",
                   "paper_2511_20982_amd/csrc/kernels/pd_step.hpp",
                   "paper_2511_20982_amd/csrc/kernels/common.hpp",
                   "paper_2511_20982_amd/csrc/kernels/attn_f32.hpp",
@@ -60,7 +61,10 @@ CALL_KERNELS = {"decode": ("decode_split_kernel", "decode_merge_kernel"),
                 "prefill": ("prefill_bf16_kernel<128, false>", "prefill_bf16_kernel<64, false>"),
                 "prefill_chunked": ("prefill_bf16_kernel<128, true>", "prefill_bf16_kernel<64, true>",
                                     "prefill_split_merge_kernel"),
-                "kv_write": ("kv_write_kernel",),
+                "prefill_chunked_fp8": ("kv_dequant_pages_kernel", "prefill_bf16_kernel<128, true>",
+                                        "prefill_bf16_kernel<64, true>",
+                                        "prefill_split_merge_kernel"),
+                "kv_write": ("kv_write_kernel",), "kv_write_fp8": ("kv_write_e4m3_kernel",),
                 "pack": ("kv_pack_kernel",), "unpack": ("kv_unpack_kernel",),
                 "pd_step": ("pd_step_kernel", "decode_merge_kernel"),
                 "kv_write_pack": ("kv_write_pack_kernel",)}
@@ -77,7 +81,8 @@ WORKLOADS = {
     "chunked": ("chunked prefill over the paged cache: the 16 prompts of the varlen prefill "
                 "workload (lognormal(1500,1.0) [32,8192], 32/32 heads, d128, bf16) in chunks of "
                 "--chunk tokens, calls filled to --budget tokens, each chunk attending to its "
-                "cached prefix", 3),
+                "cached prefix; --kv fp8: the prompts written to an E4M3 cache and the chunks "
+                "read from it", 3),
     "pd_step": ("the mixed P/D step + handoff of the mixed workload as one PD-aggregated launch "
                 "(dopd_pd_step: decode slices, prefill items and write+pack workgroups in one "
                 "grid, then the decode merge)", 5),
@@ -127,6 +132,14 @@ def pack_bytes(lens, layers, hkv, d, s=2):
 
 
 # ------------------------------------------------------------------ helpers
+def e4m3_head_scales(x) -> np.ndarray:
+    """One E4M3 scale per KV head of bf16 x[T][Hkv][d]: its absolute maximum
+    over the tokens and dims / 448 (the largest finite E4M3 value), in fp32."""
+    a = np.abs((np.asarray(x, np.uint16).astype(np.uint32) << np.uint32(16)).view(np.float32))
+    a = a.max(axis=(0, 2))
+    return (a / np.float32(448)).astype(np.float32)
+
+
 def source_hash() -> str:
     import hashlib
     h = hashlib.sha256()
@@ -693,31 +706,59 @@ def build_workload(name, args, torch, A, I, sA):
                                                device=dev),
                                cu=A.to_device(cu_c), cu_h=cu_c, pre=A.to_device(pre), pre_h=pre,
                                pt=A.to_device(pt_c), n=len(sel)))
-        ws_bytes = max(A.dopd_prefill_paged_workspace_size(shape, ch["cu_h"], ch["pre_h"], ch["n"],
-                                                           args.splits) for ch in chunks)
+        fp8 = args.kv == "fp8"
+        wsize = (A.dopd_prefill_paged_fp8_workspace_size if fp8 else
+                 A.dopd_prefill_paged_workspace_size)
+        shape_c = A.make_shape(w.hq, w.hkv, w.d, "fp8", w.scale) if fp8 else shape
+        ws_bytes = max(wsize(shape_c, ch["cu_h"], ch["pre_h"], ch["n"], args.splits)
+                       for ch in chunks)
         ws_buf = torch.empty(ws_bytes + 256, dtype=torch.uint8, device=dev)
         ws = ws_buf[(-ws_buf.data_ptr()) % 256:][:ws_bytes]
-
-        def write():
-            A.dopd_kv_write(shape, k, v, kp, vp, w.num_pages, pt, stride, cu, start, n_pre, T, sA)
-
-        def chunked():
-            for ch in chunks:
-                A.dopd_prefill_paged_attn_split(shape, ch["q"], kp, vp, w.num_pages, ch["pt"],
-                                                stride, ch["cu"], ch["cu_h"], ch["pre"],
-                                                ch["pre_h"], ch["n"], args.splits, ch["out"],
-                                                None, ws, ws_bytes, sA)
 
         def result():
             for ch in chunks:
                 out_p.index_copy_(0, ch["rows"], ch["out"])
             return out_p
 
-        calls = [("kv_write", write), ("prefill_chunked", chunked)]
-        work = {"prefill_chunked": ("TFLOP/s", prefill_flops(w.prefill_lens, w.hq, w.d)),
-                "kv_write": ("GB/s", write_bytes(w.prefill_lens, w.hkv, w.d))}
-        dominant = "prefill_chunked"
-        extra = {"chunk": C, "budget": B, "calls_per_pass": len(chunks)}
+        if fp8:
+            ks_h, vs_h = e4m3_head_scales(w.k), e4m3_head_scales(w.v)
+            ks, vs = A.to_device(ks_h), A.to_device(vs_h)
+            kp = torch.full((w.num_pages, w.hkv, 16, w.d), 0x7F, dtype=torch.uint8, device=dev)
+            vp = torch.full((w.num_pages, w.hkv, w.d, 16), 0x7F, dtype=torch.uint8, device=dev)
+
+            def write():
+                A.dopd_kv_write_fp8(shape_c, k, v, ks, vs, kp, vp, w.num_pages, pt, stride, cu,
+                                    start, n_pre, T, sA)
+
+            def chunked():
+                for ch in chunks:
+                    A.dopd_prefill_paged_attn_fp8(shape_c, ch["q"], kp, vp, ks, vs, w.num_pages,
+                                                  ch["pt"], stride, ch["cu"], ch["cu_h"],
+                                                  ch["pre"], ch["pre_h"], ch["n"], args.splits,
+                                                  ch["out"], None, ws, ws_bytes, sA)
+
+            calls = [("kv_write_fp8", write), ("prefill_chunked_fp8", chunked)]
+            work = {"prefill_chunked_fp8": ("TFLOP/s",
+                                            prefill_flops(w.prefill_lens, w.hq, w.d)),
+                    "kv_write_fp8": ("GB/s", write_bytes(w.prefill_lens, w.hkv, w.d, out_s=1))}
+            dominant = "prefill_chunked_fp8"
+        else:
+            def write():
+                A.dopd_kv_write(shape, k, v, kp, vp, w.num_pages, pt, stride, cu, start, n_pre, T,
+                                sA)
+
+            def chunked():
+                for ch in chunks:
+                    A.dopd_prefill_paged_attn_split(shape, ch["q"], kp, vp, w.num_pages,
+                                                    ch["pt"], stride, ch["cu"], ch["cu_h"],
+                                                    ch["pre"], ch["pre_h"], ch["n"], args.splits,
+                                                    ch["out"], None, ws, ws_bytes, sA)
+
+            calls = [("kv_write", write), ("prefill_chunked", chunked)]
+            work = {"prefill_chunked": ("TFLOP/s", prefill_flops(w.prefill_lens, w.hq, w.d)),
+                    "kv_write": ("GB/s", write_bytes(w.prefill_lens, w.hkv, w.d))}
+            dominant = "prefill_chunked"
+        extra = {"chunk": C, "budget": B, "calls_per_pass": len(chunks), "kv": args.kv}
     else:
         if args.kv == "fp8":
             # the prompts' K/V go to an E4M3 cache (scales from each head's
@@ -756,13 +797,31 @@ def build_workload(name, args, torch, A, I, sA):
         import oracle
         rows_tok = np.repeat(np.concatenate([w.cu_seqlens[1:] - 1 - i for i in range(4)]), 4)
         heads = (np.arange(len(rows_tok)) * 7) % w.hq
-        (ref, _), n, dt = repeat_timed(
-            lambda: oracle.prefill_rows(w.q, w.k, w.v, w.cu_seqlens, w.scale, rows_tok, heads),
-            args.cpu_seconds)
+        if name == "chunked" and args.kv == "fp8":
+            # the oracle quantises the prompts with the same scales into pools
+            # of its own and reads them as one chunk per prompt
+            ks_h, vs_h = e4m3_head_scales(w.k), e4m3_head_scales(w.v)
+            k8 = np.full((w.num_pages, w.hkv, 16, w.d), 0x7F, np.uint8)
+            v8 = np.full((w.num_pages, w.hkv, w.d, 16), 0x7F, np.uint8)
+            zeros = np.zeros(n_pre, np.int32)
+            k8, v8 = oracle.kv_write(oracle.e4m3_quantize(w.k, ks_h),
+                                     oracle.e4m3_quantize(w.v, vs_h), k8, v8,
+                                     w.page_table[w.prefill_rows], w.cu_seqlens, zeros)
+
+            def run():
+                return oracle.prefill_paged_e4m3(w.q, k8, v8, ks_h, vs_h,
+                                                 w.page_table[w.prefill_rows], w.cu_seqlens,
+                                                 zeros, w.scale, rows_tok, heads)
+            what = "fp64 oracle chunk prefill over E4M3 pages"
+        else:
+            def run():
+                return oracle.prefill_rows(w.q, w.k, w.v, w.cu_seqlens, w.scale, rows_tok, heads)
+            what = "fp64 oracle prefill"
+        (ref, _), n, dt = repeat_timed(run, args.cpu_seconds)
         req_of = np.searchsorted(w.cu_seqlens, rows_tok, side="right") - 1
         flops = int((4 * w.d * (rows_tok - w.cu_seqlens[req_of] + 1)).sum())
         base = cpu_entry(round(n * flops / dt / 1e12, 6), "TFLOP/s", flops, n, dt,
-                         f"fp64 oracle prefill of {len(rows_tok)} sampled rows (the last 4 rows "
+                         f"{what} of {len(rows_tok)} sampled rows (the last 4 rows "
                          f"of every prompt, 4 heads each; {flops / 1e9:.2f} GFLOP), {n} passes")
         got = widen(result())[rows_tok, heads]
         return base, {dominant: err_block(got, ref)}

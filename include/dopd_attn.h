@@ -31,9 +31,9 @@
  *   out and fresh K/V stay bf16.  The paper's models store FP8 (Sec. VI-A);
  *   it gives no scaling rule, so the per-head scale is this library's.  It
  *   halves the bytes decode and handoff move.  Entry points that take it:
- *   dopd_kv_write_fp8, dopd_decode_attn_fp8, dopd_decode_workspace_size and
- *   the handoff pack/unpack (byte copies); the others return
- *   DOPD_ERR_UNSUPPORTED for it.
+ *   dopd_kv_write_fp8, dopd_decode_attn_fp8, dopd_decode_workspace_size,
+ *   dopd_prefill_paged_attn_fp8 with its workspace size, and the handoff
+ *   pack/unpack (byte copies); the others return DOPD_ERR_UNSUPPORTED for it.
  * - Fresh tokens are token-major: Q/out [T][Hq][d], K/V [T][Hkv][d].
  * - GQA: query head h uses KV head h / (Hq / Hkv); Hq % Hkv must be 0.
  * - Paged cache (one pool per layer, page_size = 16 tokens):
@@ -192,6 +192,47 @@ size_t dopd_prefill_paged_workspace_size(const dopd_attn_shape* shape,
                                          const int32_t* cu_seqlens_host,
                                          const int32_t* prefix_lens_host, int32_t num_reqs,
                                          int32_t num_splits);
+
+/*
+ * Chunk prefill over E4M3 pools.
+ * Paper: the prefill of dopd_prefill_paged_attn (Eq. 1 over a cached prefix,
+ * Sec. III-A, Sec. V-E) over FP8 blocks, the models' precision (Sec. VI-A).
+ * shape->dtype = DOPD_FP8_E4M3: dopd_prefill_paged_attn's operation with
+ * K_j = code * k_scale[c] and V_j = code * v_scale[c] for KV head c (pool
+ * layouts as there, one byte per element; k_scale/v_scale fp32 device arrays
+ * [Hkv], positive and finite, not checked on the device); q and out bf16,
+ * lse as there.  A first kernel widens the pages the call reads to bf16
+ * (exactly: every E4M3 value is a bf16 value) into the workspace, packed
+ * per request with their own page table; the bf16 prefill then runs over
+ * them with the K scale folded into the softmax scale and the V scale into
+ * the output, in fp32.  num_splits as in dopd_prefill_paged_attn_split.
+ *   workspace: device memory of at least
+ *     dopd_prefill_paged_fp8_workspace_size() bytes for the same arguments,
+ *     256-byte aligned, any contents (2 * pages * Hkv * 16 * d * 2 bytes of
+ *     widened pages, where pages = sum over non-empty chunks of
+ *     ceil((prefix_r + n_r) / 16), then the page table and the split
+ *     partials).  Null only when every chunk is empty.  Calls that overlap
+ *     in time must not share it.
+ */
+dopd_status dopd_prefill_paged_attn_fp8(const dopd_attn_shape* shape, const void* q,
+                                        const void* k_pool, const void* v_pool,
+                                        const float* k_scale, const float* v_scale,
+                                        int32_t num_pages, const int32_t* page_table,
+                                        int32_t page_table_stride, const int32_t* cu_seqlens,
+                                        const int32_t* cu_seqlens_host,
+                                        const int32_t* prefix_lens,
+                                        const int32_t* prefix_lens_host, int32_t num_reqs,
+                                        int32_t num_splits, void* out, float* lse,
+                                        void* workspace, size_t workspace_bytes, void* stream);
+
+/* Workspace bytes dopd_prefill_paged_attn_fp8 needs for these arguments on
+ * the current device (at least 256; 0 on bad input or a dtype other than
+ * DOPD_FP8_E4M3).
+ * Paper: as dopd_prefill_paged_attn_fp8 (Eq. 1, Sec. III-A, Sec. VI-A). */
+size_t dopd_prefill_paged_fp8_workspace_size(const dopd_attn_shape* shape,
+                                             const int32_t* cu_seqlens_host,
+                                             const int32_t* prefix_lens_host, int32_t num_reqs,
+                                             int32_t num_splits);
 
 /*
  * Paged KV write.

@@ -27,7 +27,8 @@ PAGE_SIZE = 16
 
 EXPORTS = (
     "dopd_prefill_attn", "dopd_prefill_workspace_size", "dopd_prefill_paged_attn", "dopd_prefill_paged_attn_split",
-    "dopd_prefill_paged_workspace_size", "dopd_kv_write", "dopd_kv_write_fp8",
+    "dopd_prefill_paged_workspace_size", "dopd_prefill_paged_attn_fp8",
+    "dopd_prefill_paged_fp8_workspace_size", "dopd_kv_write", "dopd_kv_write_fp8",
     "dopd_decode_attn", "dopd_decode_attn_fp8", "dopd_decode_workspace_size",
     "dopd_decode_attn_noalloc",
     "dopd_kv_pack_for_handoff", "dopd_kv_unpack_from_handoff", "dopd_validate_page_table_host",
@@ -84,6 +85,10 @@ def lib():
                                                     i32, P, P, P, sz, P]
         L.dopd_prefill_paged_workspace_size.argtypes = [SP, P, P, i32, i32]
         L.dopd_prefill_paged_workspace_size.restype = sz
+        L.dopd_prefill_paged_attn_fp8.argtypes = [SP, P, P, P, P, P, i32, P, i32, P, P, P, P, i32,
+                                                  i32, P, P, P, sz, P]
+        L.dopd_prefill_paged_fp8_workspace_size.argtypes = [SP, P, P, i32, i32]
+        L.dopd_prefill_paged_fp8_workspace_size.restype = sz
         L.dopd_kv_write.argtypes = [SP, P, P, P, P, i32, P, i32, P, P, i32, i32, P]
         L.dopd_decode_attn.argtypes = [SP, P, P, P, i32, P, i32, P, P, i32, i32, P, P, P, sz, P]
         L.dopd_kv_write_fp8.argtypes = [SP, P, P, P, P, P, P, i32, P, i32, P, P, i32, i32, P]
@@ -105,7 +110,7 @@ def lib():
         L.dopd_status_string.restype = C.c_char_p
         L.dopd_last_hip_error.restype = i32
         for f in ("dopd_prefill_attn", "dopd_prefill_paged_attn",
-                  "dopd_prefill_paged_attn_split", "dopd_kv_write",
+                  "dopd_prefill_paged_attn_split", "dopd_prefill_paged_attn_fp8", "dopd_kv_write",
                   "dopd_kv_write_fp8", "dopd_decode_attn", "dopd_decode_attn_fp8",
                   "dopd_decode_attn_noalloc",
                   "dopd_kv_pack_for_handoff", "dopd_kv_unpack_from_handoff",
@@ -197,6 +202,30 @@ def dopd_prefill_paged_attn_split(shape, q, k_pool, v_pool, num_pages, page_tabl
         _dptr(page_table), int(page_table_stride), _dptr(cu_seqlens), _hptr(cu_h),
         _dptr(prefix_lens), _hptr(pre_h), int(num_reqs), int(num_splits), _dptr(out), _dptr(lse),
         _dptr(workspace), int(workspace_bytes), _stream(stream)), "dopd_prefill_paged_attn_split")
+
+
+def dopd_prefill_paged_fp8_workspace_size(shape, cu_seqlens_host, prefix_lens_host, num_reqs,
+                                          num_splits=0) -> int:
+    cu_h = _host_i32(cu_seqlens_host)
+    pre_h = _host_i32(prefix_lens_host)
+    return int(lib().dopd_prefill_paged_fp8_workspace_size(
+        C.byref(shape), _hptr(cu_h), _hptr(pre_h), int(num_reqs), int(num_splits)))
+
+
+def dopd_prefill_paged_attn_fp8(shape, q, k_pool, v_pool, k_scale, v_scale, num_pages,
+                                page_table, page_table_stride, cu_seqlens, cu_seqlens_host,
+                                prefix_lens, prefix_lens_host, num_reqs, num_splits, out, lse,
+                                workspace, workspace_bytes=None, stream=None):
+    cu_h = _host_i32(cu_seqlens_host)
+    pre_h = _host_i32(prefix_lens_host)
+    if workspace_bytes is None:
+        workspace_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check(lib().dopd_prefill_paged_attn_fp8(
+        C.byref(shape), _dptr(q), _dptr(k_pool), _dptr(v_pool), _dptr(k_scale), _dptr(v_scale),
+        int(num_pages), _dptr(page_table), int(page_table_stride), _dptr(cu_seqlens),
+        _hptr(cu_h), _dptr(prefix_lens), _hptr(pre_h), int(num_reqs), int(num_splits),
+        _dptr(out), _dptr(lse), _dptr(workspace), int(workspace_bytes), _stream(stream)),
+        "dopd_prefill_paged_attn_fp8")
 
 
 def dopd_kv_write(shape, k_new, v_new, k_pool, v_pool, num_pages, page_table,
@@ -366,6 +395,19 @@ def prefill_paged_workspace(shape, cu_seqlens_host, prefix_lens_host, num_reqs, 
                                           num_splits)
     if n == 0:
         raise DopdError(DOPD_ERR_INVALID_SHAPE, "dopd_prefill_paged_workspace_size")
+    ws = torch.empty(n + 256, dtype=torch.uint8, device=device)
+    off = (-ws.data_ptr()) % 256
+    return ws[off:off + n]
+
+
+def prefill_paged_fp8_workspace(shape, cu_seqlens_host, prefix_lens_host, num_reqs,
+                                num_splits=0, device="cuda"):
+    """A 256-byte aligned workspace for dopd_prefill_paged_attn_fp8."""
+    import torch
+    n = dopd_prefill_paged_fp8_workspace_size(shape, cu_seqlens_host, prefix_lens_host, num_reqs,
+                                              num_splits)
+    if n == 0:
+        raise DopdError(DOPD_ERR_INVALID_SHAPE, "dopd_prefill_paged_fp8_workspace_size")
     ws = torch.empty(n + 256, dtype=torch.uint8, device=device)
     off = (-ws.data_ptr()) % 256
     return ws[off:off + n]

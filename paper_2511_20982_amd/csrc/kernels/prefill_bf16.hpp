@@ -65,6 +65,12 @@ struct PrefillArgs {
   const int32_t* page_table;  // [nreq][pt_stride]
   const int32_t* prefix;      // [nreq]
   int pt_stride;
+  // Per-KV-head scales of the cached K and V (null: 1): key = cached value *
+  // k_scale[c], value = cached value * v_scale[c] (pages dequantised from E4M3
+  // codes, which bf16 holds exactly).  The K scale multiplies the softmax
+  // scale, the V scale the output.
+  const float* k_scale;
+  const float* v_scale;
   // Key splits of the paged kernel (nsplit > 1): workgroup b computes split
   // b % nsplit of item b / nsplit, keys of tiles [t_s, t_{s+1}) with
   // t_s = min(s * ntiles / nsplit, nfull) (the last split also takes every
@@ -348,7 +354,8 @@ __device__ __forceinline__ void prefill_workgroup(const PrefillArgs& a, int bid,
     // running max m kept in the scaled domain.  For c <= 0 the scores are
     // scaled first and c is taken as 1, so the max is always taken on the
     // exponent.
-    const float c_in = a.scale_log2;
+    const float c_in = PAGED && a.k_scale ? a.scale_log2 * a.k_scale[kvh] : a.scale_log2;
+    const float v_sc = PAGED && a.v_scale ? a.v_scale[kvh] : 1.f;
     const bool pos_scale = c_in > 0.f;
     const float c_eff = pos_scale ? c_in : 1.f;
     // Lazy rescaling on masked tiles: the running max only moves when a tile
@@ -647,13 +654,13 @@ __device__ __forceinline__ void prefill_workgroup(const PrefillArgs& a, int bid,
             for (int gq = 0; gq < 4; ++gq)
               *reinterpret_cast<f32x4*>(po + 32 * et + 8 * gq) =
                   f32x4{oacc[et][4 * gq], oacc[et][4 * gq + 1], oacc[et][4 * gq + 2],
-                        oacc[et][4 * gq + 3]};
+                        oacc[et][4 * gq + 3]} * v_sc;
           if (hi == 0) *reinterpret_cast<float2*>(a.part_ml + row * 2) = float2{m_run, l_tot};
         }
         return;
       }
     }
-    const float inv = 1.f / l_tot;
+    const float inv = v_sc / l_tot;
     // The wave's 32 x D output block goes through LDS (no load is in flight
     // and every wave is past its last tile read: the loop's last barrier), so
     // that 16 lanes store one 256-byte row instead of 32 rows taking 8-byte

@@ -189,6 +189,34 @@ def gpu_decode_fp8(shape, q, k_pool, v_pool, k_scale, v_scale, page_table, ctx, 
     return widen(A.to_host(out)), (lse.cpu().numpy().astype(np.float64) if with_lse else None)
 
 
+def gpu_prefill_paged_fp8(shape, q, k_pool, v_pool, k_scale, v_scale, page_table, cu, prefix,
+                          splits=0, pools_dev=None):
+    """dopd_prefill_paged_attn_fp8 with a 0xFF-filled workspace whose guard
+    bytes are checked afterwards."""
+    if pools_dev is None:
+        pools_dev = (A.to_device(k_pool), A.to_device(v_pool))
+    kp, vp = pools_dev
+    qd = A.to_device(q)
+    out, obuf, margin = guarded(qd.shape, qd.dtype)
+    lse = torch.full((q.shape[0], q.shape[1]), float("nan"), device=DEV)
+    prefix = np.asarray(prefix, np.int32)
+    n = A.dopd_prefill_paged_fp8_workspace_size(shape, cu, prefix, len(cu) - 1, splits)
+    assert n >= 256 and n % 256 == 0
+    wbuf = torch.full((n + 4096 + 256,), 0xFF, dtype=torch.uint8, device=DEV)
+    off = (-wbuf.data_ptr()) % 256
+    ws = wbuf[off:off + n]
+    A.dopd_prefill_paged_attn_fp8(shape, qd, kp, vp, A.to_device(np.asarray(k_scale, np.float32)),
+                                  A.to_device(np.asarray(v_scale, np.float32)), kp.shape[0],
+                                  A.to_device(page_table), page_table.shape[1], A.to_device(cu),
+                                  cu, A.to_device(prefix), prefix, len(cu) - 1, splits, out, lse,
+                                  ws, n)
+    torch.cuda.synchronize()
+    assert bool((wbuf[off + n:] == 0xFF).all()), "fp8 paged prefill wrote past its workspace"
+    assert canary_intact(obuf, margin, out.numel() * out.element_size()), \
+        "fp8 paged prefill wrote out of bounds"
+    return widen(A.to_host(out)), lse.cpu().numpy().astype(np.float64)
+
+
 def gpu_unpack(shape, buf, offs, req, lens, k_pool, v_pool, layers, pt):
     kp, vp = A.to_device(k_pool), A.to_device(v_pool)
     num_pages = k_pool.shape[-4]

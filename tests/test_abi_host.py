@@ -286,6 +286,46 @@ def test_prefill_paged_split_host_validation(lib):
     assert call(4, FAKE, need, stride=39) == A.DOPD_ERR_INVALID_SHAPE  # table too narrow
 
 
+def test_prefill_paged_fp8_workspace_size(lib):
+    s8 = _shape(dtype="fp8")  # 8 query heads, 2 KV heads, d = 128
+    cu = np.array([0, 40, 41, 41], np.int32)
+    pre = np.array([600, 0, 900], np.int32)
+    ws = A.dopd_prefill_paged_fp8_workspace_size
+    # pages read: ceil(640 / 16) + ceil(1 / 16) (the empty third chunk reads
+    # none) = 41, widened to bf16 for K and V; then the [3][40] page table.
+    pages = 2 * 41 * 2 * 16 * 128 * 2 + _align256(3 * 40 * 4)
+    for n in (1, 0, 3):
+        split = A.dopd_prefill_paged_workspace_size(_shape(), cu, pre, 3, n)
+        assert ws(s8, cu, pre, 3, n) == pages + (0 if split == 256 else split)
+    assert ws(_shape(), cu, pre, 3, 0) == 0                     # bf16 pools: not this entry
+    assert ws(s8, cu, pre, 0, 0) == 256
+    assert ws(s8, np.zeros(4, np.int32), pre, 3, 0) == 256      # every chunk empty
+    assert ws(s8, cu, pre, 3, -1) == 0
+    assert ws(s8, np.array([1, 40, 41, 41], np.int32), pre, 3, 0) == 0
+    assert ws(s8, cu, np.array([0, -1, 0], np.int32), 3, 0) == 0
+
+
+def test_prefill_paged_fp8_host_validation(lib):
+    s8 = _shape(dtype="fp8")
+    p = C.c_void_p(FAKE)
+    cu = np.array([0, 40, 41], np.int32)
+    pre = np.array([600, 0], np.int32)
+    H = A._hptr
+    need = A.dopd_prefill_paged_fp8_workspace_size(s8, cu, pre, 2, 4)
+
+    def call(splits, ws, nbytes, stride=64, shape=s8, scales=p):
+        return lib.dopd_prefill_paged_attn_fp8(
+            C.byref(shape), p, p, p, scales, scales, 100, p, stride, p, H(cu), p, H(pre), 2,
+            splits, p, None, None if ws is None else C.c_void_p(ws), nbytes, None)
+    assert call(4, FAKE, need, shape=_shape()) == A.DOPD_ERR_UNSUPPORTED
+    assert call(4, FAKE, need, scales=None) == A.DOPD_ERR_NULL_POINTER
+    assert call(4, None, need) == A.DOPD_ERR_NULL_POINTER
+    assert call(4, FAKE, need - 1) == A.DOPD_ERR_WORKSPACE_TOO_SMALL
+    assert call(4, FAKE + 64, need) == A.DOPD_ERR_INVALID_SHAPE   # not 256-byte aligned
+    assert call(-1, FAKE, need) == A.DOPD_ERR_INVALID_SHAPE
+    assert call(4, FAKE, need, stride=39) == A.DOPD_ERR_INVALID_SHAPE  # table too narrow
+
+
 def _write_pack(lib, shape, cu, stride=64, out=FAKE, offs=FAKE, nreq=None):
     cu = np.asarray(cu, np.int32)
     p = C.c_void_p(FAKE)
