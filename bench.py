@@ -826,7 +826,8 @@ def build_workload(name, args, torch, A, I, sA):
         got = widen(result())[rows_tok, heads]
         return base, {dominant: err_block(got, ref)}
 
-    return Workload(name, desc, w.seed, calls, work, dominant, cpu, extra=extra)
+    return Workload(name, desc, w.seed, calls, work, dominant, cpu,
+                    label=name + ("_fp8" if args.kv == "fp8" else ""), extra=extra)
 
 
 def run_workload(wl, args, torch, sA, flush, steps, warmup, reps):
@@ -908,7 +909,8 @@ def main():
     ap.add_argument("--kv", choices=("bf16", "fp8"), default="bf16",
                     help="KV cache element type (fp8 = E4M3 pages with per-KV-head scales): "
                          "decode workloads read it (written by the fp8 writer before timing), "
-                         "the prefill workload writes it")
+                         "the prefill workload writes it, the chunked workload writes it "
+                         "and its chunk calls read it")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calib-mib", type=int, default=0,
                     help="after timing, run one elementwise kernel over this many MiB "
@@ -928,8 +930,9 @@ def main():
         summarize(args)
         return
 
-    if args.kv == "fp8" and args.workload not in ("decode_mha", "decode_gqa", "prefill"):
-        print("--kv fp8 applies to the decode_mha, decode_gqa and prefill workloads",
+    if args.kv == "fp8" and args.workload not in ("decode_mha", "decode_gqa", "prefill",
+                                                  "chunked"):
+        print("--kv fp8 applies to the decode_mha, decode_gqa, prefill and chunked workloads",
               file=sys.stderr)
         sys.exit(2)
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:

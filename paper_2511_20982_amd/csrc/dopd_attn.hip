@@ -990,22 +990,42 @@ dopd_status dopd_kv_pack_for_handoff(const dopd_attn_shape* s, int32_t num_layer
   }
   if (max_len == 0) return DOPD_OK;
   const int64_t zdim = (int64_t)num_layers * 2 * s->num_kv_heads;
-  if (zdim > 65535 || num_handoff > 65535) return DOPD_ERR_INVALID_SHAPE;
-  dim3 grid((unsigned)((max_len + dopd::kPage - 1) / dopd::kPage), (unsigned)num_handoff,
-            (unsigned)zdim);
+  int64_t pages = 0;
+  for (int32_t n = 0; n < num_handoff; ++n) pages += (seq_lens_host[n] + dopd::kPage - 1) / dopd::kPage;
+  if (zdim * pages > INT32_MAX - 64) return DOPD_ERR_INVALID_SHAPE;
   hipStream_t strm = as_stream(stream);
+  auto launch = [&](auto type_tag) {
+    using T = decltype(type_tag);
+    dopd::PackArgs<T> a;
+    a.k_pool = static_cast<const T*>(k_pool);
+    a.v_pool = static_cast<const T*>(v_pool);
+    a.num_pages = num_pages;
+    a.page_table = pt;
+    a.pt_stride = pt_stride;
+    a.req_ids = req_ids;
+    a.seq_lens = seq_lens;
+    a.out_off = out_offsets;
+    a.hkv = s->num_kv_heads;
+    a.nz = (int)zdim;
+    a.nhand = num_handoff;
+    a.nblocks = (int)(zdim * pages);
+    a.out = static_cast<T*>(out);
+    if (s->head_dim == 64) {
+      constexpr int per = dopd::pack_blocks_per_wg<T, 64>();
+      hipLaunchKernelGGL((dopd::kv_pack_kernel<T, 64, per>), dim3((a.nblocks + per - 1) / per),
+                         dim3(256), 0, strm, a);
+    } else {
+      constexpr int per = dopd::pack_blocks_per_wg<T, 128>();
+      hipLaunchKernelGGL((dopd::kv_pack_kernel<T, 128, per>), dim3((a.nblocks + per - 1) / per),
+                         dim3(256), 0, strm, a);
+    }
+  };
   if (s->dtype == DOPD_FP8_E4M3)
-    hipLaunchKernelGGL(dopd::kv_pack_kernel<uint8_t>, grid, dim3(256), 0, strm,
-                       (const uint8_t*)k_pool, (const uint8_t*)v_pool, num_pages, pt, pt_stride,
-                       req_ids, seq_lens, out_offsets, s->num_kv_heads, s->head_dim, (uint8_t*)out);
+    launch(uint8_t{});
   else if (s->dtype == DOPD_BF16)
-    hipLaunchKernelGGL(dopd::kv_pack_kernel<uint16_t>, grid, dim3(256), 0, strm,
-                       (const uint16_t*)k_pool, (const uint16_t*)v_pool, num_pages, pt, pt_stride,
-                       req_ids, seq_lens, out_offsets, s->num_kv_heads, s->head_dim, (uint16_t*)out);
+    launch(uint16_t{});
   else
-    hipLaunchKernelGGL(dopd::kv_pack_kernel<uint32_t>, grid, dim3(256), 0, strm,
-                       (const uint32_t*)k_pool, (const uint32_t*)v_pool, num_pages, pt, pt_stride,
-                       req_ids, seq_lens, out_offsets, s->num_kv_heads, s->head_dim, (uint32_t*)out);
+    launch(uint32_t{});
   return launch_status();
 }
 
