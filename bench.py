@@ -45,7 +45,6 @@ PROFILES = os.path.join(ROOT, "profiles")
 KERNEL_SOURCES = ("paper_2511_20982_amd/csrc/dopd_attn.hip",
                   "paper_2511_20982_amd/csrc/plan.hpp",
                   "paper_2511_20982_amd/csrc/kernels/kv_write_pack.hpp",
-                  "paper_2511_20982_amd/csrc/kernels/kv_dequant.hpp",
                   "paper_2511_20982_amd/csrc/kernels/pd_step.hpp",
                   "paper_2511_20982_amd/csrc/kernels/common.hpp",
                   "paper_2511_20982_amd/csrc/kernels/attn_f32.hpp",
@@ -58,13 +57,16 @@ KERNEL_SOURCES = ("paper_2511_20982_amd/csrc/dopd_attn.hip",
 # some context exceeds one split, a merge kernel; a chunk call with key splits
 # adds the prefill merge kernel).
 CALL_KERNELS = {"decode": ("decode_split_kernel", "decode_merge_kernel"),
-                "prefill": ("prefill_bf16_kernel<128, false>", "prefill_bf16_kernel<64, false>"),
-                "prefill_chunked": ("prefill_bf16_kernel<128, true>", "prefill_bf16_kernel<64, true>",
+                "prefill": ("prefill_bf16_kernel<128, false, false>",
+                            "prefill_bf16_kernel<64, false, false>"),
+                "prefill_chunked": ("prefill_bf16_kernel<128, true, false>",
+                                    "prefill_bf16_kernel<64, true, false>",
                                     "prefill_split_merge_kernel"),
-                "prefill_chunked_fp8": ("kv_dequant_pages_kernel", "prefill_bf16_kernel<128, true>",
-                                        "prefill_bf16_kernel<64, true>",
+                "prefill_chunked_fp8": ("prefill_bf16_kernel<128, true, true>",
+                                        "prefill_bf16_kernel<64, true, true>",
                                         "prefill_split_merge_kernel"),
                 "kv_write": ("kv_write_kernel",), "kv_write_fp8": ("kv_write_e4m3_kernel",),
+                "plain_copy": ("bitwise_not_kernel",),
                 "pack": ("kv_pack_kernel",), "unpack": ("kv_unpack_kernel",),
                 "pd_step": ("pd_step_kernel", "decode_merge_kernel"),
                 "kv_write_pack": ("kv_write_pack_kernel",)}
@@ -88,7 +90,8 @@ WORKLOADS = {
                 "grid, then the decode merge)", 5),
     "write_pack": ("paged write + handoff pack of the mixed step's 8 x 512 fresh prompts (28/4 "
                    "heads, d128, bf16, 1 layer): the separate write and pack calls, then the "
-                   "one-pass write+pack (dopd_kv_write_pack_for_handoff)", 5),
+                   "one-pass write+pack (dopd_kv_write_pack_for_handoff), and a plain "
+                   "elementwise kernel moving the pack's bytes (the floor at this size)", 5),
     "handoff": ("P->D handoff on one GPU: pack 8 prefilled requests x 512 tokens from the P pool, "
                 "unpack into a D pool with another page order; 28/4 heads, d128, bf16, "
                 "--pack-layers layers", 5),
@@ -526,9 +529,19 @@ def build_workload(name, args, torch, A, I, sA):
             A.dopd_kv_write_pack_for_handoff(shape, k, v, kp, vp, w.num_pages, pt[n_dec:],
                                              stride, cu, w.cu_seqlens, n_pre, offs, out_h2, sA)
 
+        # The floor at this size: a plain elementwise kernel that reads and
+        # writes as many bytes as the pack does.
+        nb = pack_bytes(w.handoff_lens, 1, w.hkv, w.d) // 2
+        src16 = torch.zeros(nb // 2, dtype=torch.int16, device=dev)
+        dst16 = torch.empty_like(src16)
+
+        def plain_copy():
+            torch.bitwise_not(src16, out=dst16)
+
         work = {"kv_write": ("GB/s", write_bytes(w.prefill_lens, w.hkv, w.d)),
                 "pack": ("GB/s", pack_bytes(w.handoff_lens, 1, w.hkv, w.d)),
-                "kv_write_pack": ("GB/s", write_pack_bytes(w.prefill_lens, w.hkv, w.d))}
+                "kv_write_pack": ("GB/s", write_pack_bytes(w.prefill_lens, w.hkv, w.d)),
+                "plain_copy": ("GB/s", 2 * nb)}
 
         def cpu():
             import oracle
@@ -541,7 +554,8 @@ def build_workload(name, args, torch, A, I, sA):
                           "write_pack_bit_exact": bool(np.array_equal(A.to_host(out_h2), ref_h))}
 
         return Workload(name, desc, w.seed, [("kv_write", write), ("pack", pack),
-                                             ("kv_write_pack", write_pack)], work,
+                                             ("kv_write_pack", write_pack),
+                                             ("plain_copy", plain_copy)], work,
                         "kv_write_pack", cpu)
 
     if name in ("decode_mha", "decode_gqa"):

@@ -201,18 +201,16 @@ size_t dopd_prefill_paged_workspace_size(const dopd_attn_shape* shape,
  * K_j = code * k_scale[c] and V_j = code * v_scale[c] for KV head c (pool
  * layouts as there, one byte per element; k_scale/v_scale fp32 device arrays
  * [Hkv], positive and finite, not checked on the device); q and out bf16,
- * lse as there.  A first kernel widens the pages the call reads to bf16
- * (exactly: every E4M3 value is a bf16 value) into the workspace, packed
- * per request with their own page table; the bf16 prefill then runs over
- * them with the K scale folded into the softmax scale and the V scale into
- * the output, in fp32.  num_splits as in dopd_prefill_paged_attn_split.
+ * lse as there.  The kernel widens the codes to bf16 (exactly: every E4M3
+ * value is a bf16 value) as it reads them from LDS, with the K scale folded
+ * into the softmax scale and the V scale into the output, in fp32; half the
+ * bytes of bf16 pages per cached token.  num_splits as in
+ * dopd_prefill_paged_attn_split.
  *   workspace: device memory of at least
- *     dopd_prefill_paged_fp8_workspace_size() bytes for the same arguments,
- *     256-byte aligned, any contents (2 * pages * Hkv * 16 * d * 2 bytes of
- *     widened pages, where pages = sum over non-empty chunks of
- *     ceil((prefix_r + n_r) / 16), then the page table and the split
- *     partials).  Null only when every chunk is empty.  Calls that overlap
- *     in time must not share it.
+ *     dopd_prefill_paged_fp8_workspace_size() bytes for the same arguments
+ *     (the key-split partials, as dopd_prefill_paged_workspace_size gives
+ *     for bf16 pools), 256-byte aligned, any contents.  May be null when no
+ *     split is made.  Calls that overlap in time must not share it.
  */
 dopd_status dopd_prefill_paged_attn_fp8(const dopd_attn_shape* shape, const void* q,
                                         const void* k_pool, const void* v_pool,

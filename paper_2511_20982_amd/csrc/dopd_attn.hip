@@ -13,7 +13,6 @@
 #include "kernels/attn_f32.hpp"
 #include "kernels/common.hpp"
 #include "kernels/decode_bf16.hpp"
-#include "kernels/kv_dequant.hpp"
 #include "kernels/kv_pack.hpp"
 #include "kernels/kv_unpack.hpp"
 #include "kernels/kv_write.hpp"
@@ -308,7 +307,7 @@ dopd_status plan_prefill_bf16(dopd::PrefillArgs& a, const int32_t* cu_host,
 // on the paged path, the cached prefixes prefix_host).  Work items are
 // (q tile, request, head); with at most 64 requests the XCD-aware order is
 // used, requests ranked by the keys their last row sees.
-template <bool PAGED>
+template <bool PAGED, bool KV8 = false>
 dopd_status launch_prefill_bf16(dopd::PrefillArgs a, int d, const int32_t* cu_host,
                                 const int32_t* prefix_host, int32_t nreq, hipStream_t strm) {
   int64_t blocks = 0;
@@ -316,10 +315,10 @@ dopd_status launch_prefill_bf16(dopd::PrefillArgs a, int d, const int32_t* cu_ho
   if (pst != DOPD_OK) return pst;
   if (blocks == 0) return DOPD_OK;
   if (d == 64)
-    hipLaunchKernelGGL((dopd::prefill_bf16_kernel<64, PAGED>), dim3((unsigned)blocks),
+    hipLaunchKernelGGL((dopd::prefill_bf16_kernel<64, PAGED, KV8>), dim3((unsigned)blocks),
                        dim3(dopd::kPfThreads), 0, strm, a);
   else
-    hipLaunchKernelGGL((dopd::prefill_bf16_kernel<128, PAGED>), dim3((unsigned)blocks),
+    hipLaunchKernelGGL((dopd::prefill_bf16_kernel<128, PAGED, KV8>), dim3((unsigned)blocks),
                        dim3(dopd::kPfThreads), 0, strm, a);
   const dopd_status st = launch_status();
   if (st != DOPD_OK || a.nsplit == 1) return st;
@@ -411,7 +410,8 @@ static dopd_status prefill_paged_impl(const dopd_attn_shape* s, const void* q, c
                                const int32_t* prefix, const int32_t* prefix_host, int32_t nreq,
                                int32_t num_splits, void* out, float* lse, void* workspace,
                                size_t workspace_bytes, void* stream,
-                               const float* k_scale = nullptr, const float* v_scale = nullptr) {
+                               const float* k_scale = nullptr, const float* v_scale = nullptr,
+                               bool kv8 = false) {
   dopd_status st = check_shape_no_fp8(s);
   if (st != DOPD_OK) return st;
   if (nreq < 0 || num_pages < 0 || pt_stride < 0 || num_splits < 0) return DOPD_ERR_INVALID_SHAPE;
@@ -465,7 +465,8 @@ static dopd_status prefill_paged_impl(const dopd_attn_shape* s, const void* q, c
     a.part_ml = reinterpret_cast<float*>(static_cast<char*>(workspace) +
                                          dopd::align256(rows * d * sizeof(float)));
   }
-  return launch_prefill_bf16<true>(a, d, cu_host, prefix_host, nreq, strm);
+  return kv8 ? launch_prefill_bf16<true, true>(a, d, cu_host, prefix_host, nreq, strm)
+             : launch_prefill_bf16<true>(a, d, cu_host, prefix_host, nreq, strm);
 }
 
 dopd_status dopd_prefill_paged_attn(const dopd_attn_shape* s, const void* q, const void* k_pool,
@@ -505,67 +506,25 @@ dopd_status dopd_prefill_paged_attn_split(const dopd_attn_shape* s, const void* 
 }
 
 // ---------------------------------------------------------------- E4M3 chunk prefill
+// The paged prefill over E4M3 pools: the same work list and workspace (split
+// partials only) as the bf16 pools; the kernel widens the codes as they leave
+// LDS.
 extern "C++" {
 namespace {
-
-// Workspace of the chunk prefill over E4M3 pages: the pages the call reads,
-// dequantised to bf16 and packed ([pages][Hkv][16][d] for K, [pages][Hkv][d][16]
-// for V), their page table ([nreq][stride]), then the key-split partials.
-struct PagedFp8Layout {
-  int64_t pages;
-  int32_t stride;
-  int nsplit;
-  size_t k_off, v_off, pt_off, split_off, total;
-};
-
 dopd_attn_shape as_bf16(const dopd_attn_shape* s) {
   dopd_attn_shape b = *s;
   b.dtype = DOPD_BF16;
   return b;
 }
-
-dopd_status paged_fp8_layout(const dopd_attn_shape* s, const int32_t* cu_host,
-                             const int32_t* prefix_host, int32_t nreq, int32_t num_splits,
-                             PagedFp8Layout* L) {
-  *L = PagedFp8Layout{};
-  if (cu_host[0] != 0) return DOPD_ERR_INVALID_SHAPE;
-  int64_t pages = 0, stride = 1;
-  for (int32_t r = 0; r < nreq; ++r) {
-    const int64_t n = (int64_t)cu_host[r + 1] - cu_host[r];
-    if (n < 0 || prefix_host[r] < 0) return DOPD_ERR_INVALID_SHAPE;
-    const int64_t np = n > 0 ? (prefix_host[r] + n + dopd::kPage - 1) / dopd::kPage : 0;
-    pages += np;
-    stride = std::max(stride, np);
-  }
-  if (pages > INT32_MAX / 2 || stride > INT32_MAX / 2) return DOPD_ERR_INVALID_SHAPE;
-  const dopd_attn_shape b = as_bf16(s);
-  L->pages = pages;
-  L->stride = (int32_t)stride;
-  L->nsplit = num_splits == 1 ? 1 : paged_splits(&b, cu_host, prefix_host, nreq, num_splits);
-  const size_t pool = (size_t)pages * s->num_kv_heads * dopd::kPage * s->head_dim * 2;
-  L->k_off = 0;
-  L->v_off = dopd::align256(pool);
-  L->pt_off = L->v_off + dopd::align256(pool);
-  L->split_off = L->pt_off + dopd::align256((size_t)nreq * stride * 4);
-  L->total = std::max<size_t>(256, L->split_off + dopd::prefill_paged_ws_bytes(
-                                                      s->num_q_heads, s->head_dim,
-                                                      cu_host[nreq], L->nsplit));
-  return DOPD_OK;
-}
-
 }  // namespace
 }  // extern "C++"
 
 size_t dopd_prefill_paged_fp8_workspace_size(const dopd_attn_shape* s, const int32_t* cu_host,
                                              const int32_t* prefix_host, int32_t nreq,
                                              int32_t num_splits) {
-  if (check_shape(s) != DOPD_OK || s->dtype != DOPD_FP8_E4M3 || nreq < 0 || num_splits < 0)
-    return 0;
-  if (nreq == 0) return 256;
-  if (!cu_host || !prefix_host) return 0;
-  PagedFp8Layout L;
-  if (paged_fp8_layout(s, cu_host, prefix_host, nreq, num_splits, &L) != DOPD_OK) return 0;
-  return L.total;
+  if (check_shape(s) != DOPD_OK || s->dtype != DOPD_FP8_E4M3) return 0;
+  const dopd_attn_shape b = as_bf16(s);
+  return dopd_prefill_paged_workspace_size(&b, cu_host, prefix_host, nreq, num_splits);
 }
 
 dopd_status dopd_prefill_paged_attn_fp8(const dopd_attn_shape* s, const void* q,
@@ -580,51 +539,11 @@ dopd_status dopd_prefill_paged_attn_fp8(const dopd_attn_shape* s, const void* q,
   dopd_status st = check_shape(s);
   if (st != DOPD_OK) return st;
   if (s->dtype != DOPD_FP8_E4M3) return DOPD_ERR_UNSUPPORTED;
-  if (nreq < 0 || num_pages < 0 || pt_stride < 0 || num_splits < 0) return DOPD_ERR_INVALID_SHAPE;
-  if (nreq == 0) return DOPD_OK;
-  if (!q || !k_pool || !v_pool || !k_scale || !v_scale || !page_table || !cu || !cu_host ||
-      !prefix || !prefix_host || !out)
-    return DOPD_ERR_NULL_POINTER;
-  PagedFp8Layout L;
-  st = paged_fp8_layout(s, cu_host, prefix_host, nreq, num_splits, &L);
-  if (st != DOPD_OK) return st;
-  for (int32_t r = 0; r < nreq; ++r) {
-    const int64_t n = (int64_t)cu_host[r + 1] - cu_host[r];
-    if (n > 0 && (prefix_host[r] + n + dopd::kPage - 1) / dopd::kPage > pt_stride)
-      return DOPD_ERR_INVALID_SHAPE;
-  }
-  if (L.pages == 0) return DOPD_OK;  // every chunk is empty
-  if (!workspace) return DOPD_ERR_NULL_POINTER;
-  if (workspace_bytes < L.total) return DOPD_ERR_WORKSPACE_TOO_SMALL;
-  if ((reinterpret_cast<uintptr_t>(workspace) & 255) != 0) return DOPD_ERR_INVALID_SHAPE;
-  if (L.pages * s->num_kv_heads > INT32_MAX) return DOPD_ERR_INVALID_SHAPE;
-  char* ws = static_cast<char*>(workspace);
-  dopd::DequantArgs dq;
-  dq.k_pool = (const uint8_t*)k_pool;
-  dq.v_pool = (const uint8_t*)v_pool;
-  dq.page_table = page_table;
-  dq.pt_stride = pt_stride;
-  dq.cu = cu;
-  dq.prefix = prefix;
-  dq.nreq = nreq;
-  dq.hkv = s->num_kv_heads;
-  dq.k_out = reinterpret_cast<uint16_t*>(ws + L.k_off);
-  dq.v_out = reinterpret_cast<uint16_t*>(ws + L.v_off);
-  dq.pt_out = reinterpret_cast<int32_t*>(ws + L.pt_off);
-  dq.pt_out_stride = L.stride;
-  hipStream_t strm = as_stream(stream);
-  const unsigned blocks = (unsigned)(L.pages * s->num_kv_heads);
-  if (s->head_dim == 64)
-    hipLaunchKernelGGL(dopd::kv_dequant_pages_kernel<64>, dim3(blocks), dim3(256), 0, strm, dq);
-  else
-    hipLaunchKernelGGL(dopd::kv_dequant_pages_kernel<128>, dim3(blocks), dim3(256), 0, strm, dq);
-  st = launch_status();
-  if (st != DOPD_OK) return st;
+  if (nreq > 0 && (!k_scale || !v_scale)) return DOPD_ERR_NULL_POINTER;
   const dopd_attn_shape b = as_bf16(s);
-  return prefill_paged_impl(&b, q, dq.k_out, dq.v_out, (int32_t)L.pages, dq.pt_out, L.stride, cu,
-                            cu_host, prefix, prefix_host, nreq, L.nsplit, out, lse,
-                            ws + L.split_off, workspace_bytes - L.split_off, stream, k_scale,
-                            v_scale);
+  return prefill_paged_impl(&b, q, k_pool, v_pool, num_pages, page_table, pt_stride, cu, cu_host,
+                            prefix, prefix_host, nreq, num_splits, out, lse, workspace,
+                            workspace_bytes, stream, k_scale, v_scale, true);
 }
 
 // ---------------------------------------------------------------- kv write

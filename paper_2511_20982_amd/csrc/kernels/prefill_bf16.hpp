@@ -66,9 +66,9 @@ struct PrefillArgs {
   const int32_t* prefix;      // [nreq]
   int pt_stride;
   // Per-KV-head scales of the cached K and V (null: 1): key = cached value *
-  // k_scale[c], value = cached value * v_scale[c] (pages dequantised from E4M3
-  // codes, which bf16 holds exactly).  The K scale multiplies the softmax
-  // scale, the V scale the output.
+  // k_scale[c], value = cached value * v_scale[c] (E4M3 pools, KV8: the pools
+  // hold one-byte codes, widened to bf16 exactly as they leave LDS).  The K
+  // scale multiplies the softmax scale, the V scale the output.
   const float* k_scale;
   const float* v_scale;
   // Key splits of the paged kernel (nsplit > 1): workgroup b computes split
@@ -172,7 +172,7 @@ constexpr int pf_q_lds_elems() { return PAGED ? 8 : (D / 32) * kPfThreads * 8; }
 // not wait for them.
 // PAGED = false: fresh prompts, K/V token-major beside Q (dopd_prefill_attn).
 // PAGED = true: chunks attending to the paged cache (dopd_prefill_paged_attn).
-template <int D, bool PAGED>
+template <int D, bool PAGED, bool KV8 = false>
 __device__ __forceinline__ void prefill_workgroup(const PrefillArgs& a, int bid, uint16_t* sK0,
                                                   uint16_t* sK1, uint16_t* sV0, uint16_t* sV1,
                                                   uint16_t* sQ) {
@@ -181,6 +181,8 @@ __device__ __forceinline__ void prefill_workgroup(const PrefillArgs& a, int bid,
   constexpr int ET = D / 32;     // O^T tiles of 32 dims
   constexpr int CPR = D / 8;     // 16-byte chunks per K/V row
   constexpr int KQW = BN * CPR / kPfThreads;   // 16-byte chunks of a K (or V) tile per thread
+  static_assert(!KV8 || PAGED, "E4M3 pools are read by the paged kernel only");
+  constexpr int NCH8 = D / 16;                 // E4M3: 16-byte chunks per K row
   auto kbuf = [&](int b) { return b ? sK1 : sK0; };
   auto vbuf = [&](int b) { return b ? sV1 : sV0; };
 
@@ -226,16 +228,21 @@ __device__ __forceinline__ void prefill_workgroup(const PrefillArgs& a, int bid,
     const bool wave_active = row_w < L;
     const int hi = l >> 5;                    // lane half
 
-    // Q^T operand, B of the QK MFMA: lane holds Q[myq][16ks + 8hi + 0..7].
+    // Q^T operand, B of the QK MFMA: lane holds Q[myq][16ks + 8hi + 0..7]
+    // (E4M3 pools: Q[myq][32(ks/2) + 16hi + 8(ks%2) + 0..7], the dims one
+    // 16-byte read of an E4M3 K row gives a lane over two k-steps; the
+    // contraction over d is the same sum in another order).
     // Rows past the chunk read its row 0 (finite values; their results are
     // never stored), so nothing waits for these loads before the tile loads
     // below are issued.
     bf16x8 qop[KS];
     {
-      const uint16_t* qp = a.q + ((int64_t)(seq0 + (myq < L ? myq : 0)) * a.hq + h) * D + 8 * hi;
+      const uint16_t* qp = a.q + ((int64_t)(seq0 + (myq < L ? myq : 0)) * a.hq + h) * D +
+                           (KV8 ? 16 : 8) * hi;
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks)
-        qop[ks] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(qp + 16 * ks));
+        qop[ks] = __builtin_bit_cast(
+            bf16x8, *reinterpret_cast<const u32x4*>(qp + (KV8 ? 32 * (ks / 2) + 8 * (ks % 2) : 16 * ks)));
     }
 
     if constexpr (!PAGED) {  // (this lane's own slots: no barrier needed)
@@ -307,13 +314,35 @@ __device__ __forceinline__ void prefill_workgroup(const PrefillArgs& a, int bid,
             rsrc, (__attribute__((address_space(3))) void*)(lds + (4 * u + w) * 512), 16, lane_off,
             u_stride * u, 0, 0);
     };
+    // E4M3 pools: wave w copies its page block (16 x D bytes) into bytes
+    // [16 D w, 16 D (w + 1)) of the tile buffer, instruction u filling its
+    // 16-byte chunks [64u, 64u + 64).  K: chunk q is row s = q / NCH8 (page
+    // slot pi(s)), physical chunk q % NCH8 holding logical chunk
+    // (q % NCH8) ^ (s % NCH8), so that 16 rows read at one logical chunk hit
+    // distinct bank groups.  V: chunk q is dim row q (its 16 keys).
+    const int lane_k8 = [&] {
+      const int s8 = l / NCH8, pc = l % NCH8;  // chunk q = 64u + l: row s8 + (64 / NCH8) u
+      return ((s8 & 3) | ((s8 & 4) << 1) | ((s8 & 8) >> 1)) * D + 16 * (pc ^ (s8 % NCH8));
+    }();
+    auto stage_page8 = [&](const uint16_t* pool, uint16_t* lds, int page, int lane_off, int u_stride) {
+      const __amdgpu_buffer_rsrc_t rsrc = __builtin_amdgcn_make_buffer_rsrc(
+          (void*)(reinterpret_cast<const uint8_t*>(pool) + ((int64_t)page * a.hkv + kvh) * (kPage * D)),
+          (short)0, kPage * D, 0x00020000);
+#pragma unroll
+      for (int u = 0; u < D / 64; ++u)
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(
+            rsrc, (__attribute__((address_space(3))) void*)(lds + (w * kPage * D + 1024 * u) / 2), 16,
+            lane_off, u_stride * u, 0, 0);
+    };
     // (Paged: the page comes from pid_k / pid_v, not from kv0.)
     auto load_k = [&](int buf, int kv0) {
-      if constexpr (PAGED) stage_page(a.k_pool, kbuf(buf), pid_k, lane_pk, 64);
+      if constexpr (KV8) stage_page8(a.k_pool, kbuf(buf), pid_k, lane_k8, 4 * D);  // rows s, s + 8: slots pi(s), pi(s) + 4
+      else if constexpr (PAGED) stage_page(a.k_pool, kbuf(buf), pid_k, lane_pk, 64);
       else stage(kg, kbuf(buf), kv0, lane_k, k_c);
     };
     auto load_v = [&](int buf, int kv0) {
-      if constexpr (PAGED) stage_page(a.v_pool, vbuf(buf), pid_v, lane_pv, 32 * 2 * kPage);
+      if constexpr (KV8) stage_page8(a.v_pool, vbuf(buf), pid_v, 16 * l, 1024);
+      else if constexpr (PAGED) stage_page(a.v_pool, vbuf(buf), pid_v, lane_pv, 32 * 2 * kPage);
       else stage(vg, vbuf(buf), kv0, lane_v, v_c);
     };
 
@@ -324,6 +353,33 @@ __device__ __forceinline__ void prefill_workgroup(const PrefillArgs& a, int bid,
     auto kread = [&](int buf, int tt, int ks) {
       const int off = (ks >> 1) * (BN * 32) + tt * 1024 + ((ks & 1) ? kr_odd : kr_even);
       return *reinterpret_cast<const bf16x8*>(kbuf(buf) + off);
+    };
+    // E4M3: row 32tt + l%32 of the tile (wave page (32tt + l%32)/16), logical
+    // chunk 2p + hi -> the k-steps 2p and 2p + 1 of this lane.
+    const int kr8 = (l & 31) * D;
+    auto kread8 = [&](int buf, int tt, int p, bf16x8& k0, bf16x8& k1) {
+      const int row = 32 * tt + (l & 31);
+      const u32x4 c = *reinterpret_cast<const u32x4*>(
+          reinterpret_cast<const uint8_t*>(kbuf(buf)) + tt * 32 * D + kr8 +
+          16 * ((2 * p + hi) ^ (row % NCH8)));
+      const u32x2 a0 = bf16x4_from_e4m3x4(c[0]), a1 = bf16x4_from_e4m3x4(c[1]);
+      const u32x2 a2 = bf16x4_from_e4m3x4(c[2]), a3 = bf16x4_from_e4m3x4(c[3]);
+      k0 = __builtin_bit_cast(bf16x8, u32x4{a0[0], a0[1], a1[0], a1[1]});
+      k1 = __builtin_bit_cast(bf16x8, u32x4{a2[0], a2[1], a3[0], a3[1]});
+    };
+    // K operands of a tile: ka[tt][ks].
+    auto kread_all = [&](int buf, bf16x8 (&ka)[2][KS]) {
+      if constexpr (KV8) {
+#pragma unroll
+        for (int tt = 0; tt < 2; ++tt)
+#pragma unroll
+          for (int p = 0; p < KS / 2; ++p) kread8(buf, tt, p, ka[tt][2 * p], ka[tt][2 * p + 1]);
+      } else {
+#pragma unroll
+        for (int tt = 0; tt < 2; ++tt)
+#pragma unroll
+          for (int ks = 0; ks < KS; ++ks) ka[tt][ks] = kread(buf, tt, ks);
+      }
     };
     // A operand of P.V k-step kk = 2tt + hh: V^T[32 et + l%32][keys 32tt + 16hh
     // + 8m + 4hi + 0..3, m = 0, 1], i.e. k-slot 8hi + jj <-> key
@@ -336,7 +392,13 @@ __device__ __forceinline__ void prefill_workgroup(const PrefillArgs& a, int bid,
     const int vr_base = 128 * hi + 32 * ((l & 15) >> 2) + 16 * ((l >> 4) & 1) + 4 * (l & 3);
     auto vread = [&](int buf, int kk, int et) {
       bf16x8 res;
-      if constexpr (PAGED) {  // keys 16kk + 8hi + 0..7 of dim 32et + l%32: one 16-byte chunk
+      if constexpr (KV8) {  // keys 16kk + 8hi + 0..7 of dim 32et + l%32: 8 bytes of its row
+        const u32x2 c = *reinterpret_cast<const u32x2*>(
+            reinterpret_cast<const uint8_t*>(vbuf(buf)) + kk * (kPage * D) + (32 * et + (l & 31)) * 16 +
+            8 * hi);
+        const u32x2 a0 = bf16x4_from_e4m3x4(c[0]), a1 = bf16x4_from_e4m3x4(c[1]);
+        res = __builtin_bit_cast(bf16x8, u32x4{a0[0], a0[1], a1[0], a1[1]});
+      } else if constexpr (PAGED) {  // keys 16kk + 8hi + 0..7 of dim 32et + l%32: one 16-byte chunk
         res = *reinterpret_cast<const bf16x8*>(vbuf(buf) + ((et * 8 + 2 * kk + hi) * 32 + (l & 31)) * 8);
       } else {
         typedef short s16x4_t __attribute__((ext_vector_type(4)));
@@ -419,23 +481,22 @@ __device__ __forceinline__ void prefill_workgroup(const PrefillArgs& a, int bid,
     };
     auto qk = [&](int buf, f32x16* s) {
       bf16x8 ka[2][KS];
-#pragma unroll
-      for (int tt = 0; tt < 2; ++tt)
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks) ka[tt][ks] = kread(buf, tt, ks);
+      kread_all(buf, ka);
       zero2(s);
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks)
 #pragma unroll
         for (int tt = 0; tt < 2; ++tt)
           s[tt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[tt][ks], qop[ks], s[tt], 0, 0, 0);
-      __builtin_amdgcn_sched_group_barrier(kDsRead, 4, 0);
+      if constexpr (!KV8) {
+        __builtin_amdgcn_sched_group_barrier(kDsRead, 4, 0);
 #pragma unroll
-      for (int ks = 0; ks < KS - 2; ++ks) {
-        __builtin_amdgcn_sched_group_barrier(kMfma, 2, 0);
-        __builtin_amdgcn_sched_group_barrier(kDsRead, 2, 0);
+        for (int ks = 0; ks < KS - 2; ++ks) {
+          __builtin_amdgcn_sched_group_barrier(kMfma, 2, 0);
+          __builtin_amdgcn_sched_group_barrier(kDsRead, 2, 0);
+        }
+        __builtin_amdgcn_sched_group_barrier(kMfma, 4, 0);
       }
-      __builtin_amdgcn_sched_group_barrier(kMfma, 4, 0);
     };
     // S^T for the diagonal steps of the dense kernel: Q operands KS/2 .. from
     // this lane's copy in LDS.
@@ -468,15 +529,17 @@ __device__ __forceinline__ void prefill_workgroup(const PrefillArgs& a, int bid,
 #pragma unroll
         for (int et = 0; et < ET; ++et)
           oacc[et] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[kk][et], pb[kk], oacc[et], 0, 0, 0);
-      __builtin_amdgcn_sched_group_barrier(kDsRead, 2 * ET, 0);
+      if constexpr (!KV8) {
+        __builtin_amdgcn_sched_group_barrier(kDsRead, 2 * ET, 0);
 #pragma unroll
-      for (int kk = 0; kk < 3; ++kk)
+        for (int kk = 0; kk < 3; ++kk)
 #pragma unroll
-        for (int et = 0; et < ET; ++et) {
-          __builtin_amdgcn_sched_group_barrier(kMfma, 1, 0);
-          __builtin_amdgcn_sched_group_barrier(kDsRead, 2, 0);
-        }
-      __builtin_amdgcn_sched_group_barrier(kMfma, ET, 0);
+          for (int et = 0; et < ET; ++et) {
+            __builtin_amdgcn_sched_group_barrier(kMfma, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(kDsRead, 2, 0);
+          }
+        __builtin_amdgcn_sched_group_barrier(kMfma, ET, 0);
+      }
     };
     auto softmax_masked = [&](f32x16* s, int kv0) {
       if (!pos_scale) {
@@ -502,10 +565,7 @@ __device__ __forceinline__ void prefill_workgroup(const PrefillArgs& a, int bid,
     // the MFMAs compute S^T of tile j + 1 (K buffer kb).
     auto half_qk = [&](f32x16* sc, f32x16* sn, int kb) {
       bf16x8 ka[2][KS];
-#pragma unroll
-      for (int tt = 0; tt < 2; ++tt)
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks) ka[tt][ks] = kread(kb, tt, ks);
+      kread_all(kb, ka);
       zero2(sn);
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks)
@@ -514,12 +574,14 @@ __device__ __forceinline__ void prefill_workgroup(const PrefillArgs& a, int bid,
           sn[tt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[tt][ks], qop[ks], sn[tt], 0, 0, 0);
       float psum = exponent(sc);
       constexpr int NM = 2 * KS;  // MFMAs of this region
-      __builtin_amdgcn_sched_group_barrier(kDsRead, 4, 0);
+      if constexpr (!KV8) {
+        __builtin_amdgcn_sched_group_barrier(kDsRead, 4, 0);
 #pragma unroll
-      for (int i = 0; i < NM; ++i) {
-        __builtin_amdgcn_sched_group_barrier(kMfma, 1, 0);
-        __builtin_amdgcn_sched_group_barrier(kValu, 100 / NM, 0);
-        if (i + 4 < NM) __builtin_amdgcn_sched_group_barrier(kDsRead, 1, 0);
+        for (int i = 0; i < NM; ++i) {
+          __builtin_amdgcn_sched_group_barrier(kMfma, 1, 0);
+          __builtin_amdgcn_sched_group_barrier(kValu, 100 / NM, 0);
+          if (i + 4 < NM) __builtin_amdgcn_sched_group_barrier(kDsRead, 1, 0);
+        }
       }
       if (__ballot(!(psum <= __builtin_exp2f(kSumLazy)))) {  // wave-uniform, rare
         rescale_to(row_max(sc));
@@ -534,7 +596,27 @@ __device__ __forceinline__ void prefill_workgroup(const PrefillArgs& a, int bid,
     // tile's V pages have landed each wave clears those keys in its own page
     // of the V tile; the barrier that closes the step publishes the zeros.
     auto clear_dead_v = [&](int buf, int jt) {
-      if constexpr (PAGED) {
+      if constexpr (KV8) {  // this wave's page: [D dim rows][16 key bytes]
+        const int nlive = kv_end - jt * BN;
+        if (nlive >= 16 * w + 16) return;
+        __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0): this wave's V page has landed
+        const int nv = nlive - 16 * w;       // live keys of the page (may be <= 0)
+        uint32_t keep[4];
+#pragma unroll
+        for (int wd = 0; wd < 4; ++wd) {
+          const int nb = nv - 4 * wd;  // live bytes of word wd
+          keep[wd] = nb >= 4 ? 0xffffffffu : (nb <= 0 ? 0u : (1u << (8 * nb)) - 1u);
+        }
+#pragma unroll
+        for (int i = 0; i < D / 64; ++i) {
+          u32x4* p = reinterpret_cast<u32x4*>(reinterpret_cast<uint8_t*>(vbuf(buf)) + w * (kPage * D) +
+                                              (l + 64 * i) * 16);
+          u32x4 x = *p;
+#pragma unroll
+          for (int wd = 0; wd < 4; ++wd) x[wd] &= keep[wd];
+          *p = x;
+        }
+      } else if constexpr (PAGED) {
         const int nlive = kv_end - jt * BN;  // live keys of tile jt (uniform, >= 1)
         if (nlive >= 16 * w + 16) return;    // this wave's page is all live
         __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0): this wave's V page has landed
@@ -699,12 +781,12 @@ __device__ __forceinline__ void prefill_workgroup(const PrefillArgs& a, int bid,
   }
 }
 
-template <int D, bool PAGED>
+template <int D, bool PAGED, bool KV8 = false>
 __global__ __launch_bounds__(kPfThreads, 2) void prefill_bf16_kernel(PrefillArgs a) {
   __shared__ __attribute__((aligned(16))) uint16_t sK0[pf_tile_elems<D>()], sK1[pf_tile_elems<D>()];
   __shared__ __attribute__((aligned(16))) uint16_t sV0[pf_tile_elems<D>()], sV1[pf_tile_elems<D>()];
   __shared__ __attribute__((aligned(16))) uint16_t sQ[pf_q_lds_elems<D, PAGED>()];
-  prefill_workgroup<D, PAGED>(a, (int)blockIdx.x, sK0, sK1, sV0, sV1, sQ);
+  prefill_workgroup<D, PAGED, KV8>(a, (int)blockIdx.x, sK0, sK1, sV0, sV1, sQ);
 }
 
 // Combines the key splits of the paged prefill.  Thread = one 4-dim chunk of
