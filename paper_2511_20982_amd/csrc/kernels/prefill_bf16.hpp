@@ -431,7 +431,7 @@ __device__ __forceinline__ void prefill_workgroup(const PrefillArgs& a, int bid,
 
     f32x16 sa[2], sb[2];  // S^T of two consecutive key tiles (current / next)
     bf16x8 pb[4];         // P^T of the current tile: B operands of the four P.V k-steps
-    constexpr int kValu = 0x002, kMfma = 0x008, kDsRead = 0x100;
+    constexpr int kMfma = 0x008, kDsRead = 0x100;  // sched_group_barrier masks
 
     auto zero2 = [&](f32x16* s) {
 #pragma unroll
@@ -488,15 +488,6 @@ __device__ __forceinline__ void prefill_workgroup(const PrefillArgs& a, int bid,
 #pragma unroll
         for (int tt = 0; tt < 2; ++tt)
           s[tt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[tt][ks], qop[ks], s[tt], 0, 0, 0);
-      if constexpr (!KV8) {
-        __builtin_amdgcn_sched_group_barrier(kDsRead, 4, 0);
-#pragma unroll
-        for (int ks = 0; ks < KS - 2; ++ks) {
-          __builtin_amdgcn_sched_group_barrier(kMfma, 2, 0);
-          __builtin_amdgcn_sched_group_barrier(kDsRead, 2, 0);
-        }
-        __builtin_amdgcn_sched_group_barrier(kMfma, 4, 0);
-      }
     };
     // S^T for the diagonal steps of the dense kernel: Q operands KS/2 .. from
     // this lane's copy in LDS.
@@ -529,7 +520,11 @@ __device__ __forceinline__ void prefill_workgroup(const PrefillArgs& a, int bid,
 #pragma unroll
         for (int et = 0; et < ET; ++et)
           oacc[et] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[kk][et], pb[kk], oacc[et], 0, 0, 0);
-      if constexpr (!KV8) {
+      // Interleaving hints for the dense kernel's P.V only (its V operands
+      // come from two transposing reads each).  Measured: hints on the QK
+      // products cost the dense kernel 2-3 %, and any hints cost the paged
+      // kernel 8 % (404 against 148 bytes of spill per lane).
+      if constexpr (!PAGED) {
         __builtin_amdgcn_sched_group_barrier(kDsRead, 2 * ET, 0);
 #pragma unroll
         for (int kk = 0; kk < 3; ++kk)
@@ -573,16 +568,6 @@ __device__ __forceinline__ void prefill_workgroup(const PrefillArgs& a, int bid,
         for (int tt = 0; tt < 2; ++tt)
           sn[tt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[tt][ks], qop[ks], sn[tt], 0, 0, 0);
       float psum = exponent(sc);
-      constexpr int NM = 2 * KS;  // MFMAs of this region
-      if constexpr (!KV8) {
-        __builtin_amdgcn_sched_group_barrier(kDsRead, 4, 0);
-#pragma unroll
-        for (int i = 0; i < NM; ++i) {
-          __builtin_amdgcn_sched_group_barrier(kMfma, 1, 0);
-          __builtin_amdgcn_sched_group_barrier(kValu, 100 / NM, 0);
-          if (i + 4 < NM) __builtin_amdgcn_sched_group_barrier(kDsRead, 1, 0);
-        }
-      }
       if (__ballot(!(psum <= __builtin_exp2f(kSumLazy)))) {  // wave-uniform, rare
         rescale_to(row_max(sc));
         psum = exponent(sc);
