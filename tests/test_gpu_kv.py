@@ -88,6 +88,27 @@ def test_pack_unaligned_offsets():
     assert np.array_equal(out[3:], ref[3:])        # elements before off[0] are not written
 
 
+@pytest.mark.parametrize("dtype,d", [("bf16", 128), ("fp32", 64)])
+def test_pack_many_handoffs(dtype, d):
+    # More handoffs than one wave scans at once (the block list is found by
+    # 64-wide scans), empty handoffs among them, and workgroups whose blocks
+    # straddle handoffs.
+    rng = np.random.default_rng(39)
+    hkv, layers = 2, 2
+    lens = rng.integers(0, 70, 150).astype(np.int32)
+    lens[[0, 64, 65, 149]] = 0
+    lens[[3, 100]] = [16, 129]
+    pt, num_pages = I.allocate_pages(rng, np.maximum(lens, 1))
+    kp = I.normal(rng, (layers, num_pages, hkv, 16, d), dtype)
+    vp = I.normal(rng, (layers, num_pages, hkv, d, 16), dtype)
+    req = rng.permutation(len(lens)).astype(np.int32)
+    seq = lens[req]
+    off = I.handoff_offsets(seq, layers, hkv, d)
+    ref = oracle.pack(kp, vp, layers, pt, req, seq, off)
+    out = G.gpu_pack(G.A.make_shape(4, hkv, d, dtype), kp, vp, layers, pt, req, seq, off)
+    assert np.array_equal(out.view(np.uint8), ref.view(np.uint8))
+
+
 def test_write_then_pack_round_trip_is_a_transpose():
     rng = np.random.default_rng(35)
     hkv, d = 4, 128

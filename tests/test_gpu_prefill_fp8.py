@@ -71,6 +71,20 @@ def test_prefill_paged_fp8_key_splits(splits, d):
     assert np.max(np.abs(lse - ref_lse)) < 2e-2
 
 
+def test_prefill_paged_fp8_many_requests():
+    # More than 64 requests: the heaviest-q-tile-first work order.
+    rng = np.random.default_rng(96)
+    prefix = rng.integers(0, 300, 70).astype(np.int32)
+    chunk = rng.integers(0, 90, 70).astype(np.int32)
+    q, k8, v8, ks, vs, pt, cu, pre = fp8_case(96, prefix, chunk, 8, 2, 128)
+    ref, ref_lse = oracle.prefill_paged_e4m3(q, k8, v8, ks, vs, pt, cu, pre, 1 / np.sqrt(128))
+    sh = G.A.make_shape(8, 2, 128, "fp8")
+    for splits in (1, 0):
+        out, lse = G.gpu_prefill_paged_fp8(sh, q, k8, v8, ks, vs, pt, cu, pre, splits=splits)
+        G.assert_attention_close(out, ref, "bf16", f"fp8 chunk prefill, 70 requests, splits={splits}")
+        assert np.max(np.abs(lse - ref_lse)) < 2e-2
+
+
 def test_prefill_paged_fp8_chunk_of_one_matches_fp8_decode():
     q, k8, v8, ks, vs, pt, cu, pre = fp8_case(97, [30, 0, 17, 2047], [1, 1, 1, 1], 28, 4, 128)
     sh = G.A.make_shape(28, 4, 128, "fp8")
