@@ -87,7 +87,7 @@ WORKLOADS = {
                 "read from it", 3),
     "pd_step": ("the mixed P/D step + handoff of the mixed workload as one PD-aggregated launch "
                 "(dopd_pd_step: decode slices, prefill items and write+pack workgroups in one "
-                "grid, then the decode merge)", 5),
+                "grid, then the decode merge); --kv fp8: over E4M3 pages (dopd_pd_step_fp8)", 5),
     "write_pack": ("paged write + handoff pack of the mixed step's 8 x 512 fresh prompts (28/4 "
                    "heads, d128, bf16, 1 layer): the separate write and pack calls, then the "
                    "one-pass write+pack (dopd_kv_write_pack_for_handoff), and a plain "
@@ -476,21 +476,65 @@ def build_workload(name, args, torch, A, I, sA):
         offs = A.to_device(offs_np)
         out_h = torch.empty(int(offs_np[-1]), dtype=torch.bfloat16, device=dev)
         ws = A.pd_step_workspace(shape, w.context_lens, n_dec, args.schedule)
+        fp8 = args.kv == "fp8"
+        if fp8:
+            # The decode requests' cache as E4M3 pages, written by the fp8 writer
+            # from their bf16 tokens (untimed); one scale per KV head from the
+            # absolute maximum of those tokens.
+            shape8 = A.make_shape(w.hq, w.hkv, w.d, "fp8", w.scale)
+            cl = w.context_lens.astype(np.int64)
+            r_idx = np.repeat(np.arange(n_dec), cl)
+            j = np.arange(int(cl.sum())) - np.repeat(np.cumsum(cl) - cl, cl)
+            pg = torch.from_numpy(w.page_table[r_idx, j // 16].astype(np.int64)).to(dev)
+            sl = torch.from_numpy((j % 16).astype(np.int64)).to(dev)
+            ktok = kp[pg, :, sl, :].contiguous()
+            vtok = vp[pg, :, :, sl].contiguous()
+            ks_h, vs_h = e4m3_head_scales(A.to_host(ktok)), e4m3_head_scales(A.to_host(vtok))
+            ks, vs = A.to_device(ks_h), A.to_device(vs_h)
+            kp = torch.full((w.num_pages, w.hkv, 16, w.d), 0x7F, dtype=torch.uint8, device=dev)
+            vp = torch.full((w.num_pages, w.hkv, w.d, 16), 0x7F, dtype=torch.uint8, device=dev)
+            A.dopd_kv_write_fp8(shape8, ktok, vtok, ks, vs, kp, vp, w.num_pages, pt[:n_dec],
+                                stride, A.to_device(I.cu_from_lens(w.context_lens)),
+                                torch.zeros(n_dec, dtype=torch.int32, device=dev), n_dec,
+                                int(cl.sum()), sA)
+            torch.cuda.synchronize()
+            del ktok, vtok
+            out_h = torch.empty(int(offs_np[-1]), dtype=torch.uint8, device=dev)
 
-        def step():
-            A.dopd_pd_step(shape, q_dec, pt[:n_dec], ctx, w.context_lens, n_dec, out_d, None, q,
-                           k, v, cu, w.cu_seqlens, n_pre, pt[n_dec:], out_p, None, kp, vp,
-                           w.num_pages, stride, offs, out_h, args.schedule, ws, stream=sA)
+            def step():
+                A.dopd_pd_step_fp8(shape8, q_dec, pt[:n_dec], ctx, w.context_lens, n_dec, out_d,
+                                   None, q, k, v, cu, w.cu_seqlens, n_pre, pt[n_dec:], out_p,
+                                   None, kp, vp, ks, vs, w.num_pages, stride, offs, out_h,
+                                   args.schedule, ws, stream=sA)
+        else:
+            def step():
+                A.dopd_pd_step(shape, q_dec, pt[:n_dec], ctx, w.context_lens, n_dec, out_d,
+                               None, q, k, v, cu, w.cu_seqlens, n_pre, pt[n_dec:], out_p, None,
+                               kp, vp, w.num_pages, stride, offs, out_h, args.schedule, ws,
+                               stream=sA)
 
         work = {"pd_step": ("step", None)}
 
         def cpu():
             import oracle
-            ref, _ = oracle.decode(w.q_dec, w.k_pool, w.v_pool, w.page_table[:n_dec],
-                                   w.context_lens, w.scale)
+            if fp8:
+                # the oracle quantises the same bf16 cache and prompts with the
+                # same scales, and decodes / writes / packs the codes
+                P, hkv, d = w.num_pages, w.hkv, w.d
+                kq = oracle.e4m3_quantize(w.k_pool.transpose(0, 2, 1, 3).reshape(-1, hkv, d), ks_h)
+                vq = oracle.e4m3_quantize(w.v_pool.transpose(0, 3, 1, 2).reshape(-1, hkv, d), vs_h)
+                k0 = kq.reshape(P, 16, hkv, d).transpose(0, 2, 1, 3).copy()
+                v0 = vq.reshape(P, 16, hkv, d).transpose(0, 2, 3, 1).copy()
+                ref, _ = oracle.decode_e4m3(w.q_dec, k0, v0, ks_h, vs_h, w.page_table[:n_dec],
+                                            w.context_lens, w.scale)
+                knew, vnew = oracle.e4m3_quantize(w.k, ks_h), oracle.e4m3_quantize(w.v, vs_h)
+            else:
+                k0, v0, knew, vnew = w.k_pool, w.v_pool, w.k, w.v
+                ref, _ = oracle.decode(w.q_dec, w.k_pool, w.v_pool, w.page_table[:n_dec],
+                                       w.context_lens, w.scale)
             ref_p, _ = oracle.prefill(w.q, w.k, w.v, w.cu_seqlens, w.scale)
-            rk, rv = oracle.kv_write(w.k, w.v, w.k_pool, w.v_pool, w.page_table[n_dec:],
-                                     w.cu_seqlens, np.zeros(n_pre, np.int32))
+            rk, rv = oracle.kv_write(knew, vnew, k0, v0, w.page_table[n_dec:], w.cu_seqlens,
+                                     np.zeros(n_pre, np.int32))
             ref_h = oracle.pack(rk, rv, 1, w.page_table[n_dec:],
                                 np.arange(n_pre, dtype=np.int32), w.prefill_lens, offs_np)
             return None, {"decode": err_block(widen(out_d), ref),
@@ -500,7 +544,8 @@ def build_workload(name, args, torch, A, I, sA):
                           "pack_bit_exact": bool(np.array_equal(A.to_host(out_h), ref_h))}
 
         return Workload(name, desc, w.seed, [("pd_step", step)], work, "pd_step", cpu,
-                        extra={"schedule": args.schedule})
+                        label=name + ("_fp8" if fp8 else ""),
+                        extra={"schedule": args.schedule, "kv": args.kv})
 
     if name == "write_pack":
         n_pre, n_dec = len(w.prefill_lens), len(w.context_lens)
@@ -924,7 +969,7 @@ def main():
                     help="KV cache element type (fp8 = E4M3 pages with per-KV-head scales): "
                          "decode workloads read it (written by the fp8 writer before timing), "
                          "the prefill workload writes it, the chunked workload writes it "
-                         "and its chunk calls read it")
+                         "and its chunk calls read it, the fused step reads and writes it")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calib-mib", type=int, default=0,
                     help="after timing, run one elementwise kernel over this many MiB "
@@ -945,8 +990,9 @@ def main():
         return
 
     if args.kv == "fp8" and args.workload not in ("decode_mha", "decode_gqa", "prefill",
-                                                  "chunked"):
-        print("--kv fp8 applies to the decode_mha, decode_gqa, prefill and chunked workloads",
+                                                  "chunked", "pd_step"):
+        print("--kv fp8 applies to the decode_mha, decode_gqa, prefill, chunked and pd_step "
+              "workloads",
               file=sys.stderr)
         sys.exit(2)
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:

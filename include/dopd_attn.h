@@ -32,8 +32,9 @@
  *   it gives no scaling rule, so the per-head scale is this library's.  It
  *   halves the bytes decode and handoff move.  Entry points that take it:
  *   dopd_kv_write_fp8, dopd_decode_attn_fp8, dopd_decode_workspace_size,
- *   dopd_prefill_paged_attn_fp8 with its workspace size, and the handoff
- *   pack/unpack (byte copies); the others return DOPD_ERR_UNSUPPORTED for it.
+ *   dopd_prefill_paged_attn_fp8 with its workspace size, dopd_pd_step_fp8
+ *   with dopd_pd_step_workspace_size, and the handoff pack/unpack (byte
+ *   copies); the others return DOPD_ERR_UNSUPPORTED for it.
  * - Fresh tokens are token-major: Q/out [T][Hq][d], K/V [T][Hkv][d].
  * - GQA: query head h uses KV head h / (Hq / Hkv); Hq % Hkv must be 0.
  * - Paged cache (one pool per layer, page_size = 16 tokens):
@@ -420,7 +421,7 @@ enum {
  *   schedule: DOPD_PD_* block order.
  *   workspace: dopd_pd_step_workspace_size() bytes (decode partials),
  *     256-byte aligned, any contents.
- * bf16 only.  Either batch may be empty.
+ * bf16 pools (dopd_pd_step_fp8: E4M3 pools).  Either batch may be empty.
  */
 dopd_status dopd_pd_step(const dopd_attn_shape* shape, const void* q_dec,
                          const int32_t* dec_page_table, const int32_t* context_lens,
@@ -433,8 +434,37 @@ dopd_status dopd_pd_step(const dopd_attn_shape* shape, const void* q_dec,
                          void* handoff_out, int32_t schedule, void* workspace,
                          size_t workspace_bytes, void* stream);
 
-/* Workspace bytes dopd_pd_step needs for this decode batch and schedule on
- * the current device (at least 256; 0 on bad input).
+/*
+ * The same PD-aggregated step over E4M3 pools.
+ * Paper: PD-aggregation on a D-instance (Sec. V-E) serving the FP8 models of
+ * Sec. VI-A, whose KV blocks are FP8; Eq. 1 for both kinds of work.
+ * shape->dtype = DOPD_FP8_E4M3; k_scale/v_scale: fp32 device arrays [Hkv]
+ * (positive and finite, not checked on the device).  Same results as, in one
+ * stream order,
+ *   dopd_decode_attn_fp8(q_dec, k_pool, v_pool, k_scale, v_scale ...)
+ *   dopd_prefill_attn(q, k, v ...)   (the fresh rows stay bf16)
+ *   the E4M3 paged write of k, v (dopd_kv_write_fp8's codes) and, with
+ *   handoff_out, the pack of those codes (dopd_kv_pack_for_handoff over the
+ *   E4M3 pools: one byte per element, handoff_offsets in elements = bytes)
+ * up to the rounding of a different decode split.  Other arguments, the
+ * block orders, the workspace (dopd_pd_step_workspace_size with the E4M3
+ * shape) and the disjoint-pages rule as for dopd_pd_step.
+ */
+dopd_status dopd_pd_step_fp8(const dopd_attn_shape* shape, const void* q_dec,
+                             const int32_t* dec_page_table, const int32_t* context_lens,
+                             const int32_t* context_lens_host, int32_t num_dec, void* out_dec,
+                             float* lse_dec, const void* q, const void* k, const void* v,
+                             const int32_t* cu_seqlens, const int32_t* cu_seqlens_host,
+                             int32_t num_pre, const int32_t* pre_page_table, void* out_pre,
+                             float* lse_pre, void* k_pool, void* v_pool, const float* k_scale,
+                             const float* v_scale, int32_t num_pages, int32_t page_table_stride,
+                             const int64_t* handoff_offsets, void* handoff_out,
+                             int32_t schedule, void* workspace, size_t workspace_bytes,
+                             void* stream);
+
+/* Workspace bytes dopd_pd_step (bf16 shape) or dopd_pd_step_fp8 (E4M3 shape)
+ * needs for this decode batch and schedule on the current device (at least
+ * 256; 0 on bad input).
  * Paper: as dopd_pd_step (Sec. V-E, Sec. III-A; the split-K partials of the
  * decode are an exact rewrite of the softmax of Eq. 1). */
 size_t dopd_pd_step_workspace_size(const dopd_attn_shape* shape,

@@ -32,7 +32,8 @@ EXPORTS = (
     "dopd_decode_attn", "dopd_decode_attn_fp8", "dopd_decode_workspace_size",
     "dopd_decode_attn_noalloc",
     "dopd_kv_pack_for_handoff", "dopd_kv_unpack_from_handoff", "dopd_validate_page_table_host",
-    "dopd_kv_write_pack_for_handoff", "dopd_pd_step", "dopd_pd_step_workspace_size",
+    "dopd_kv_write_pack_for_handoff", "dopd_pd_step", "dopd_pd_step_fp8",
+    "dopd_pd_step_workspace_size",
     "dopd_status_string",
     "dopd_last_hip_error",
 )
@@ -104,6 +105,8 @@ def lib():
                                                      P, P]
         L.dopd_pd_step.argtypes = [SP, P, P, P, P, i32, P, P, P, P, P, P, P, i32, P, P, P, P, P,
                                    i32, i32, P, P, i32, P, sz, P]
+        L.dopd_pd_step_fp8.argtypes = [SP, P, P, P, P, i32, P, P, P, P, P, P, P, i32, P, P, P,
+                                       P, P, P, P, i32, i32, P, P, i32, P, sz, P]
         L.dopd_pd_step_workspace_size.argtypes = [SP, P, i32, i32]
         L.dopd_pd_step_workspace_size.restype = sz
         L.dopd_status_string.argtypes = [i32]
@@ -115,7 +118,7 @@ def lib():
                   "dopd_decode_attn_noalloc",
                   "dopd_kv_pack_for_handoff", "dopd_kv_unpack_from_handoff",
                   "dopd_validate_page_table_host", "dopd_kv_write_pack_for_handoff",
-                  "dopd_pd_step"):
+                  "dopd_pd_step", "dopd_pd_step_fp8"):
             getattr(L, f).restype = i32
         _LIB = L
     return _LIB
@@ -354,6 +357,25 @@ def dopd_pd_step(shape, q_dec, dec_page_table, context_lens, context_lens_host, 
         _dptr(lse_pre), _dptr(k_pool), _dptr(v_pool), int(num_pages), int(page_table_stride),
         _dptr(handoff_offsets), _dptr(handoff_out), int(schedule), _dptr(workspace),
         int(workspace_bytes), _stream(stream)), "dopd_pd_step")
+
+
+def dopd_pd_step_fp8(shape, q_dec, dec_page_table, context_lens, context_lens_host, num_dec,
+                     out_dec, lse_dec, q, k, v, cu_seqlens, cu_seqlens_host, num_pre,
+                     pre_page_table, out_pre, lse_pre, k_pool, v_pool, k_scale, v_scale,
+                     num_pages, page_table_stride, handoff_offsets, handoff_out, schedule,
+                     workspace, workspace_bytes=None, stream=None):
+    ctx = _host_i32(context_lens_host)
+    cu_h = _host_i32(cu_seqlens_host)
+    if workspace_bytes is None:
+        workspace_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check(lib().dopd_pd_step_fp8(
+        C.byref(shape), _dptr(q_dec), _dptr(dec_page_table), _dptr(context_lens), _hptr(ctx),
+        int(num_dec), _dptr(out_dec), _dptr(lse_dec), _dptr(q), _dptr(k), _dptr(v),
+        _dptr(cu_seqlens), _hptr(cu_h), int(num_pre), _dptr(pre_page_table), _dptr(out_pre),
+        _dptr(lse_pre), _dptr(k_pool), _dptr(v_pool), _dptr(k_scale), _dptr(v_scale),
+        int(num_pages), int(page_table_stride), _dptr(handoff_offsets), _dptr(handoff_out),
+        int(schedule), _dptr(workspace), int(workspace_bytes), _stream(stream)),
+        "dopd_pd_step_fp8")
 
 
 def pd_step_workspace(shape, context_lens_host, num_dec, schedule=DOPD_PD_AUTO, device="cuda"):

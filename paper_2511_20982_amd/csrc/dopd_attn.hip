@@ -739,6 +739,8 @@ dopd::WritePackArgs write_pack_args(const void* k_new, const void* v_new, void* 
   w.hkv = hkv;
   w.out = (uint16_t*)out;
   w.out_off = out_offsets;
+  w.k_scale = nullptr;
+  w.v_scale = nullptr;
   return w;
 }
 
@@ -796,25 +798,30 @@ int pd_decode_quarters(int schedule) {
 size_t dopd_pd_step_workspace_size(const dopd_attn_shape* s, const int32_t* ctx_host,
                                    int32_t num_dec, int32_t schedule) {
   if (check_decode_host(s, ctx_host, num_dec, 0) != DOPD_OK) return 0;
-  if (s->dtype != DOPD_BF16 || schedule < DOPD_PD_AUTO || schedule > kPdLastSchedule) return 0;
+  if ((s->dtype != DOPD_BF16 && s->dtype != DOPD_FP8_E4M3) || schedule < DOPD_PD_AUTO ||
+      schedule > kPdLastSchedule)
+    return 0;
   if (num_dec == 0) return 256;
   return dopd::decode_layout(s->num_q_heads / s->num_kv_heads, s->num_kv_heads, s->head_dim,
                              ctx_host, num_dec, 0, machine_shape(), pd_decode_quarters(schedule))
       .total;
 }
 
-dopd_status dopd_pd_step(const dopd_attn_shape* s, const void* q_dec,
-                         const int32_t* dec_page_table, const int32_t* ctx,
-                         const int32_t* ctx_host, int32_t num_dec, void* out_dec,
-                         float* lse_dec, const void* q, const void* k, const void* v,
-                         const int32_t* cu, const int32_t* cu_host, int32_t num_pre,
-                         const int32_t* pre_page_table, void* out_pre, float* lse_pre,
-                         void* k_pool, void* v_pool, int32_t num_pages, int32_t pt_stride,
-                         const int64_t* handoff_offsets, void* handoff_out, int32_t schedule,
-                         void* workspace, size_t workspace_bytes, void* stream) {
+// dopd_pd_step(_fp8): bf16 pools, or (kv8) E4M3 pools with per-head scales.
+static dopd_status pd_step_impl(const dopd_attn_shape* s, const void* q_dec,
+                                const int32_t* dec_page_table, const int32_t* ctx,
+                                const int32_t* ctx_host, int32_t num_dec, void* out_dec,
+                                float* lse_dec, const void* q, const void* k, const void* v,
+                                const int32_t* cu, const int32_t* cu_host, int32_t num_pre,
+                                const int32_t* pre_page_table, void* out_pre, float* lse_pre,
+                                void* k_pool, void* v_pool, int32_t num_pages, int32_t pt_stride,
+                                const int64_t* handoff_offsets, void* handoff_out,
+                                int32_t schedule, void* workspace, size_t workspace_bytes,
+                                void* stream, bool kv8, const float* k_scale,
+                                const float* v_scale) {
   dopd_status st = check_decode_host(s, ctx_host, num_dec, 0);
   if (st != DOPD_OK) return st;
-  if (s->dtype != DOPD_BF16) return DOPD_ERR_UNSUPPORTED;
+  if (s->dtype != (kv8 ? DOPD_FP8_E4M3 : DOPD_BF16)) return DOPD_ERR_UNSUPPORTED;
   if (schedule < DOPD_PD_AUTO || schedule > kPdLastSchedule || num_pre < 0 ||
       num_pages < 0 || pt_stride < 0)
     return DOPD_ERR_INVALID_SHAPE;
@@ -824,6 +831,7 @@ dopd_status dopd_pd_step(const dopd_attn_shape* s, const void* q_dec,
   if (num_pre > 0 && (!q || !k || !v || !cu || !cu_host || !pre_page_table || !out_pre))
     return DOPD_ERR_NULL_POINTER;
   if ((handoff_out == nullptr) != (handoff_offsets == nullptr)) return DOPD_ERR_NULL_POINTER;
+  if (kv8 && (!k_scale || !v_scale)) return DOPD_ERR_NULL_POINTER;
   for (int32_t r = 0; r < num_dec; ++r)
     if ((int64_t)(ctx_host[r] + dopd::kPage - 1) / dopd::kPage > pt_stride)
       return DOPD_ERR_INVALID_SHAPE;
@@ -838,22 +846,30 @@ dopd_status dopd_pd_step(const dopd_attn_shape* s, const void* q_dec,
   std::memset(&p, 0, sizeof(p));
   bool merge = false;
   if (num_dec > 0) {
-    st = plan_decode_bf16<false>(s, q_dec, k_pool, v_pool, nullptr, nullptr, dec_page_table,
-                                 pt_stride, ctx, ctx_host, num_dec, 0, out_dec, lse_dec,
-                                 workspace, workspace_bytes, pd_decode_quarters(schedule),
-                                 &p.dec, &merge);
+    st = kv8 ? plan_decode_bf16<true>(s, q_dec, k_pool, v_pool, k_scale, v_scale, dec_page_table,
+                                      pt_stride, ctx, ctx_host, num_dec, 0, out_dec, lse_dec,
+                                      workspace, workspace_bytes, pd_decode_quarters(schedule),
+                                      &p.dec, &merge)
+             : plan_decode_bf16<false>(s, q_dec, k_pool, v_pool, nullptr, nullptr, dec_page_table,
+                                       pt_stride, ctx, ctx_host, num_dec, 0, out_dec, lse_dec,
+                                       workspace, workspace_bytes, pd_decode_quarters(schedule),
+                                       &p.dec, &merge);
     if (st != DOPD_OK) return st;
     p.n_dec = p.dec.nwg;
   }
   int64_t pf_blocks = 0;
   if (num_pre > 0 && cu_host[num_pre] > 0) {
-    p.pf = prefill_args(s, q, out_pre, lse_pre, cu);
+    dopd_attn_shape sb = *s;  // the prefill reads the bf16 fresh rows
+    sb.dtype = DOPD_BF16;
+    p.pf = prefill_args(&sb, q, out_pre, lse_pre, cu);
     p.pf.k = (const uint16_t*)k;
     p.pf.v = (const uint16_t*)v;
     st = plan_prefill_bf16<false>(p.pf, cu_host, nullptr, num_pre, &pf_blocks);
     if (st != DOPD_OK) return st;
     p.wp = write_pack_args(k, v, k_pool, v_pool, pre_page_table, pt_stride, cu, num_pre, hkv,
                            handoff_offsets, handoff_out);
+    p.wp.k_scale = k_scale;
+    p.wp.v_scale = v_scale;
   }
   p.n_pf = (int)pf_blocks;
   if (pages * hkv > INT32_MAX / 4) return DOPD_ERR_INVALID_SHAPE;
@@ -877,13 +893,48 @@ dopd_status dopd_pd_step(const dopd_attn_shape* s, const void* q_dec,
   if (total > INT32_MAX / 2) return DOPD_ERR_INVALID_SHAPE;
   if (total == 0) return DOPD_OK;
   hipStream_t strm = as_stream(stream);
-  if (d == 64)
-    hipLaunchKernelGGL(dopd::pd_step_kernel<64>, dim3((unsigned)total), dim3(dopd::kPfThreads), 0, strm, p);
-  else
-    hipLaunchKernelGGL(dopd::pd_step_kernel<128>, dim3((unsigned)total), dim3(dopd::kPfThreads), 0, strm, p);
+  const dim3 grid((unsigned)total), block(dopd::kPfThreads);
+  if (kv8) {
+    if (d == 64) hipLaunchKernelGGL((dopd::pd_step_kernel<64, true>), grid, block, 0, strm, p);
+    else hipLaunchKernelGGL((dopd::pd_step_kernel<128, true>), grid, block, 0, strm, p);
+  } else {
+    if (d == 64) hipLaunchKernelGGL((dopd::pd_step_kernel<64, false>), grid, block, 0, strm, p);
+    else hipLaunchKernelGGL((dopd::pd_step_kernel<128, false>), grid, block, 0, strm, p);
+  }
   st = launch_status();
   if (st != DOPD_OK || !merge) return st;
   return launch_decode_merge(p.dec, d, strm);
+}
+
+dopd_status dopd_pd_step(const dopd_attn_shape* s, const void* q_dec,
+                         const int32_t* dec_page_table, const int32_t* ctx,
+                         const int32_t* ctx_host, int32_t num_dec, void* out_dec,
+                         float* lse_dec, const void* q, const void* k, const void* v,
+                         const int32_t* cu, const int32_t* cu_host, int32_t num_pre,
+                         const int32_t* pre_page_table, void* out_pre, float* lse_pre,
+                         void* k_pool, void* v_pool, int32_t num_pages, int32_t pt_stride,
+                         const int64_t* handoff_offsets, void* handoff_out, int32_t schedule,
+                         void* workspace, size_t workspace_bytes, void* stream) {
+  return pd_step_impl(s, q_dec, dec_page_table, ctx, ctx_host, num_dec, out_dec, lse_dec, q, k, v,
+                      cu, cu_host, num_pre, pre_page_table, out_pre, lse_pre, k_pool, v_pool,
+                      num_pages, pt_stride, handoff_offsets, handoff_out, schedule, workspace,
+                      workspace_bytes, stream, false, nullptr, nullptr);
+}
+
+dopd_status dopd_pd_step_fp8(const dopd_attn_shape* s, const void* q_dec,
+                             const int32_t* dec_page_table, const int32_t* ctx,
+                             const int32_t* ctx_host, int32_t num_dec, void* out_dec,
+                             float* lse_dec, const void* q, const void* k, const void* v,
+                             const int32_t* cu, const int32_t* cu_host, int32_t num_pre,
+                             const int32_t* pre_page_table, void* out_pre, float* lse_pre,
+                             void* k_pool, void* v_pool, const float* k_scale,
+                             const float* v_scale, int32_t num_pages, int32_t pt_stride,
+                             const int64_t* handoff_offsets, void* handoff_out, int32_t schedule,
+                             void* workspace, size_t workspace_bytes, void* stream) {
+  return pd_step_impl(s, q_dec, dec_page_table, ctx, ctx_host, num_dec, out_dec, lse_dec, q, k, v,
+                      cu, cu_host, num_pre, pre_page_table, out_pre, lse_pre, k_pool, v_pool,
+                      num_pages, pt_stride, handoff_offsets, handoff_out, schedule, workspace,
+                      workspace_bytes, stream, true, k_scale, v_scale);
 }
 
 // ---------------------------------------------------------------- handoff pack

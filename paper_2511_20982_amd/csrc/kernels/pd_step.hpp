@@ -10,6 +10,9 @@
 //                       kernel; pf_first is a multiple of the XCD count so a
 //                       block's XCD is the one the order assumes)
 //   [dec_first, + n_dec) decode slices (the decode partition's workgroups)
+// KV8: the decode reads E4M3 pages and the write + pack quantises the fresh
+// rows to E4M3 codes with one scale per KV head (the prefill reads the bf16
+// fresh rows either way).
 // The three kinds touch disjoint memory: the decode reads the pages of the
 // decode requests, the write fills the pages of the prompts, the prefill
 // reads only the fresh rows.  The decode's split-K partials are merged by the
@@ -33,7 +36,7 @@ struct PdStepArgs {
   int dec_first, n_dec;  // decode blocks (n_dec = dec.nwg)
 };
 
-template <int D>
+template <int D, bool KV8 = false>
 __global__ __launch_bounds__(kPfThreads, 2) void pd_step_kernel(PdStepArgs s) {
   __shared__ __attribute__((aligned(16))) uint16_t sK0[pf_tile_elems<D>()], sK1[pf_tile_elems<D>()];
   __shared__ __attribute__((aligned(16))) uint16_t sV0[pf_tile_elems<D>()], sV1[pf_tile_elems<D>()];
@@ -47,13 +50,16 @@ __global__ __launch_bounds__(kPfThreads, 2) void pd_step_kernel(PdStepArgs s) {
     prefill_workgroup<D, false>(s.pf, b - s.pf_first, sK0, sK1, sV0, sV1, sQ);
   } else if (b >= s.dec_first && b < s.dec_first + s.n_dec) {
     constexpr int kWaveElems = dec_wave_o_bytes<D>() / 2;  // bf16 elements of one block
-    decode_workgroup<D, false>(s.dec, b - s.dec_first, reinterpret_cast<float*>(sQ),
+    decode_workgroup<D, KV8>(s.dec, b - s.dec_first, reinterpret_cast<float*>(sQ),
                                reinterpret_cast<f32x4*>(sK0),
                                reinterpret_cast<f32x4*>(sK0 + kWaveElems),
                                reinterpret_cast<f32x4*>(sK1));
   } else if (b >= s.wp_first && b < s.wp_first + s.n_wp) {
     const int j = b - s.wp_first;
-    kv_write_pack_workgroup<D>(s.wp, j / s.wp.hkv, j % s.wp.hkv, sV0);
+    if constexpr (KV8)
+      kv_write_pack_e4m3_workgroup<D>(s.wp, j / s.wp.hkv, j % s.wp.hkv, reinterpret_cast<uint8_t*>(sV0));
+    else
+      kv_write_pack_workgroup<D>(s.wp, j / s.wp.hkv, j % s.wp.hkv, sV0);
   }
 }
 

@@ -385,3 +385,28 @@ def test_pd_step_host_validation(lib):
     assert lib.dopd_pd_step(C.byref(s), None, None, None, None, 0, None, None, None, None, None,
                             None, None, 0, None, None, None, None, None, 0, 0, None, None, 0,
                             None, 0, None) == A.DOPD_OK
+
+
+
+def _pd8(lib, shape, ctx, cu, scales=FAKE, ws=FAKE, ws_bytes=1 << 30):
+    ctx = np.asarray(ctx, np.int32)
+    cu = np.asarray(cu, np.int32)
+    p = C.c_void_p(FAKE)
+    sc = C.c_void_p(scales) if scales else None
+    return lib.dopd_pd_step_fp8(
+        C.byref(shape), p, p, p, A._hptr(ctx), len(ctx), p, None, p, p, p, p, A._hptr(cu),
+        len(cu) - 1, p, p, None, p, p, sc, sc, 100, 1024, p, p, 0,
+        C.c_void_p(ws) if ws else None, ws_bytes, None)
+
+
+def test_pd_step_fp8_host_validation(lib):
+    s8 = _shape(hq=28, hkv=4, dtype="fp8")
+    assert _pd8(lib, _shape(hq=28, hkv=4), [5], [0, 4]) == A.DOPD_ERR_UNSUPPORTED  # bf16 shape
+    assert _pd(lib, s8, [5], [0, 4]) == A.DOPD_ERR_UNSUPPORTED   # E4M3 shape, bf16 entry
+    assert _pd8(lib, s8, [5], [0, 4], scales=0) == A.DOPD_ERR_NULL_POINTER
+    assert _pd8(lib, s8, [5, 0], [0, 4]) == A.DOPD_ERR_INVALID_SHAPE
+    assert _pd8(lib, s8, [5], [0, 4], ws=0) == A.DOPD_ERR_NULL_POINTER
+    need = A.dopd_pd_step_workspace_size(s8, [3000, 17], 2, A.DOPD_PD_AUTO)
+    assert need == A.dopd_pd_step_workspace_size(_shape(hq=28, hkv=4), [3000, 17], 2,
+                                                 A.DOPD_PD_AUTO)
+    assert _pd8(lib, s8, [3000, 17], [0, 4], ws_bytes=need - 1) == A.DOPD_ERR_WORKSPACE_TOO_SMALL
