@@ -143,6 +143,22 @@ def e4m3_head_scales(x) -> np.ndarray:
     return (a / np.float32(448)).astype(np.float32)
 
 
+def json_safe(x):
+    """The record with non-finite floats as null (strict JSON)."""
+    if isinstance(x, dict):
+        return {k: json_safe(v) for k, v in x.items()}
+    if isinstance(x, (list, tuple)):
+        return [json_safe(v) for v in x]
+    if isinstance(x, float) and not np.isfinite(x):
+        return None
+    return x
+
+
+def mean_or_none(xs):
+    """Mean of a list of times in us (None when empty: no back-to-back steps)."""
+    return round(float(np.mean(xs)), 2) if len(xs) else None
+
+
 def source_hash() -> str:
     import hashlib
     h = hashlib.sha256()
@@ -912,7 +928,7 @@ def run_workload(wl, args, torch, sA, flush, steps, warmup, reps):
         if amount is None:  # a whole step: times only
             calls[name] = {"unit": unit, "cold_us": stats_us(cold[name]),
                            "warm_us": stats_us(warm[name]),
-                           "step_mean_us": round(float(np.mean(step_us[name])), 2)}
+                           "step_mean_us": mean_or_none(step_us[name])}
             continue
         scale = 1e12 if unit == "TFLOP/s" else 1e9
         peak = BF16_PEAK_TFLOPS if unit == "TFLOP/s" else HBM_PEAK_GBS
@@ -923,7 +939,7 @@ def run_workload(wl, args, torch, sA, flush, steps, warmup, reps):
                "frac": round(amount / (c["median"] * 1e-6) / scale / peak, 4),
                "warm_rate": round(amount / (wm["median"] * 1e-6) / scale, 2),
                "warm_frac": round(amount / (wm["median"] * 1e-6) / scale / peak, 4),
-               "step_mean_us": round(float(np.mean(step_us[name])), 2)}
+               "step_mean_us": mean_or_none(step_us[name])}
         kt = ktimes.get(name)
         if kt:  # rocprofv3 kernel time (no event or launch overhead)
             rec["kernel_us_rocprof"] = kt["avg_us"]
@@ -1053,7 +1069,7 @@ def main():
                            "schedule": head.get("schedule")},
                 "calls": head["calls"], "parity": head.get("parity"),
                 "device": {"name": props.name, "cus": props.multi_processor_count}}
-        print(json.dumps(line), flush=True)
+        print(json.dumps(json_safe(line), allow_nan=False), flush=True)
         return
     roofline = {"kernel": head["dominant"], "kernels": list(CALL_KERNELS[head["dominant"]]),
                 "bound": "mfma" if unit == "TFLOP/s" else "hbm",
@@ -1094,7 +1110,7 @@ def main():
         "flush": "write 1 GiB, then read another 1 GiB, before every cold rep",
         "input_gen_s": round(gen_s, 1),
     }
-    print(json.dumps(line), flush=True)
+    print(json.dumps(json_safe(line), allow_nan=False), flush=True)
 
 
 def wl_desc(args):
