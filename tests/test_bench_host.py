@@ -99,3 +99,13 @@ def test_repeat_timed_covers_the_requested_time():
     assert res == 1 and n == len(calls) and n >= 2 and dt >= 0.05
     res, n, _ = B.repeat_timed(lambda: 7, 0.0)
     assert res == 7 and n == 1
+
+
+def test_bench_line_is_strict_json():
+    import json
+    line = {"value": 1.5, "calls": {"a": {"step_mean_us": B.mean_or_none([])}},
+            "parity": [float("nan"), float("inf"), 2.0]}
+    text = json.dumps(B.json_safe(line), allow_nan=False)
+    assert json.loads(text) == {"value": 1.5, "calls": {"a": {"step_mean_us": None}},
+                                "parity": [None, None, 2.0]}
+    assert B.mean_or_none([1.0, 2.0]) == 1.5
