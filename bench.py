@@ -73,28 +73,30 @@ CALL_KERNELS = {"decode": ("decode_split_kernel", "decode_merge_kernel"),
 
 WORKLOADS = {
     "mixed": ("mixed P/D step + handoff: prefill 8x512, decode 192 req ctx lognormal(2048,0.7) "
-              "[64,16384], 28/4 heads, d128, bf16, pack 8 req x 1 layer", 5),
+              "[64,16384], 28/4 heads, d128, bf16, pack 8 req x 1 layer", "mixed_step"),
     "decode_mha": ("decode, MHA 7B-shaped: B64, 32 heads, d128, bf16, ctx lognormal(1024,0.8) "
-                   "[16,4096]", 2),
+                   "[16,4096]", "decode_mha_7b"),
     "prefill": ("varlen causal prefill + paged write: 16 prompts lognormal(1500,1.0) [32,8192], "
-                "32/32 heads, d128, bf16", 3),
+                "32/32 heads, d128, bf16", "varlen_prefill"),
     "decode_gqa": ("decode, GQA 70B-shaped: B256, 64/8 heads, d128, bf16, ctx 80% U[100,500] + "
-                   "20% U[4096,16384]", 4),
+                   "20% U[4096,16384]", "decode_gqa_70b"),
     "chunked": ("chunked prefill over the paged cache: the 16 prompts of the varlen prefill "
                 "workload (lognormal(1500,1.0) [32,8192], 32/32 heads, d128, bf16) in chunks of "
                 "--chunk tokens, calls filled to --budget tokens, each chunk attending to its "
                 "cached prefix; --kv fp8: the prompts written to an E4M3 cache and the chunks "
-                "read from it", 3),
+                "read from it", "varlen_prefill"),
     "pd_step": ("the mixed P/D step + handoff of the mixed workload as one PD-aggregated launch "
                 "(dopd_pd_step: decode slices, prefill items and write+pack workgroups in one "
-                "grid, then the decode merge); --kv fp8: over E4M3 pages (dopd_pd_step_fp8)", 5),
+                "grid, then the decode merge); --kv fp8: over E4M3 pages (dopd_pd_step_fp8)",
+                "mixed_step"),
     "write_pack": ("paged write + handoff pack of the mixed step's 8 x 512 fresh prompts (28/4 "
                    "heads, d128, bf16, 1 layer): the separate write and pack calls, then the "
                    "one-pass write+pack (dopd_kv_write_pack_for_handoff), and a plain "
-                   "elementwise kernel moving the pack's bytes (the floor at this size)", 5),
+                   "elementwise kernel moving the pack's bytes (the floor at this size)",
+                   "mixed_step"),
     "handoff": ("P->D handoff on one GPU: pack 8 prefilled requests x 512 tokens from the P pool, "
                 "unpack into a D pool with another page order; 28/4 heads, d128, bf16, "
-                "--pack-layers layers", 5),
+                "--pack-layers layers", "mixed_step"),
 }
 
 
@@ -376,10 +378,10 @@ class Workload:
 
 def build_workload(name, args, torch, A, I, sA):
     """Allocates and fills the device inputs of workload `name` (untimed)."""
-    desc, cfg = WORKLOADS[name]
+    desc, inputs = WORKLOADS[name]  # the inputs module's builder of its seeded inputs
     dev = "cuda"
-    w = {5: lambda: I.config5(num_layers=args.pack_layers), 2: I.config2, 3: I.config3,
-         4: I.config4}[cfg]()
+    w = (I.mixed_step(num_layers=args.pack_layers) if inputs == "mixed_step"
+         else getattr(I, inputs)())
     shape = A.make_shape(w.hq, w.hkv, w.d, w.dtype, w.scale)
     threads = int(os.environ.get("OMP_NUM_THREADS", "0")) or len(os.sched_getaffinity(0))
     os.environ.setdefault("OMP_NUM_THREADS", str(threads))

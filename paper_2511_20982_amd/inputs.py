@@ -161,7 +161,8 @@ class Workload:
     # decode batch
     context_lens: np.ndarray | None = None
     q_dec: np.ndarray | None = None
-    # config-1 style decode steps: list of (q[B][Hq][d], k[B][Hkv][d], v[B][Hkv][d])
+    # decode steps after the prefill (the tiny fp32 workload): list of
+    # (q[B][Hq][d], k[B][Hkv][d], v[B][Hkv][d])
     steps: list = field(default_factory=list)
     # handoff
     handoff_reqs: np.ndarray | None = None
@@ -222,7 +223,7 @@ def steep_score_batch(rng, lens, hq, hkv, d, pattern, rise=40.0):
             f32_to_bf16_bits(v))
 
 
-def config1(seed=SEED_BASE + 1, n_steps=8) -> Workload:
+def tiny_fp32(seed=SEED_BASE + 1, n_steps=8) -> Workload:
     """Tiny fp32 check: 4 requests {17,64,5,120}, 8/2 heads, d 64, 64-page pool,
     prefill then ``n_steps`` decode steps per request."""
     rng = np.random.default_rng(seed)
@@ -235,7 +236,7 @@ def config1(seed=SEED_BASE + 1, n_steps=8) -> Workload:
         steps.append((normal(rng, (4, hq, d), dt), normal(rng, (4, hkv, d), dt),
                       normal(rng, (4, hkv, d), dt)))
     k_pool, v_pool = empty_pools(num_pages, hkv, d, dt)
-    return Workload("config1_tiny_fp32", seed, dt, hq, hkv, d, 1.0 / math.sqrt(d),
+    return Workload("tiny_fp32_prefill_then_decode", seed, dt, hq, hkv, d, 1.0 / math.sqrt(d),
                     prefill_lens=lens, cu_seqlens=cu_from_lens(lens), q=q, k=k, v=v,
                     prefill_rows=np.arange(4, dtype=np.int32), num_pages=num_pages,
                     k_pool=k_pool, v_pool=v_pool, page_table=page_table, steps=steps)
@@ -253,16 +254,16 @@ def decode_workload(name, seed, ctx, hq, hkv, d, dtype="bf16") -> Workload:
                     context_lens=ctx, q_dec=q_dec)
 
 
-def config2(seed=SEED_BASE + 2) -> Workload:
+def decode_mha_7b(seed=SEED_BASE + 2) -> Workload:
     """Decode, MHA layer shaped like a 7B model: B 64, 32 heads, d 128, bf16,
     ctx lognormal(1024, 0.8) clipped to [16, 4096]."""
     rng = np.random.default_rng(seed)
     ctx = lognormal_lengths(rng, 64, 1024, 0.8, 16, 4096)
-    w = decode_workload("config2_decode_mha7b", seed, ctx, 32, 32, 128)
+    w = decode_workload("decode_mha_7b_b64", seed, ctx, 32, 32, 128)
     return w
 
 
-def config3(seed=SEED_BASE + 3) -> Workload:
+def varlen_prefill(seed=SEED_BASE + 3) -> Workload:
     """Varlen causal prefill + paged write: 16 prompts lognormal(1500, 1.0)
     clipped to [32, 8192], 32/32 heads, d 128, bf16."""
     rng = np.random.default_rng(seed)
@@ -272,23 +273,23 @@ def config3(seed=SEED_BASE + 3) -> Workload:
     page_table, num_pages = allocate_pages(rng, lens)
     q, k, v = prefill_batch(rng, lens, hq, hkv, d, dt)
     k_pool, v_pool = empty_pools(num_pages, hkv, d, dt)
-    return Workload("config3_prefill_write", seed, dt, hq, hkv, d, 1.0 / math.sqrt(d),
+    return Workload("varlen_prefill_16_prompts", seed, dt, hq, hkv, d, 1.0 / math.sqrt(d),
                     prefill_lens=lens, cu_seqlens=cu_from_lens(lens), q=q, k=k, v=v,
                     prefill_rows=np.arange(16, dtype=np.int32), num_pages=num_pages,
                     k_pool=k_pool, v_pool=v_pool, page_table=page_table)
 
 
-def config4(seed=SEED_BASE + 4) -> Workload:
+def decode_gqa_70b(seed=SEED_BASE + 4) -> Workload:
     """High-concurrency GQA decode, 70B-shaped: B 256, 64/8 heads, d 128, bf16;
     51 long contexts U[4096,16384] and 205 short U[100,500] at shuffled positions."""
     rng = np.random.default_rng(seed)
     ctx, is_long = bimodal_lengths(rng, 256, 0.2, 100, 500, 4096, 16384)
-    w = decode_workload("config4_decode_gqa70b", seed, ctx, 64, 8, 128)
+    w = decode_workload("decode_gqa_70b_b256", seed, ctx, 64, 8, 128)
     w.notes["n_long"] = int(is_long.sum())
     return w
 
 
-def config5(seed=SEED_BASE + 5, num_layers=1) -> Workload:
+def mixed_step(seed=SEED_BASE + 5, num_layers=1) -> Workload:
     """Mixed P/D step: 28/4 heads, d 128, bf16; prefill 8x512 writing the shared
     pool, 192 decode requests with ctx lognormal(2048, 0.7) clipped to
     [64, 16384], then the 8 prefilled requests are packed for handoff.
@@ -305,7 +306,7 @@ def config5(seed=SEED_BASE + 5, num_layers=1) -> Workload:
     q_dec = normal(rng, (n_dec, hq, d), dt)
     q, k, v = prefill_batch(rng, pre_lens, hq, hkv, d, dt)
     rows = np.arange(n_dec, n_dec + n_pre, dtype=np.int32)
-    w = Workload("config5_mixed_pd_handoff", seed, dt, hq, hkv, d, 1.0 / math.sqrt(d),
+    w = Workload("mixed_step_192_decode_8x512_prefill", seed, dt, hq, hkv, d, 1.0 / math.sqrt(d),
                  prefill_lens=pre_lens, cu_seqlens=cu_from_lens(pre_lens), q=q, k=k, v=v,
                  prefill_rows=rows, num_pages=num_pages, k_pool=k_pool, v_pool=v_pool,
                  page_table=page_table, context_lens=ctx, q_dec=q_dec,
@@ -314,7 +315,6 @@ def config5(seed=SEED_BASE + 5, num_layers=1) -> Workload:
     return w
 
 
-CONFIGS = {1: config1, 2: config2, 3: config3, 4: config4, 5: config5}
 
 
 def handoff_offsets(handoff_lens, num_layers, hkv, d) -> np.ndarray:

@@ -19,14 +19,14 @@ def _gpu(require_gpu):
 from tests import gpu_util as G  # noqa: E402
 
 
-def test_config1_tiny_fp32_prefill_then_eight_decode_steps():
-    w = I.config1()
+def test_tiny_fp32_prefill_then_eight_decode_steps():
+    w = I.tiny_fp32()
     sh = G.shape_of(w)
     n = len(w.prefill_lens)
     # prefill on the GPU vs the oracle
     ref_p, ref_lse = oracle.prefill(w.q, w.k, w.v, w.cu_seqlens, w.scale)
     out_p, lse_p = G.gpu_prefill(sh, w.q, w.k, w.v, w.cu_seqlens)
-    G.assert_attention_close(out_p, ref_p, "fp32", "config1 prefill")
+    G.assert_attention_close(out_p, ref_p, "fp32", "tiny fp32 prefill")
     assert np.max(np.abs(lse_p - ref_lse)) < 1e-5
     # the paged cache lives on the GPU for the whole sequence
     kp, vp = A.to_device(w.k_pool), A.to_device(w.v_pool)
@@ -45,31 +45,31 @@ def test_config1_tiny_fp32_prefill_then_eight_decode_steps():
         ctx = (w.prefill_lens + s + 1).astype(np.int32)
         out_d, lse_d = G.gpu_decode(sh, qd, None, None, w.page_table, ctx, pools_dev=(kp, vp))
         ref_d, ref_lse_d = oracle.decode(qd, ref_kp, ref_vp, w.page_table, ctx, w.scale)
-        G.assert_attention_close(out_d, ref_d, "fp32", f"config1 decode step {s}")
+        G.assert_attention_close(out_d, ref_d, "fp32", f"tiny fp32 decode step {s}")
         assert np.max(np.abs(lse_d - ref_lse_d)) < 1e-5
     torch.cuda.synchronize()
     assert np.array_equal(A.to_host(kp).view(np.uint32), ref_kp.view(np.uint32))
     assert np.array_equal(A.to_host(vp).view(np.uint32), ref_vp.view(np.uint32))
 
 
-@pytest.mark.parametrize("cfg", [2, 4])
-def test_full_size_decode(cfg):
-    w = I.CONFIGS[cfg]()
+@pytest.mark.parametrize("make", [I.decode_mha_7b, I.decode_gqa_70b], ids=["mha_7b", "gqa_70b"])
+def test_full_size_decode(make):
+    w = make()
     ref, ref_lse = oracle.decode(w.q_dec, w.k_pool, w.v_pool, w.page_table, w.context_lens, w.scale)
     out, lse = G.gpu_decode(G.shape_of(w), w.q_dec, w.k_pool, w.v_pool, w.page_table, w.context_lens)
-    G.assert_attention_close(out, ref, "bf16", f"config{cfg} decode")
+    G.assert_attention_close(out, ref, "bf16", f"{w.name} decode")
     assert np.max(np.abs(lse - ref_lse)) < 2e-2
 
 
-def test_full_size_prefill_and_write_config3():
+def test_full_size_varlen_prefill_and_write():
     """Every (row, head) output and lse of the varlen prefill batch (16 prompts,
     32 heads, d 128) against the oracle, and the paged write of the whole batch
     bit-exact."""
-    w = I.config3()
+    w = I.varlen_prefill()
     sh = G.shape_of(w)
     out, lse = G.gpu_prefill(sh, w.q, w.k, w.v, w.cu_seqlens)
     ref, ref_lse = oracle.prefill(w.q, w.k, w.v, w.cu_seqlens, w.scale)
-    G.assert_attention_close(out, ref, "bf16", "config3 prefill, all rows")
+    G.assert_attention_close(out, ref, "bf16", "varlen prefill, all rows")
     assert np.max(np.abs(lse - ref_lse)) < 2e-2
     del out, ref
     # paged write of the whole batch, bit-exact
@@ -81,12 +81,12 @@ def test_full_size_prefill_and_write_config3():
     assert np.array_equal(gk, ref_k) and np.array_equal(gv, ref_v)
 
 
-def test_full_size_mixed_step_one_stream_decode_first_config5():
+def test_full_size_mixed_step_one_stream_decode_first():
     """The mixed step exactly as the benchmark times it: one stream, the decode
     batch first, then prefill, paged write and pack.  Every decode and prefill
     output against the oracle (absolute and per-(row, head) normalised
     error), the write and the pack bit-exact."""
-    w = I.config5()
+    w = I.mixed_step()
     sh = G.shape_of(w)
     s = torch.cuda.current_stream()
     kp, vp = A.to_device(w.k_pool), A.to_device(w.v_pool)
@@ -113,9 +113,9 @@ def test_full_size_mixed_step_one_stream_decode_first_config5():
                                w.handoff_lens, offs_d, n_pre, out_h, s)
     torch.cuda.synchronize()
     ref_d, _ = oracle.decode(w.q_dec, w.k_pool, w.v_pool, w.page_table, w.context_lens, w.scale)
-    G.assert_attention_close(G.widen(A.to_host(out_d)), ref_d, "bf16", "config5 decode (timed order)")
+    G.assert_attention_close(G.widen(A.to_host(out_d)), ref_d, "bf16", "mixed step decode (timed order)")
     ref_p, _ = oracle.prefill(w.q, w.k, w.v, w.cu_seqlens, w.scale)
-    G.assert_attention_close(G.widen(A.to_host(out_p)), ref_p, "bf16", "config5 prefill (timed order)")
+    G.assert_attention_close(G.widen(A.to_host(out_p)), ref_p, "bf16", "mixed step prefill (timed order)")
     ref_kp, ref_vp = oracle.kv_write(w.k, w.v, w.k_pool, w.v_pool, w.page_table[n_dec:],
                                      w.cu_seqlens, np.zeros(n_pre, np.int32))
     assert np.array_equal(A.to_host(kp), ref_kp) and np.array_equal(A.to_host(vp), ref_vp)
@@ -123,10 +123,10 @@ def test_full_size_mixed_step_one_stream_decode_first_config5():
     assert np.array_equal(A.to_host(out_h), ref_h)
 
 
-def test_full_size_mixed_step_two_streams_config5():
+def test_full_size_mixed_step_two_streams():
     """The mixed step's two-stream form (the benchmark's --streams 2): prefill,
     write and pack on one stream, the decode on another, against the oracle."""
-    w = I.config5()
+    w = I.mixed_step()
     sh = G.shape_of(w)
     sA = torch.cuda.current_stream()
     sB = torch.cuda.Stream()
@@ -155,9 +155,9 @@ def test_full_size_mixed_step_two_streams_config5():
                                hlen, w.handoff_lens, offs_d, n_pre, out_h, sA)
     torch.cuda.synchronize()
     ref_d, _ = oracle.decode(w.q_dec, w.k_pool, w.v_pool, w.page_table, w.context_lens, w.scale)
-    G.assert_attention_close(G.widen(A.to_host(out_d)), ref_d, "bf16", "config5 decode")
+    G.assert_attention_close(G.widen(A.to_host(out_d)), ref_d, "bf16", "mixed step decode")
     ref_p, _ = oracle.prefill(w.q, w.k, w.v, w.cu_seqlens, w.scale)
-    G.assert_attention_close(G.widen(A.to_host(out_p)), ref_p, "bf16", "config5 prefill")
+    G.assert_attention_close(G.widen(A.to_host(out_p)), ref_p, "bf16", "mixed step prefill")
     ref_kp, ref_vp = oracle.kv_write(w.k, w.v, w.k_pool, w.v_pool, w.page_table[n_dec:],
                                      w.cu_seqlens, np.zeros(n_pre, np.int32))
     ref_h = oracle.pack(ref_kp, ref_vp, 1, w.page_table, w.handoff_reqs, w.handoff_lens, offs)
@@ -165,7 +165,7 @@ def test_full_size_mixed_step_two_streams_config5():
     assert np.array_equal(A.to_host(kp), ref_kp) and np.array_equal(A.to_host(vp), ref_vp)
 
 
-def test_pack_28_layers_config5_shape():
+def test_pack_28_layers_mixed_step_shape():
     """The supplementary 28-layer handoff of the mixed step, bit-exact."""
     rng = np.random.default_rng(5)
     layers, hkv, d = 28, 4, 128

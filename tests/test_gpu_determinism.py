@@ -29,7 +29,7 @@ def _repeat(fn, n):
 
 
 def test_prefill_full_size_bit_identical_across_runs():
-    w = I.config3()
+    w = I.varlen_prefill()
     sh = A.make_shape(w.hq, w.hkv, w.d, "bf16", w.scale)
     q, k, v, cu = A.to_device(w.q), A.to_device(w.k), A.to_device(w.v), A.to_device(w.cu_seqlens)
 
@@ -45,7 +45,7 @@ def test_prefill_full_size_bit_identical_across_runs():
 
 def test_chunk_prefill_bit_identical_across_runs():
     # whole prompts of the varlen batch read back from the paged cache
-    w = I.config3()
+    w = I.varlen_prefill()
     sh = A.make_shape(w.hq, w.hkv, w.d, "bf16", w.scale)
     n = len(w.prefill_lens)
     q, k, v, cu = A.to_device(w.q), A.to_device(w.k), A.to_device(w.v), A.to_device(w.cu_seqlens)
@@ -66,7 +66,7 @@ def test_chunk_prefill_bit_identical_across_runs():
 
 @pytest.mark.parametrize("kv", ["bf16", "fp8"])
 def test_decode_full_size_bit_identical_across_runs(kv):
-    w = I.config4()
+    w = I.decode_gqa_70b()
     n = len(w.context_lens)
     q, pt, ctx = A.to_device(w.q_dec), A.to_device(w.page_table), A.to_device(w.context_lens)
     if kv == "bf16":

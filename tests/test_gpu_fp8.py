@@ -176,7 +176,7 @@ def test_pack_unpack_fp8_bit_exact(d, layers):
 def test_decode_fp8_full_size_gqa_70b_shape():
     # The 70B-shaped GQA decode (B 256, 64/8 heads, bimodal contexts) over an
     # E4M3 cache, whole batch against the oracle.
-    w = I.config4()
+    w = I.decode_gqa_70b()
     ks, vs = _scales(w.hkv, 10)
     kq, vq = G.quantize_pools(w.k_pool, w.v_pool, ks, vs)
     ref, _ = oracle.decode_e4m3(w.q_dec, kq, vq, ks, vs, w.page_table, w.context_lens, w.scale)

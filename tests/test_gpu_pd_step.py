@@ -92,12 +92,12 @@ def _run_pd_step(w, sh, schedule, with_lse=True, handoff=True):
 
 
 @pytest.mark.parametrize("schedule", SCHEDULES)
-def test_pd_step_config5_full_size(schedule):
+def test_pd_step_mixed_step_full_size(schedule):
     """The mixed step (192 decode requests, 8 x 512 prompts, 28/4 heads, d 128)
     in one launch: every decode and prefill output against the oracle, the
     paged write and the handoff buffer bit-exact, and the prefill bit-identical
     to dopd_prefill_attn (same kernel body and work order)."""
-    w = I.config5()
+    w = I.mixed_step()
     sh = G.shape_of(w)
     n_pre, n_dec = len(w.prefill_lens), len(w.context_lens)
     r = _run_pd_step(w, sh, schedule)
@@ -120,7 +120,7 @@ def test_pd_step_config5_full_size(schedule):
 def test_pd_step_prefill_first_decode_equals_decode_entry():
     """With two decode slices per CU the step's decode partition is the one
     dopd_decode_attn uses: bit-identical outputs."""
-    w = I.config5()
+    w = I.mixed_step()
     sh = G.shape_of(w)
     n_dec = len(w.context_lens)
     r = _run_pd_step(w, sh, A.DOPD_PD_PREFILL_FIRST, with_lse=False, handoff=False)
@@ -191,7 +191,7 @@ def test_pd_step_one_batch_empty(which):
 
 
 def test_pd_step_repeat_runs_bit_identical():
-    w = I.config5()
+    w = I.mixed_step()
     sh = G.shape_of(w)
     for schedule in SCHEDULES[1:]:
         a = _run_pd_step(w, sh, schedule)

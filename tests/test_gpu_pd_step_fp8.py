@@ -97,10 +97,10 @@ def _check(c, r, hq, hkv, d, shift=0):
 
 
 @pytest.mark.parametrize("schedule", [A.DOPD_PD_AUTO, A.DOPD_PD_DECODE_FIRST])
-def test_pd_step_fp8_config5_shape(schedule):
+def test_pd_step_fp8_mixed_step_shape(schedule):
     """The mixed step's shapes (192 decode requests with contexts
     lognormal(2048, 0.7), 8 x 512 prompts, 28/4 heads, d 128) over E4M3 pools."""
-    w = I.config5()
+    w = I.mixed_step()
     n_dec = len(w.context_lens)
     c = _case(530, w.context_lens, w.prefill_lens, w.hq, w.hkv, w.d)
     r = _run(c, w.hq, w.hkv, w.d, schedule)

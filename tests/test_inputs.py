@@ -15,8 +15,8 @@ def test_bf16_rounding_is_nearest_even():
     assert I.f32_to_bf16_bits(np.array([np.nan], np.float32))[0] == 0x7FC0
 
 
-def test_config1_shape_and_pages():
-    w = I.config1()
+def test_tiny_fp32_shape_and_pages():
+    w = I.tiny_fp32()
     assert list(w.prefill_lens) == [17, 64, 5, 120] and w.q.shape == (206, 8, 64)
     assert w.num_pages == 64
     used = w.page_table[w.page_table >= 0]
@@ -25,7 +25,7 @@ def test_config1_shape_and_pages():
 
 
 def test_generator_is_deterministic():
-    a, b = I.config1(), I.config1()
+    a, b = I.tiny_fp32(), I.tiny_fp32()
     assert np.array_equal(a.q, b.q) and np.array_equal(a.page_table, b.page_table)
     assert np.array_equal(a.steps[3][0], b.steps[3][0])
 

@@ -137,7 +137,7 @@ def chk_decode_brute():
 
 
 def chk_last_row_equals_decode():
-    w = I.config1(n_steps=0)
+    w = I.tiny_fp32(n_steps=0)
     out_p, lse_p = oracle.prefill(w.q, w.k, w.v, w.cu_seqlens, w.scale)
     kp, vp = oracle.kv_write(w.k, w.v, w.k_pool, w.v_pool, w.page_table, w.cu_seqlens,
                              np.zeros(4, np.int32))

@@ -175,8 +175,8 @@ def test_decode_invariant_under_page_permutation():
     assert np.array_equal(out1, out2) and np.array_equal(lse1, lse2)
 
 
-def test_config1_last_prefill_row_equals_decode_step():
-    w = I.config1()
+def test_tiny_fp32_last_prefill_row_equals_decode_step():
+    w = I.tiny_fp32()
     out_p, lse_p = oracle.prefill(w.q, w.k, w.v, w.cu_seqlens, w.scale)
     kp, vp = _write_prefill_into_pool(w)
     last = w.cu_seqlens[1:] - 1
@@ -185,10 +185,10 @@ def test_config1_last_prefill_row_equals_decode_step():
     np.testing.assert_allclose(lse_d, lse_p[last], rtol=0, atol=1e-13)
 
 
-def test_config1_decode_steps_equal_prefill_over_extended_sequence():
+def test_tiny_fp32_decode_steps_equal_prefill_over_extended_sequence():
     # Appending step tokens with kv_write and decoding must equal a prefill over
     # the prompt extended by those tokens (the row of the appended token).
-    w = I.config1()
+    w = I.tiny_fp32()
     kp, vp = _write_prefill_into_pool(w)
     n = len(w.prefill_lens)
     ones = I.cu_from_lens(np.ones(n, np.int32))
