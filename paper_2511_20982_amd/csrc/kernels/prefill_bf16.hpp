@@ -669,10 +669,16 @@ __device__ __forceinline__ void prefill_workgroup(const PrefillArgs& a, int bid,
     };
     auto even = [] { return 0; };
     auto odd = [] { return 1; };
+    // The dense kernel raises the wave's priority over its softmax and the
+    // next tile's QK products, so its VALU work issues first and the other
+    // workgroup's P.V MFMAs fill the slots it leaves (measured 1-2 % faster;
+    // the paged kernel measured slower with it).
     auto step_full = [&](f32x16* sc, f32x16* sn, auto par) {
       prefetch(j, par);
       if (wave_active) {
+        if constexpr (!PAGED) __builtin_amdgcn_s_setprio(1);
         half_qk(sc, sn, par() ^ 1);
+        if constexpr (!PAGED) __builtin_amdgcn_s_setprio(0);
         pv(par());
       }
       if (j + 1 < je) clear_dead_v(par() ^ 1, j + 1);
