@@ -126,6 +126,15 @@ dopd_status check_decode_host(const dopd_attn_shape* s, const int32_t* ctx_host,
   return DOPD_OK;
 }
 
+// How the decode's partials are merged: not at all (every (request, KV head)
+// is one segment), by the kernel over the listed (r, c) (count > 0), or by
+// the kernel that finds them itself (the list does not fit its arguments).
+struct DecodeMergePlan {
+  bool needed = false;
+  int count = 0;
+  dopd::DecodeMergeList list;
+};
+
 // Decode arguments and workspace layout of the bf16-operand decode (bf16 or
 // E4M3 pools) after the host checks; quarter_wgs: resident decode workgroups
 // per CU, in quarters, the automatic partition plans for.
@@ -135,7 +144,8 @@ dopd_status plan_decode_bf16(const dopd_attn_shape* s, const void* q, const void
                              const int32_t* pt, int32_t pt_stride, const int32_t* ctx,
                              const int32_t* ctx_host, int32_t nreq, int32_t split_tokens,
                              void* out, float* lse, void* workspace, size_t workspace_bytes,
-                             int quarter_wgs, dopd::DecodeArgs* a_out, bool* merge_out) {
+                             int quarter_wgs, dopd::DecodeArgs* a_out,
+                             DecodeMergePlan* merge_out) {
   const int hkv = s->num_kv_heads, hq = s->num_q_heads, d = s->head_dim;
   const int64_t total = dopd::decode_total_units(ctx_host, nreq, hkv);
   if (total > INT32_MAX / 2) return DOPD_ERR_INVALID_SHAPE;
@@ -146,7 +156,11 @@ dopd_status plan_decode_bf16(const dopd_attn_shape* s, const void* q, const void
   if (workspace_bytes < L.total) return DOPD_ERR_WORKSPACE_TOO_SMALL;
   if ((reinterpret_cast<uintptr_t>(workspace) & 255) != 0) return DOPD_ERR_INVALID_SHAPE;
   char* ws = static_cast<char*>(workspace);
-  *merge_out = dopd::decode_needs_merge(ctx_host, nreq, hkv, total, nwg);
+  merge_out->count = dopd::decode_merge_list(ctx_host, nreq, hkv, total, nwg,
+                                              merge_out->list.item, dopd::kMergeListMax);
+  merge_out->list.n = std::max(0, merge_out->count);
+  merge_out->needed = merge_out->count > 0 ||
+                      (merge_out->count < 0 && dopd::decode_needs_merge(ctx_host, nreq, hkv, total, nwg));
   dopd::DecodeArgs& a = *a_out;
   a.q = (const uint16_t*)q;
   a.k_pool = k_pool;
@@ -170,8 +184,19 @@ dopd_status plan_decode_bf16(const dopd_attn_shape* s, const void* q, const void
 }
 
 // The decode's second kernel: merges the (request, KV head) pairs whose keys
-// span several slices.
-dopd_status launch_decode_merge(const dopd::DecodeArgs& a, int d, hipStream_t strm) {
+// span several slices (nothing to launch when there are none).
+dopd_status launch_decode_merge(const dopd::DecodeArgs& a, const DecodeMergePlan& m, int d,
+                                hipStream_t strm) {
+  if (!m.needed) return DOPD_OK;
+  if (m.count > 0) {
+    if (d == 64)
+      hipLaunchKernelGGL(dopd::decode_merge_list_kernel<64>, dim3((unsigned)m.count), dim3(256), 0,
+                         strm, a, m.list);
+    else
+      hipLaunchKernelGGL(dopd::decode_merge_list_kernel<128>, dim3((unsigned)m.count), dim3(256), 0,
+                         strm, a, m.list);
+    return launch_status();
+  }
   const unsigned items = (unsigned)((int64_t)a.nreq * a.hkv);
   if (d == 64)
     hipLaunchKernelGGL(dopd::decode_merge_kernel<64>, dim3(items), dim3(256), 0, strm, a);
@@ -191,7 +216,7 @@ dopd_status launch_decode_bf16(const dopd_attn_shape* s, const void* q, const vo
                                void* out, float* lse, void* workspace, size_t workspace_bytes,
                                hipStream_t strm) {
   dopd::DecodeArgs a;
-  bool merge = false;
+  DecodeMergePlan merge;
   const dopd_status pst = plan_decode_bf16<KV8>(s, q, k_pool, v_pool, k_scale, v_scale, pt,
                                                 pt_stride, ctx, ctx_host, nreq, split_tokens,
                                                 out, lse, workspace, workspace_bytes,
@@ -202,8 +227,8 @@ dopd_status launch_decode_bf16(const dopd_attn_shape* s, const void* q, const vo
   else
     hipLaunchKernelGGL((dopd::decode_split_kernel<128, KV8>), dim3((unsigned)a.nwg), dim3(256), 0, strm, a);
   const dopd_status st = launch_status();
-  if (st != DOPD_OK || !merge) return st;
-  return launch_decode_merge(a, s->head_dim, strm);
+  if (st != DOPD_OK) return st;
+  return launch_decode_merge(a, merge, s->head_dim, strm);
 }
 
 }  // namespace
@@ -844,7 +869,7 @@ static dopd_status pd_step_impl(const dopd_attn_shape* s, const void* q_dec,
   const int hkv = s->num_kv_heads, d = s->head_dim;
   dopd::PdStepArgs p;
   std::memset(&p, 0, sizeof(p));
-  bool merge = false;
+  DecodeMergePlan merge;
   if (num_dec > 0) {
     st = kv8 ? plan_decode_bf16<true>(s, q_dec, k_pool, v_pool, k_scale, v_scale, dec_page_table,
                                       pt_stride, ctx, ctx_host, num_dec, 0, out_dec, lse_dec,
@@ -902,8 +927,8 @@ static dopd_status pd_step_impl(const dopd_attn_shape* s, const void* q_dec,
     else hipLaunchKernelGGL((dopd::pd_step_kernel<128, false>), grid, block, 0, strm, p);
   }
   st = launch_status();
-  if (st != DOPD_OK || !merge) return st;
-  return launch_decode_merge(p.dec, d, strm);
+  if (st != DOPD_OK) return st;
+  return launch_decode_merge(p.dec, merge, d, strm);
 }
 
 dopd_status dopd_pd_step(const dopd_attn_shape* s, const void* q_dec,

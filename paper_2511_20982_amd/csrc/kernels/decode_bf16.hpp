@@ -387,23 +387,13 @@ __global__ __launch_bounds__(256, 2) void decode_split_kernel(DecodeArgs a) {
   decode_workgroup<D, KV8>(a, (int)blockIdx.x, s_ml, s_o[0], s_o[1], s_o[2]);
 }
 
-// Merges the partials of every (r, c) whose pairs span more than one slice.
-// Workgroup = one (r, c); thread = one 4-dim chunk of one query head.
+// The merge of the (r, c) whose pairs span more than one slice: the partials
+// of (r, c) from slices b0 .. b1 (slot b + r * Hkv + c) are folded in slice
+// order into the output; thread = one 4-dim chunk of one query head.
 template <int D>
-__global__ __launch_bounds__(256) void decode_merge_kernel(DecodeArgs a) {
-  const int tid = threadIdx.x, l = lane_id();
+__device__ __forceinline__ void decode_merge_pair(const DecodeArgs& a, int r, int c, int b0, int b1) {
+  const int tid = threadIdx.x;
   const int hq = a.hq, hkv = a.hkv, g = hq / hkv;
-  const int r = blockIdx.x / hkv, c = blockIdx.x % hkv;
-  const int np = (a.ctx_lens[r] + 31) / 32;
-  int base = 0;  // first work unit of request r
-  for (int r0 = 0; r0 < r; r0 += 64) {
-    const int rr = r0 + l;
-    const int v = rr < r ? (kDecSegCost + (a.ctx_lens[rr] + 31) / 32) * hkv : 0;
-    base += __shfl(wave_inclusive_scan(v), 63, 64);
-  }
-  const int first = base + c * (kDecSegCost + np) + kDecSegCost;  // unit of the first pair
-  const int b0 = dec_slice_of(a, first), b1 = dec_slice_of(a, first + np - 1);
-  if (b0 == b1) return;  // one segment: written directly
   const int64_t rc = (int64_t)r * hkv + c;
   const int chunks = g * (D / 4);
   for (int ch = tid; ch < chunks; ch += 256) {
@@ -443,6 +433,44 @@ __global__ __launch_bounds__(256) void decode_merge_kernel(DecodeArgs a) {
     *reinterpret_cast<u32x2*>(op) = wv;
     if (a.lse && e0 == 0) a.lse[(int64_t)r * hq + c * g + hh] = (M + __log2f(L)) * kLn2;
   }
+}
+
+// Workgroup = one (r, c); it finds the slices of its first and last pair
+// itself (a scan over the context lengths) and returns when they are one.
+template <int D>
+__global__ __launch_bounds__(256) void decode_merge_kernel(DecodeArgs a) {
+  const int l = lane_id();
+  const int hkv = a.hkv;
+  const int r = blockIdx.x / hkv, c = blockIdx.x % hkv;
+  const int np = (a.ctx_lens[r] + 31) / 32;
+  int base = 0;  // first work unit of request r
+  for (int r0 = 0; r0 < r; r0 += 64) {
+    const int rr = r0 + l;
+    const int v = rr < r ? (kDecSegCost + (a.ctx_lens[rr] + 31) / 32) * hkv : 0;
+    base += __shfl(wave_inclusive_scan(v), 63, 64);
+  }
+  const int first = base + c * (kDecSegCost + np) + kDecSegCost;  // unit of the first pair
+  const int b0 = dec_slice_of(a, first), b1 = dec_slice_of(a, first + np - 1);
+  if (b0 == b1) return;  // one segment: written directly
+  decode_merge_pair<D>(a, r, c, b0, b1);
+}
+
+// The (r, c) to merge as the host listed them (decode_merge_list): workgroup
+// = one list item, whose (r, c) and slices come from the kernel arguments, so
+// the merge starts with the loads of the partials.
+constexpr int kMergeListMax = 768;
+struct DecodeMergeList {
+  int n;
+  uint32_t item[kMergeListMax];
+};
+
+template <int D>
+__global__ __launch_bounds__(256) void decode_merge_list_kernel(DecodeArgs a, DecodeMergeList m) {
+  const uint32_t it = m.item[blockIdx.x];
+  const int rc = (int)(it & ((1u << kMergeRcBits) - 1));
+  const int b0 = (int)((it >> kMergeRcBits) & ((1u << kMergeB0Bits) - 1));
+  const int b1 = b0 + (int)(it >> (kMergeRcBits + kMergeB0Bits));
+  decode_merge_pair<D>(a, rc / a.hkv, rc % a.hkv, b0, b1);
 }
 
 }  // namespace dopd

@@ -107,6 +107,35 @@ inline bool decode_needs_merge(const int32_t* ctx, int32_t n, int hkv, int64_t t
   return false;
 }
 
+// The (r, c) whose pairs span several slices (the ones the merge kernel
+// combines), listed for the merge kernel's arguments: item = r * Hkv + c
+// | b0 << 14 | (b1 - b0) << 24, with b0 and b1 the slices of its first and
+// last pair, in (r, c) order.  Returns the count, or -1 when the list would
+// not fit that packing (more than 2^14 (r, c), 2^10 workgroups, a span of
+// more than 255 slices) or more than max items (the caller then merges with
+// the kernel that finds its pairs itself).
+constexpr int kMergeRcBits = 14, kMergeB0Bits = 10;
+
+inline int decode_merge_list(const int32_t* ctx, int32_t n, int hkv, int64_t total, int64_t nwg,
+                             uint32_t* items, int max) {
+  if ((int64_t)n * hkv > (1 << kMergeRcBits) || nwg > (1 << kMergeB0Bits)) return -1;
+  int cnt = 0;
+  int64_t base = 0;
+  for (int32_t r = 0; r < n; ++r) {
+    const int64_t np = (ctx[r] + 31) / 32, span = kDecSegCost + np;
+    for (int c = 0; c < hkv; ++c) {
+      const int64_t first = base + c * span + kDecSegCost;  // unit of the first pair
+      const int64_t b0 = dec_slice_of(first, total, nwg), b1 = dec_slice_of(first + np - 1, total, nwg);
+      if (b0 == b1) continue;
+      if (cnt == max || b1 - b0 > 255) return -1;
+      items[cnt++] = (uint32_t)((int64_t)r * hkv + c) | (uint32_t)b0 << kMergeRcBits |
+                     (uint32_t)(b1 - b0) << (kMergeRcBits + kMergeB0Bits);
+    }
+    base += span * hkv;
+  }
+  return cnt;
+}
+
 // ---- prefill work order ----------------------------------------------------
 // With the XCD-aware order the work list of n_items items is dealt to the
 // XCDs in contiguous slices of per_xcd items; the hardware dispatcher sends

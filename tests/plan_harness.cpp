@@ -74,6 +74,36 @@ static int check_decode(const std::vector<int32_t>& ctx, int hkv, int split, int
       if (pairs_seen[(size_t)r * hkv + c] != (ctx[r] + 31) / 32) return fail("pairs not covered once", r, c);
   if (merge != decode_needs_merge(ctx.data(), n, hkv, total, nwg))
     return fail("merge decision", merge, nwg);
+  // the merge list: exactly the (r, c) with a partial segment, in (r, c)
+  // order, with the slices of their first and last pairs
+  std::vector<uint32_t> want;
+  bool fits = (int64_t)n * hkv <= (1 << kMergeRcBits) && nwg <= (1 << kMergeB0Bits);
+  for (int r = 0; r < n && fits; ++r)
+    for (int c = 0; c < hkv; ++c) {
+      const int64_t np = (ctx[r] + 31) / 32;
+      const int64_t first = span_start[r] + c * (kDecSegCost + np) + kDecSegCost;
+      const int64_t b0 = dec_slice_of(first, total, nwg), b1 = dec_slice_of(first + np - 1, total, nwg);
+      bool split = false;  // from the segment walk: some slice holds only part of (r, c)
+      for (int64_t b = b0; b <= b1; ++b)
+        if (partial_slots.count(b + (int64_t)r * hkv + c)) split = true;
+      if (split != (b0 != b1)) return fail("split pair vs slices", r, c);
+      if (!split) continue;
+      if (b1 - b0 > 255) fits = false;
+      want.push_back((uint32_t)(r * hkv + c) | (uint32_t)b0 << kMergeRcBits |
+                     (uint32_t)(b1 - b0) << (kMergeRcBits + kMergeB0Bits));
+    }
+  std::vector<uint32_t> got(want.size() + 1);
+  const int cnt = decode_merge_list(ctx.data(), n, hkv, total, nwg, got.data(), (int)got.size());
+  if (!fits) {
+    if (cnt != -1) return fail("merge list should not fit", cnt, nwg);
+  } else {
+    if (cnt != (int)want.size()) return fail("merge list count", cnt, (long)want.size());
+    for (size_t i = 0; i < want.size(); ++i)
+      if (got[i] != want[i]) return fail("merge list item", (long)i, (long)got[i]);
+    if (!want.empty() && decode_merge_list(ctx.data(), n, hkv, total, nwg, got.data(),
+                                           (int)want.size() - 1) != -1)
+      return fail("merge list past its capacity", (long)want.size(), 0);
+  }
   return 0;
 }
 
