@@ -54,9 +54,10 @@ KERNEL_SOURCES = ("paper_2511_20982_amd/csrc/dopd_attn.hip",
                   "paper_2511_20982_amd/csrc/kernels/kv_pack.hpp",
                   "paper_2511_20982_amd/csrc/kernels/kv_unpack.hpp")
 # Kernels behind each timed call (the decode call is a split kernel plus, when
-# some context exceeds one split, a merge kernel; a chunk call with key splits
-# adds the prefill merge kernel).
-CALL_KERNELS = {"decode": ("decode_split_kernel", "decode_merge_kernel"),
+# some (request, KV head) spans two slices, one of the two merge kernels; a
+# chunk call with key splits adds the prefill merge kernel).
+CALL_KERNELS = {"decode": ("decode_split_kernel", "decode_merge_list_kernel",
+                           "decode_merge_kernel"),
                 "prefill": ("prefill_bf16_kernel<128, false, false>",
                             "prefill_bf16_kernel<64, false, false>"),
                 "prefill_chunked": ("prefill_bf16_kernel<128, true, false>",
@@ -68,7 +69,8 @@ CALL_KERNELS = {"decode": ("decode_split_kernel", "decode_merge_kernel"),
                 "kv_write": ("kv_write_kernel",), "kv_write_fp8": ("kv_write_e4m3_kernel",),
                 "plain_copy": ("bitwise_not_kernel",),
                 "pack": ("kv_pack_kernel",), "unpack": ("kv_unpack_kernel",),
-                "pd_step": ("pd_step_kernel", "decode_merge_kernel"),
+                "pd_step": ("pd_step_kernel", "decode_merge_list_kernel",
+                            "decode_merge_kernel"),
                 "kv_write_pack": ("kv_write_pack_kernel",)}
 
 WORKLOADS = {
